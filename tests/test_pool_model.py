@@ -1,0 +1,125 @@
+"""Pins for the oracle's pool/session model (CPU only).
+
+The model is fixed by a hand-worked trace of the documented policy, by the
+invariants the paper states (write-on-evict writes an unmodified page to the
+cold tier at most once, Sec. III; KV never changes once written, Sec. II) and
+by conservation properties checked on random call sequences.
+"""
+
+import copy
+
+import numpy as np
+import pytest
+
+from oracle.pool_model import (ACTIVE, ERR_INVALID, ERR_NO_COLD, ERR_NO_HOT, ERR_STATE, PAUSED,
+                               ModelError, PoolModel)
+
+
+def test_hand_worked_trace():
+    m = PoolModel(num_hot=8, num_cold=6, max_sessions=3, max_pages_per_session=4)
+    a = m.create(40)                 # 3 pages: lowest free hot ids
+    b = m.create(16)                 # 1 page
+    assert (a, b) == (0, 1)
+    assert m.row(a) == [0, 1, 2, -1] and m.row(b) == [3, -1, -1, -1]
+    copies = m.evict(a)              # all 3 pages dirty -> cold 0,1,2
+    assert copies == [(0, 0), (1, 1), (2, 2)] and m.cold_writes == 3
+    assert m.row(a) == [-1] * 4 and m.free_hot() == 7
+    c = m.create(33)                 # reuses hot 0,1,2 (lowest)
+    assert c == 2 and m.row(c) == [0, 1, 2, -1]
+    res = m.resume([a])              # needs 3 hot pages: 4,5,6
+    assert res == [[(0, 4), (1, 5), (2, 6)]] and m.row(a) == [4, 5, 6, -1]
+    assert m.evict(a) == [] and m.cold_writes == 3      # clean: nothing written
+    m.resume([a])
+    m.write_tokens(a, 20, 1)         # token 20 lives in page 1 -> its cold copy dropped
+    assert m.sessions[a].cold == [0, -1, 2]
+    assert m.evict(a) == [(5, 1)] and m.cold_writes == 4  # page 1 rewritten into cold id 1
+
+
+def test_exhaustion_leaves_state_unchanged():
+    m = PoolModel(num_hot=4, num_cold=2, max_sessions=4, max_pages_per_session=4)
+    a = m.create(48)
+    before = copy.deepcopy(m.__dict__)
+    with pytest.raises(ModelError) as e:
+        m.create(33)
+    assert e.value.code == ERR_NO_HOT and m.__dict__ == before
+    with pytest.raises(ModelError) as e:
+        m.evict(a)                   # 3 dirty pages, 2 cold pages
+    assert e.value.code == ERR_NO_COLD and m.__dict__ == before
+    with pytest.raises(ModelError) as e:
+        m.resume([a])
+    assert e.value.code == ERR_STATE and m.__dict__ == before
+    with pytest.raises(ModelError) as e:
+        m.create(16 * 5)             # longer than a row
+    assert e.value.code == ERR_INVALID and m.__dict__ == before
+
+
+def test_batched_resume_is_atomic_and_ordered():
+    m = PoolModel(num_hot=10, num_cold=10, max_sessions=4, max_pages_per_session=4)
+    a, b = m.create(32), m.create(48)
+    m.evict(a), m.evict(b)
+    x = m.create(64)                 # takes hot 0..3, leaves 6 free
+    before = copy.deepcopy(m.__dict__)
+    m2 = copy.deepcopy(m)
+    with pytest.raises(ModelError):
+        m2.resume([a, b, x])         # x is active -> whole batch refused
+    assert m2.__dict__ == before
+    res = m.resume([b, a])           # b first: 3 lowest, then a: next 2
+    assert res[0] == [(2, 4), (3, 5), (4, 6)] and res[1] == [(0, 7), (1, 8)]
+
+
+def test_write_on_evict_at_most_once_per_page():
+    """Paper Sec. III: an unmodified page is written to the cold tier once,
+    however many times its session is evicted and resumed."""
+    m = PoolModel(num_hot=64, num_cold=64, max_sessions=4, max_pages_per_session=16)
+    sid = m.create(16 * 7 + 3)       # 8 pages
+    for _ in range(5):
+        m.evict(sid)
+        m.resume([sid])
+    assert m.cold_writes == 8
+
+
+def test_random_sequences_conserve_pages():
+    rng = np.random.default_rng(0)
+    nh, nc, ms, stride = 40, 30, 6, 8
+    m = PoolModel(nh, nc, ms, stride)
+    for step in range(3000):
+        op = rng.integers(0, 6)
+        sid = int(rng.integers(0, ms))
+        before = copy.deepcopy(m.__dict__)
+        try:
+            if op == 0:
+                m.create(int(rng.integers(0, 16 * stride + 1)))
+            elif op == 1:
+                m.evict(sid)
+            elif op == 2:
+                k = int(rng.integers(1, 3))
+                m.resume([int(x) for x in rng.choice(ms, size=k, replace=False)])
+            elif op == 3:
+                s = m.sessions[sid]
+                if s.state == ACTIVE and s.seq_len:
+                    t0 = int(rng.integers(0, s.seq_len))
+                    m.write_tokens(sid, t0, int(rng.integers(0, s.seq_len - t0 + 1)))
+            elif op == 4:
+                m.destroy(sid)
+            else:
+                n = int(rng.integers(0, stride + 1))
+                m.import_cold(16 * n, rng.choice(nc, size=n, replace=False))
+        except ModelError:
+            assert m.__dict__ == before
+        # conservation and disjointness
+        hot_used = [p for s in m.sessions if s.state == ACTIVE for p in s.hot]
+        assert len(hot_used) == len(set(hot_used))
+        assert len(hot_used) + m.free_hot() == nh
+        assert set(hot_used).isdisjoint(m.hot_free)
+        refs = [0] * nc
+        for s in m.sessions:
+            for c in s.cold:
+                if c >= 0:
+                    refs[c] += 1
+        assert refs == m.cold_ref
+        assert all((refs[c] == 0) == (c in m.cold_free) for c in range(nc))
+        for s in m.sessions:
+            if s.state == PAUSED:
+                assert all(c >= 0 for c in s.cold)
+            if s.state == ACTIVE:
+                assert len(s.hot) == (s.seq_len + 15) // 16 == len(s.cold)
