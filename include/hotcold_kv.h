@@ -1,0 +1,331 @@
+/*
+ * hotcold_kv.h — C ABI of the hot-cold KV-cache hot path for AMD Instinct MI355X (gfx950).
+ *
+ * The paper ("Hot-Cold Tiering of HBM and High Bandwidth Flash for Agentic LLM
+ * Serving") splits the KV cache of agentic sessions into a hot set, the KV of
+ * sessions that are decoding and that every decode step reads (Sec. I; Sec. II,
+ * "Agentic AI Serving"), and a cold pool, the KV of paused sessions, read only
+ * when a session resumes.  The hot set lives in the fast tier; the cold pool in
+ * a capacity tier (Sec. III, first paragraph).  This library implements the
+ * data-parallel part of that hierarchy on one GPU:
+ *
+ *   - decode attention over every active session's hot pages   (data path 1)
+ *   - resume: gather a paused session's pages into free hot pages and
+ *     rewrite its page table                                     (data path 2)
+ *   - writing fresh KV into hot pages                            (data path 3)
+ *   - eviction with write-on-evict                               (data path 4)
+ *
+ * (Data paths 1-4: Sec. III, "Architecture and data paths".)
+ *
+ * The cold tier is a second page pool in device memory standing in for the
+ * flash tier, or, optionally, a pool in pinned host memory read over PCIe.
+ *
+ * ---------------------------------------------------------------------------
+ * Page layout
+ * ---------------------------------------------------------------------------
+ * KV is stored in pages of KV_PAGE_TOKENS = 16 tokens (paged KV cache, Sec. II;
+ * 16 tokens x 96 KiB per token = the paper's 1.5 MiB block, Sec. IV).  Hot and
+ * cold pools use the same page format and separate int32 page-id spaces.  One
+ * page holds, for every layer and KV head, a K tile and a V tile:
+ *
+ *   page    = [num_layers][num_kv_heads][2 (K tile, V tile)][tile]
+ *   tile    = KV_PAGE_TOKENS * head_dim elements
+ *   K tile  : element (token t, dim d) at index ((d / x) * 16 + t) * x + d % x,
+ *             x = 16 bytes / element size (8 for bf16, 4 for float32):
+ *             16-byte groups of x consecutive dims, token-minor.
+ *   V tile  : element (t, d) at index d * 16 + t (dims-major, token-minor).
+ *
+ * page_bytes = num_layers * num_kv_heads * 2 * 16 * head_dim * element size
+ * (1.5 MiB for 48 layers x 4 KV heads x 128 dims x bf16).
+ *
+ * A page table is int32 [rows][stride]; row r, entry i is the hot page holding
+ * tokens 16 i .. 16 i + 15 of that row's session, -1 when unused.
+ *
+ * ---------------------------------------------------------------------------
+ * Conventions
+ * ---------------------------------------------------------------------------
+ *  - Every call returns a status code (KV_OK or a negative KV_ERR_*).  No C++
+ *    exception crosses this boundary.  kv_last_error() gives a message for the
+ *    calling thread's last failure.
+ *  - All buffers are owned by the caller and must outlive the pool.  The
+ *    library owns only host bookkeeping, a small pinned staging ring and a
+ *    small device buffer for copy lists.
+ *  - Device work is enqueued on the caller's stream (kv_stream_t is a
+ *    hipStream_t; NULL is the default stream) and the call returns without
+ *    waiting for it.  Asynchronous device faults surface at the caller's next
+ *    synchronisation.
+ *  - A failing call changes nothing: no bookkeeping, no page table, no pages.
+ *  - A pool is externally synchronised: one thread at a time.  Work on one
+ *    stream is ordered; across streams the caller orders it with events, with
+ *    one exception the pool handles itself: hot pages freed by an eviction or
+ *    a destroy are not handed out to a call on another stream before the
+ *    freeing call's device work has finished.
+ */
+#ifndef HOTCOLD_KV_H
+#define HOTCOLD_KV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KV_PAGE_TOKENS 16
+
+enum kv_status {
+    KV_OK = 0,
+    KV_ERR_INVALID = -1,        /* bad argument, descriptor, id or size */
+    KV_ERR_STATE = -2,          /* session in the wrong state for the call */
+    KV_ERR_NO_HOT_PAGES = -3,   /* hot pool has too few free pages */
+    KV_ERR_NO_COLD_PAGES = -4,  /* cold pool has too few free pages */
+    KV_ERR_HIP = -5,            /* a HIP runtime call failed (message has detail) */
+    KV_ERR_OOM = -6             /* the library's own small allocations failed */
+};
+
+enum kv_dtype { KV_DTYPE_BF16 = 0, KV_DTYPE_F32 = 1 };
+
+enum kv_cold_location {
+    KV_COLD_DEVICE = 0,         /* cold pool in device memory (stands in for flash) */
+    KV_COLD_PINNED_HOST = 1     /* cold pool in pinned host memory, read over PCIe */
+};
+
+enum kv_session_state { KV_SESSION_FREE = 0, KV_SESSION_ACTIVE = 1, KV_SESSION_PAUSED = 2 };
+
+/* kv_pool_desc.flags */
+#define KV_POOL_METADATA_ONLY 1  /* bookkeeping only: no buffers, no device work */
+
+/* Kernel ids for the profiling hook. */
+enum kv_kernel_id {
+    KV_KERNEL_DECODE_SPLIT = 0,   /* split-K paged decode attention */
+    KV_KERNEL_DECODE_COMBINE = 1, /* combine of split partials */
+    KV_KERNEL_PAGE_COPY = 2,      /* resume gather / evict scatter */
+    KV_KERNEL_COUNT = 3
+};
+
+typedef void* kv_stream_t;
+typedef struct kv_pool kv_pool;
+
+typedef struct kv_pool_desc {
+    int32_t num_layers;            /* >= 1 */
+    int32_t num_kv_heads;          /* 1 .. 16 */
+    int32_t head_dim;              /* 64 or 128 */
+    int32_t page_size;             /* must be KV_PAGE_TOKENS */
+    int32_t dtype;                 /* enum kv_dtype */
+    int32_t num_hot_pages;         /* >= 0 */
+    int32_t num_cold_pages;        /* >= 0 */
+    int32_t cold_location;         /* enum kv_cold_location */
+    int32_t max_sessions;          /* rows of the pool's page table */
+    int32_t max_pages_per_session; /* row stride of the pool's page table */
+    int32_t device;                /* HIP device ordinal holding the pools */
+    int32_t flags;                 /* KV_POOL_METADATA_ONLY or 0 */
+} kv_pool_desc;
+
+typedef struct kv_pool_stats {
+    int32_t free_hot_pages;
+    int32_t free_cold_pages;
+    int32_t active_sessions;
+    int32_t paused_sessions;
+    int64_t pages_to_cold;   /* pages written to the cold tier (write-on-evict) */
+    int64_t pages_to_hot;    /* pages copied cold -> hot by resumes */
+    int64_t bytes_to_cold;
+    int64_t bytes_to_hot;
+    int64_t resumes;         /* sessions resumed */
+    int64_t evicts;          /* sessions evicted */
+} kv_pool_stats;
+
+/* ----------------------------------------------------------------------- */
+/* Pool                                                                     */
+/* ----------------------------------------------------------------------- */
+
+/* Bytes of one page for this descriptor's layout (0 if the descriptor is invalid). */
+size_t kv_page_bytes(const kv_pool_desc* desc);
+
+/*
+ * Create a pool over caller-owned memory.
+ *   hot_base/hot_bytes   device memory, >= num_hot_pages * page_bytes, 256-byte aligned
+ *   cold_base/cold_bytes device memory (KV_COLD_DEVICE) or pinned host memory
+ *                        (KV_COLD_PINNED_HOST), >= num_cold_pages * page_bytes
+ *   page_table           device int32 [max_sessions][max_pages_per_session]; the pool
+ *                        fills it with -1 on `stream` and owns its contents afterwards
+ * With KV_POOL_METADATA_ONLY all pointers may be NULL and no device is touched.
+ * Hot and cold pages are handed out lowest id first (the paper leaves the
+ * choice open; lowest-first makes page tables predictable).
+ * Errors: KV_ERR_INVALID (descriptor or sizes), KV_ERR_HIP, KV_ERR_OOM.
+ */
+int kv_pool_create(const kv_pool_desc* desc, void* hot_base, size_t hot_bytes, void* cold_base,
+                   size_t cold_bytes, int32_t* page_table, kv_stream_t stream, kv_pool** out);
+
+/* Free host bookkeeping.  The caller must have synchronised streams using the pool. */
+void kv_pool_destroy(kv_pool* pool);
+
+int kv_pool_stats_get(const kv_pool* pool, kv_pool_stats* out);
+
+/* ----------------------------------------------------------------------- */
+/* Sessions                                                                 */
+/* ----------------------------------------------------------------------- */
+
+/*
+ * Create an ACTIVE session of seq_len tokens (a stand-in for prefill, which is
+ * outside this library): allocates ceil(seq_len / 16) hot pages and writes the
+ * session's page-table row.  hot_pages (host array, nullable) picks the exact
+ * pages, which must be free and distinct; NULL takes the lowest free ones.
+ * The page contents are left as they are: fill them with kv_write_tokens or
+ * kv_fill_synthetic.  The new session id (lowest free row) goes to *sid_out.
+ * Errors: KV_ERR_INVALID, KV_ERR_NO_HOT_PAGES.
+ */
+int kv_session_create(kv_pool* pool, int32_t seq_len, const int32_t* hot_pages,
+                      kv_stream_t stream, int32_t* sid_out);
+
+/*
+ * Register a PAUSED session of seq_len tokens whose KV already sits in the given
+ * cold pages (host array of ceil(seq_len / 16) distinct ids).  Cold pages may be
+ * shared with other paused sessions: KV never changes once written (Sec. II), so
+ * a virtualised cold pool may alias them; they are reference counted.
+ * Errors: KV_ERR_INVALID.
+ */
+int kv_session_import_cold(kv_pool* pool, int32_t seq_len, const int32_t* cold_pages,
+                           int32_t* sid_out);
+
+/* Release a session: its hot pages return to the free set (see the cross-stream
+ * rule above), its cold references are dropped and its row is reset to -1. */
+int kv_session_destroy(kv_pool* pool, int32_t sid, kv_stream_t stream);
+
+/*
+ * Describe a session.  Host outputs (any may be NULL): state, seq_len, and up to
+ * `cap` entries each of its hot page ids (logical page order; empty unless
+ * ACTIVE) and cold page ids (-1 where the page has no valid cold copy).
+ */
+int kv_session_info(const kv_pool* pool, int32_t sid, int32_t* state, int32_t* seq_len,
+                    int32_t* hot_pages, int32_t* cold_pages, int32_t cap);
+
+/*
+ * Fresh KV into the hot tier (data path 3, Sec. III): write tokens
+ * [tok_begin, tok_begin + n_tok) of an ACTIVE session for one layer.  k and v
+ * are device arrays [n_tok][num_kv_heads][head_dim] of the pool's dtype.  Pages
+ * written to lose their cold copy, so the next eviction writes them again.
+ * Errors: KV_ERR_INVALID (range beyond seq_len, bad layer), KV_ERR_STATE.
+ */
+int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin, int32_t n_tok,
+                    const void* k, const void* v, kv_stream_t stream);
+
+/*
+ * Test and benchmark input: fill every slot of an ACTIVE session's pages, all
+ * layers, with counter-based pseudo-normal values.  Element (kind, layer, head,
+ * token, dim) of logical session gen_sid gets value(seed, coordinate) computed
+ * with SplitMix64 (Steele, Lea and Flood 2014): h = mix(mix(seed) ^ c) with c
+ * the packed coordinate (kind:2 | gen_sid:20 | layer:6 | head:5 | token:23 |
+ * dim:8, kind 0 = K, 1 = V); s = sum of the four 16-bit fields of h - 131070;
+ * value = float32(s) * value_mult, then rounded to bf16 (nearest-even) for bf16
+ * pools.  Pages lose their cold copy.
+ */
+int kv_fill_synthetic(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed,
+                      float value_mult, kv_stream_t stream);
+
+/*
+ * Evict an ACTIVE session to the cold tier (data path 4) with write-on-evict
+ * (Sec. III, "Memory hierarchy and write policy"): only pages without a valid
+ * cold copy are copied, each into the lowest free cold page; pages that already
+ * have one cost no write, so an unmodified page reaches the cold tier at most
+ * once.  Then the session's hot pages are freed and its row set to -1; the
+ * session becomes PAUSED.
+ * Errors: KV_ERR_STATE (not ACTIVE), KV_ERR_NO_COLD_PAGES (nothing changes).
+ */
+int kv_evict_session(kv_pool* pool, int32_t sid, kv_stream_t stream);
+
+/*
+ * Resume a PAUSED session (data path 2; Sec. III, "Eviction, resume and
+ * decode": the KV is brought back into the fast tier before the session runs).
+ * Takes ceil(seq_len / 16) free hot pages, lowest ids first in logical page
+ * order, copies every page cold -> hot (whole pages, byte for byte) and writes
+ * the page-table row.  The cold copies stay valid.  One kernel launch.
+ * Errors: KV_ERR_STATE (not PAUSED), KV_ERR_NO_HOT_PAGES (nothing changes).
+ */
+int kv_resume_session(kv_pool* pool, int32_t sid, kv_stream_t stream);
+
+/* Batched resume: sessions in argument order, atomic as a whole, one launch. */
+int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t stream);
+
+/* ----------------------------------------------------------------------- */
+/* Decode attention (data path 1)                                           */
+/* ----------------------------------------------------------------------- */
+
+/*
+ * Number of waves the decode kernel splits the work over for this pool
+ * (a persistent grid sized to the GPU), or the value set below.
+ */
+int32_t paged_decode_waves(const kv_pool* pool);
+
+/* Override the number of decode waves (>= 1); 0 restores the automatic choice. */
+int kv_pool_set_decode_waves(kv_pool* pool, int32_t waves);
+
+/* Device workspace bytes paged_decode_attention needs for this batch. */
+size_t paged_decode_workspace_bytes(const kv_pool* pool, int32_t batch, int32_t num_q_heads);
+
+/*
+ * Paged grouped-query decode attention for one layer.  Decoding attends to the
+ * cached KV of all past tokens (Sec. II) and reads the whole hot set every step
+ * (Sec. III, data path 1).  For batch row b with L = seq_lens[b] and query head
+ * h (KV head g = h / (num_q_heads / num_kv_heads)):
+ *
+ *     out[b][h] = sum_t softmax_t(scale * q[b][h] . k_t) v_t,  t = 0 .. L-1,
+ *
+ * with token t in page page_table[b * pt_stride + t / 16], slot t % 16.
+ *
+ *   q          device [batch][num_q_heads][head_dim], pool dtype
+ *   page_table device int32, row b used for batch row b; may be the pool's own
+ *              table (row = session id) or any gathered copy of rows
+ *   seq_lens   device int32 [batch]; L = 0 writes zeros; L < 0 or
+ *              L > 16 * pt_stride writes NaN for that row (no memory is read
+ *              out of bounds); so does a page id outside the hot pool
+ *   out        device [batch][num_q_heads][head_dim], pool dtype (bf16 rounded
+ *              to nearest-even), written in full
+ *   workspace  device, >= paged_decode_workspace_bytes(), 256-byte aligned
+ * Only tokens [0, L) are read: other slots of the tail page and pages past
+ * ceil(L / 16) may hold anything, NaN included.
+ * Numerics: bf16 or float32 inputs, float32 accumulation, scores and weights in
+ * float32 (bf16 pools round the softmax weights to bf16 for the weighted sum of
+ * V and use the same rounded weights in the normaliser).  The result does not
+ * depend on where pages sit in the pool.
+ * num_q_heads / num_kv_heads must be an integer in 1 .. 16.
+ * Errors: KV_ERR_INVALID (shapes, sizes, layer, metadata-only pool), KV_ERR_HIP.
+ */
+int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const int32_t* page_table,
+                           int64_t pt_stride, const int32_t* seq_lens, int32_t batch,
+                           int32_t num_q_heads, float scale, void* out, void* workspace,
+                           size_t ws_bytes, kv_stream_t stream);
+
+/*
+ * The work split of paged_decode_attention, written out (device int32
+ * [waves + batch * num_kv_heads][4]).  A unit is one page of one (row b, KV
+ * head g); units are ordered by (b, g, page); wave k of `waves` takes units
+ * [floor(k T / waves), floor((k + 1) T / waves)) of the T units; where a wave
+ * meets the units of (b, g) it makes one partial result, stored in slot
+ * k + b * num_kv_heads + g as (b, g, first page, end page).  Unused slots hold
+ * (-1, -1, 0, 0).  The split is not the paper's: it is how this library
+ * balances sessions of different lengths over the GPU.
+ */
+int paged_decode_partition(kv_pool* pool, const int32_t* seq_lens, int32_t batch, int32_t waves,
+                           int32_t* slots_out, kv_stream_t stream);
+
+/* ----------------------------------------------------------------------- */
+/* Diagnostics                                                              */
+/* ----------------------------------------------------------------------- */
+
+const char* kv_strerror(int status);
+const char* kv_last_error(void);
+
+/*
+ * Profiling hook.  When enabled, every kernel the pool launches is bracketed by
+ * HIP events on the launch stream.  kv_pool_profile_read waits for the recorded
+ * launches of one kernel id, returns their count and summed duration in
+ * milliseconds, and forgets them.
+ */
+int kv_pool_set_profiling(kv_pool* pool, int enable);
+int kv_pool_profile_read(kv_pool* pool, int32_t kernel_id, int32_t* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HOTCOLD_KV_H */

@@ -1,0 +1,465 @@
+// Split-K paged grouped-query decode attention for gfx950 (data path 1 of the
+// hot-cold hierarchy: every decode step reads the whole hot set).
+//
+// Work split.  A unit is one page (16 tokens) of one (row b, KV head g).  The
+// units of all rows are laid end to end and cut into `waves` equal ranges, one
+// per wave of a persistent grid, so long and short contexts balance exactly.
+// Where a wave's range meets the units of one (b, g) it produces a partial
+// result (running max m, weight sum l, unnormalised output o) for the group of
+// query heads sharing KV head g; the combine kernel merges the partials of each
+// (b, g) with the usual log-sum-exp rescaling.  Reduction order depends only on
+// seq_lens, never on page placement, so results are bitwise independent of
+// where pages sit in the pool.
+//
+// One wave processes one page of one KV head per step with matrix cores:
+//   scores  S^T[t][h] = K[t][:] . Q[h][:]   v_mfma_f32_16x16x32_bf16 (f32: 16x16x4)
+//           (16 tokens x 16 head slots; the group's heads fill the first slots)
+//   output  O^T[d][h] += V^T[d][t] P^T[t][h] v_mfma_f32_16x16x16_bf16 (f32: 16x16x4)
+// The score tile comes out of the first product in exactly the register layout
+// the second product takes for P (lane l: head l % 16, tokens 4 (l / 16) + r),
+// so the softmax needs no data movement besides two cross-lane max steps.
+// Each query-head group reads every K/V byte once (the GQA reuse).
+//
+// Memory.  K tiles are stored as 16-byte groups of dims, token-minor, so the
+// four 16-byte loads a lane issues for a K tile are each 1 KiB contiguous across
+// the wave; V tiles are stored dims-major, token-minor, so each lane's slice of
+// V^T for one 16-dim chunk is 8 contiguous bytes and a wave reads 512
+// contiguous bytes per load.  Pages are addressed through buffer resources
+// whose base is the page and whose size is its two tiles: an out-of-range page
+// id becomes a zero-sized resource, reads return 0 and the row is flagged NaN.
+// Each wave keeps a ring of page buffers in registers: while one page is
+// computed, the loads of the next ring - 1 pages are in flight.
+
+#include "device_common.h"
+#include "kernels.h"
+
+#include <math.h>
+
+namespace hck {
+namespace {
+
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9 family)
+
+template <int D, bool BF16>
+struct Shape {
+    static constexpr int kElt = BF16 ? 2 : 4;
+    static constexpr int kTile = kPageTokens * D * kElt;  // bytes of a K or V tile
+    static constexpr int kKLoads = kTile / 1024;          // 16-byte K loads per lane
+    static constexpr int kChunks = D / 16;                // 16-dim output chunks
+};
+
+template <bool BF16>
+struct VSlice;
+template <>
+struct VSlice<true> {
+    typedef u32x2 type;  // 4 bf16 tokens of one dim
+};
+template <>
+struct VSlice<false> {
+    typedef u32x4 type;  // 4 f32 tokens of one dim
+};
+
+template <int D, bool BF16>
+struct PageRegs {
+    u32x4 k[Shape<D, BF16>::kKLoads];
+    typename VSlice<BF16>::type v[Shape<D, BF16>::kChunks];
+};
+
+__device__ __forceinline__ float wave_max_4(float x) {
+    // max over lanes l, l^16, l^32, l^48 (the four token quarters of one head)
+    x = fmaxf(x, __shfl_xor(x, 16));
+    x = fmaxf(x, __shfl_xor(x, 32));
+    return x;
+}
+
+__device__ __forceinline__ float wave_sum_4(float x) {
+    x += __shfl_xor(x, 16);
+    x += __shfl_xor(x, 32);
+    return x;
+}
+
+template <int D, bool BF16>
+__device__ __forceinline__ void load_page(PageRegs<D, BF16>& r, const char* lh_base,
+                                          int64_t page_bytes, int pid, int num_pages, bool& bad,
+                                          unsigned koff, unsigned voff) {
+    using S = Shape<D, BF16>;
+    const bool ok = static_cast<unsigned>(pid) < static_cast<unsigned>(num_pages);
+    bad |= !ok;
+    const char* base = lh_base + static_cast<int64_t>(ok ? pid : 0) * page_bytes;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), static_cast<short>(0),
+                                          ok ? 2 * S::kTile : 0, kRsrcWord3);
+#pragma unroll
+    for (int i = 0; i < S::kKLoads; ++i)
+        r.k[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, koff + 1024u * i, 0, 0);
+#pragma unroll
+    for (int c = 0; c < S::kChunks; ++c) {
+        if constexpr (BF16)
+            r.v[c] = __builtin_amdgcn_raw_buffer_load_b64(rs, voff + S::kTile + 512u * c, 0, 0);
+        else
+            r.v[c] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + S::kTile + 1024u * c, 0, 0);
+    }
+}
+
+// S^T tile of one page: lane l gets scores of head l % 16 for tokens 4 (l / 16) + r.
+template <int D, bool BF16>
+__device__ __forceinline__ f32x4 page_scores(const PageRegs<D, BF16>& r,
+                                             const u32x4 (&q)[Shape<D, BF16>::kKLoads]) {
+    using S = Shape<D, BF16>;
+    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < S::kKLoads; ++i) {
+        if constexpr (BF16) {
+            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, r.k[i]),
+                                                        __builtin_bit_cast(bf16x8, q[i]), s, 0,
+                                                        0, 0);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                s = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, r.k[i][j]),
+                                                         __builtin_bit_cast(float, q[i][j]), s, 0,
+                                                         0, 0);
+        }
+    }
+    return s;
+}
+
+// Zero the V slice entries of tokens >= valid (this lane holds tokens 4 qg + j).
+template <int D, bool BF16>
+__device__ __forceinline__ void mask_v(PageRegs<D, BF16>& r, int valid, int qg) {
+    using S = Shape<D, BF16>;
+    const int t0 = 4 * qg;
+    if constexpr (BF16) {
+        const unsigned m0 = (t0 + 0 < valid ? 0x0000FFFFu : 0u) | (t0 + 1 < valid ? 0xFFFF0000u : 0u);
+        const unsigned m1 = (t0 + 2 < valid ? 0x0000FFFFu : 0u) | (t0 + 3 < valid ? 0xFFFF0000u : 0u);
+#pragma unroll
+        for (int c = 0; c < S::kChunks; ++c) {
+            r.v[c][0] &= m0;
+            r.v[c][1] &= m1;
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < S::kChunks; ++c)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (t0 + j >= valid) r.v[c][j] = 0u;
+    }
+}
+
+template <int D, bool BF16>
+struct SegmentState {
+    u32x4 q[Shape<D, BF16>::kKLoads];
+    f32x4 o[Shape<D, BF16>::kChunks];
+    float m;
+    float l;
+};
+
+// Online-softmax update and weighted V for one page with `valid` tokens (1..16).
+template <int D, bool BF16>
+__device__ __forceinline__ void compute_page(SegmentState<D, BF16>& st, PageRegs<D, BF16>& pg,
+                                             int valid, float scale_log2, int qg) {
+    using S = Shape<D, BF16>;
+    f32x4 s = page_scores<D, BF16>(pg, st.q);
+    if (valid < kPageTokens) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s[r] = (4 * qg + r < valid) ? s[r] : -INFINITY;
+        mask_v<D, BF16>(pg, valid, qg);
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        s[r] *= scale_log2;
+        mx = fmaxf(mx, s[r]);
+    }
+    mx = wave_max_4(mx);
+    const float m_new = fmaxf(st.m, mx);
+    // Rescale only when some head's running max grew; otherwise every factor
+    // would be exactly 1.
+    if (__builtin_amdgcn_ballot_w64(m_new > st.m)) {
+        const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
+        st.l *= alpha;
+#pragma unroll
+        for (int c = 0; c < S::kChunks; ++c) st.o[c] *= alpha;
+        st.m = m_new;
+    }
+    float p[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) p[r] = __builtin_amdgcn_exp2f(s[r] - st.m);
+    if constexpr (BF16) {
+        __bf16 pb[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            pb[r] = static_cast<__bf16>(p[r]);
+            st.l += static_cast<float>(pb[r]);
+        }
+        const s16x4 pv = {__builtin_bit_cast(short, pb[0]), __builtin_bit_cast(short, pb[1]),
+                          __builtin_bit_cast(short, pb[2]), __builtin_bit_cast(short, pb[3])};
+#pragma unroll
+        for (int c = 0; c < S::kChunks; ++c)
+            st.o[c] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, pg.v[c]),
+                                                                pv, st.o[c], 0, 0, 0);
+    } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) st.l += p[r];
+#pragma unroll
+        for (int c = 0; c < S::kChunks; ++c)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                st.o[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                    __builtin_bit_cast(float, pg.v[c][j]), p[j], st.o[c], 0, 0, 0);
+    }
+}
+
+__device__ __forceinline__ int load_ids(const int32_t* __restrict__ row, int first, int end,
+                                        int lane) {
+    const int i = first + lane;
+    return i < end ? row[i] : -1;
+}
+
+// Process pages [p0, p1) of row b, KV head g, and write the partial to its slot.
+// R page buffers form a ring: while one page is computed, the next R - 1 are
+// in flight.
+template <int D, bool BF16, int R>
+__device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_len, int lane) {
+    using S = Shape<D, BF16>;
+    const int h = lane & 15, qg = lane >> 4;
+    const bool hvalid = h < a.group;
+    SegmentState<D, BF16> st;
+    {
+        const char* qrow = static_cast<const char*>(a.q) +
+                           (static_cast<int64_t>(pc.b) * a.num_q_heads + pc.g * a.group +
+                            (hvalid ? h : 0)) * D * S::kElt;
+#pragma unroll
+        for (int i = 0; i < S::kKLoads; ++i)
+            st.q[i] = hvalid ? *reinterpret_cast<const u32x4*>(qrow + 16 * (4 * i + qg))
+                             : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int c = 0; c < S::kChunks; ++c) st.o[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    st.m = -INFINITY;
+    st.l = 0.f;
+    bool bad = false;
+
+    const int32_t* row = a.page_table + static_cast<int64_t>(pc.b) * a.pt_stride;
+    const char* lh_base = a.hot + a.layer_offset + static_cast<int64_t>(pc.g) * 2 * S::kTile;
+    const unsigned koff = 16u * lane;
+    const unsigned voff = BF16 ? (32u * (lane & 15) + 8u * qg) : (64u * (lane & 15) + 16u * qg);
+    // valid tokens of the row's last page (16 when full)
+    const int tail_valid = seq_len - kPageTokens * (nb - 1);
+
+    int ids_cur = load_ids(row, pc.p0, pc.p1, lane);
+    int ids_nxt = load_ids(row, pc.p0 + kWave, pc.p1, lane);
+    int cur_chunk = 0;
+    auto pid_at = [&](int i) -> int {
+        const int rel = i - pc.p0;
+        const int cc = rel >> 6;
+        if (cc != cur_chunk) {
+            ids_cur = ids_nxt;
+            cur_chunk = cc;
+            ids_nxt = load_ids(row, pc.p0 + kWave * (cc + 1), pc.p1, lane);
+        }
+        return __builtin_amdgcn_readlane(ids_cur, rel & 63);
+    };
+
+    PageRegs<D, BF16> buf[R];
+#pragma unroll
+    for (int r = 0; r < R - 1; ++r)
+        if (pc.p0 + r < pc.p1)
+            load_page<D, BF16>(buf[r], lh_base, a.page_bytes, pid_at(pc.p0 + r), a.num_pages, bad,
+                               koff, voff);
+    for (int i = pc.p0; i < pc.p1; i += R) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int ip = i + r;
+            if (ip < pc.p1) {
+                const int ahead = ip + R - 1;
+                if (ahead < pc.p1)
+                    load_page<D, BF16>(buf[(r + R - 1) % R], lh_base, a.page_bytes, pid_at(ahead),
+                                       a.num_pages, bad, koff, voff);
+                compute_page<D, BF16>(st, buf[r], ip == nb - 1 ? tail_valid : kPageTokens,
+                                      a.scale_log2, qg);
+            }
+        }
+    }
+
+    float l = wave_sum_4(st.l);
+    if (bad) l = __builtin_nanf("");
+    if (hvalid) {
+        float* po = a.part_o + (static_cast<int64_t>(pc.slot) * a.group + h) * D + 4 * qg;
+#pragma unroll
+        for (int c = 0; c < S::kChunks; ++c) *reinterpret_cast<f32x4*>(po + 16 * c) = st.o[c];
+        if (qg == 0) {
+            float* pml = a.part_ml + static_cast<int64_t>(pc.slot) * 2 * a.group;
+            pml[h] = st.m;
+            pml[a.group + h] = l;
+        }
+    }
+}
+
+template <int D, bool BF16, int R>
+__global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs a) {
+    extern __shared__ int32_t s_pref[];
+    block_prefix_pages(a.seq_lens, a.batch, a.pt_stride, s_pref);
+    __syncthreads();
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kBlockWaves + threadIdx.x / kWave);
+    if (wave >= a.waves) return;
+    const int64_t total = static_cast<int64_t>(lds_uniform(s_pref + a.batch)) * a.num_kv_heads;
+    int64_t u, u1;
+    wave_units(total, wave, a.waves, u, u1);
+    while (u < u1) {
+        const Piece pc = piece_at(s_pref, a.batch, a.num_kv_heads, wave, u, u1);
+        if (pc.p1 <= pc.p0) break;  // cannot happen for a consistent prefix; never spin
+        const int nb = lds_uniform(s_pref + pc.b + 1) - lds_uniform(s_pref + pc.b);
+        const int32_t L = a.seq_lens[pc.b];
+        const int seq_len = L < kPageTokens * nb ? L : kPageTokens * nb;
+        run_piece<D, BF16, R>(a, pc, nb, seq_len, lane);
+        u += pc.p1 - pc.p0;
+    }
+}
+
+// Merge the partials of one (b, g) and write the group's output rows.
+template <int D, bool BF16>
+__global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArgs a) {
+    __shared__ int64_t s_red[2][kBlockWaves];
+    const int seg = blockIdx.x;
+    const int b = seg / a.num_kv_heads, g = seg % a.num_kv_heads;
+    const int tid = threadIdx.x;
+    int64_t before = 0, total = 0;
+    for (int r = tid; r < a.batch; r += kBlockThreads) {
+        const int n = row_pages(a.seq_lens[r], a.pt_stride);
+        total += n;
+        if (r < b) before += n;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        before += __shfl_xor(before, o);
+        total += __shfl_xor(total, o);
+    }
+    if ((tid & (kWave - 1)) == 0) {
+        s_red[0][tid / kWave] = before;
+        s_red[1][tid / kWave] = total;
+    }
+    __syncthreads();
+    before = s_red[0][0] + s_red[0][1] + s_red[0][2] + s_red[0][3];
+    total = s_red[1][0] + s_red[1][1] + s_red[1][2] + s_red[1][3];
+
+    const int32_t L = a.seq_lens[b];
+    const bool invalid = L < 0 || static_cast<int64_t>(L) > kPageTokens * a.pt_stride;
+    const int nb = row_pages(L, a.pt_stride);
+    const int64_t T = total * a.num_kv_heads;
+    const int64_t u_a = before * a.num_kv_heads + static_cast<int64_t>(g) * nb;
+    const int64_t u_e = u_a + nb;
+    const int N = a.waves;
+    int k_first = 0, k_last = -1;
+    if (!invalid && nb > 0) {
+        k_first = static_cast<int>(((u_a + 1) * N - 1) / T);
+        k_last = static_cast<int>((u_e * N - 1) / T);
+    }
+    constexpr int kQuads = D / 4;
+    for (int idx = tid; idx < a.group * kQuads; idx += kBlockThreads) {
+        const int h = idx / kQuads, d4 = 4 * (idx % kQuads);
+        f32x4 res;
+        if (invalid) {
+            const float nan = __builtin_nanf("");
+            res = f32x4{nan, nan, nan, nan};
+        } else if (nb == 0) {
+            res = f32x4{0.f, 0.f, 0.f, 0.f};
+        } else {
+            float M = -INFINITY, den = 0.f;
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int k = k_first; k <= k_last; ++k) {
+                if (static_cast<int64_t>(k) * T / N == static_cast<int64_t>(k + 1) * T / N) continue;
+                const int64_t slot = static_cast<int64_t>(k) + seg;
+                const float* pml = a.part_ml + slot * 2 * a.group;
+                const float mk = pml[h], lk = pml[a.group + h];
+                const f32x4 ok =
+                    *reinterpret_cast<const f32x4*>(a.part_o + (slot * a.group + h) * D + d4);
+                const float Mn = fmaxf(M, mk);
+                const float c_old = __builtin_amdgcn_exp2f(M - Mn);
+                const float c_new = __builtin_amdgcn_exp2f(mk - Mn);
+                acc = acc * c_old + ok * c_new;
+                den = den * c_old + lk * c_new;
+                M = Mn;
+            }
+            res = acc / den;
+        }
+        const int64_t orow = (static_cast<int64_t>(b) * a.num_q_heads + g * a.group + h) * D + d4;
+        if constexpr (BF16) {
+            __bf16* o = static_cast<__bf16*>(a.out) + orow;
+            __bf16 v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = static_cast<__bf16>(res[j]);
+            *reinterpret_cast<u32x2*>(o) = __builtin_bit_cast(u32x2, v);
+        } else {
+            *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + orow) = res;
+        }
+    }
+}
+
+// Ring depth per shape: the deepest ring that still leaves two (or three)
+// waves per SIMD, i.e. at most 256 (168) VGPRs.
+template <int D, bool BF16>
+constexpr int ring_depth() {
+    return BF16 ? (D == 128 ? 3 : 5) : (D == 128 ? 2 : 3);
+}
+
+template <int D, bool BF16>
+const void* split_kernel_ptr() {
+    return reinterpret_cast<const void*>(&decode_split_kernel<D, BF16, ring_depth<D, BF16>()>);
+}
+
+const void* pick_split(int head_dim, int dtype) {
+    if (dtype == kDtypeBf16) {
+        if (head_dim == 128) return split_kernel_ptr<128, true>();
+        if (head_dim == 64) return split_kernel_ptr<64, true>();
+    } else {
+        if (head_dim == 128) return split_kernel_ptr<128, false>();
+        if (head_dim == 64) return split_kernel_ptr<64, false>();
+    }
+    return nullptr;
+}
+
+const void* pick_combine(int head_dim, int dtype) {
+    if (dtype == kDtypeBf16) {
+        if (head_dim == 128) return reinterpret_cast<const void*>(&decode_combine_kernel<128, true>);
+        if (head_dim == 64) return reinterpret_cast<const void*>(&decode_combine_kernel<64, true>);
+    } else {
+        if (head_dim == 128) return reinterpret_cast<const void*>(&decode_combine_kernel<128, false>);
+        if (head_dim == 64) return reinterpret_cast<const void*>(&decode_combine_kernel<64, false>);
+    }
+    return nullptr;
+}
+
+size_t prefix_lds_bytes(int batch) { return static_cast<size_t>(batch + 1) * sizeof(int32_t); }
+
+}  // namespace
+
+hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s) {
+    const void* k = pick_split(head_dim, dtype);
+    if (!k || a.waves <= 0) return hipErrorInvalidValue;
+    const int blocks = (a.waves + kBlockWaves - 1) / kBlockWaves;
+    void* args[] = {const_cast<DecodeArgs*>(&a)};
+    return hipLaunchKernel(k, dim3(blocks), dim3(kBlockThreads), args, prefix_lds_bytes(a.batch), s);
+}
+
+hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s) {
+    const void* k = pick_combine(head_dim, dtype);
+    if (!k) return hipErrorInvalidValue;
+    const int blocks = a.batch * a.num_kv_heads;
+    if (blocks == 0) return hipSuccess;
+    void* args[] = {const_cast<DecodeArgs*>(&a)};
+    return hipLaunchKernel(k, dim3(blocks), dim3(kBlockThreads), args, 0, s);
+}
+
+int decode_split_blocks_per_cu(int head_dim, int dtype, int batch) {
+    const void* k = pick_split(head_dim, dtype);
+    if (!k) return 0;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kBlockThreads, prefix_lds_bytes(batch)) !=
+        hipSuccess)
+        return 0;
+    return n;
+}
+
+}  // namespace hck

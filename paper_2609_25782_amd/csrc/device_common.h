@@ -1,0 +1,102 @@
+// Device-side helpers shared by the library's kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hck {
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kPageTokens = 16;
+constexpr int kWave = 64;
+constexpr int kBlockThreads = 256;
+constexpr int kBlockWaves = kBlockThreads / kWave;
+
+// Pages a row of `seq_len` tokens occupies, clamped to the row stride; rows
+// with a non-positive length occupy none.
+__device__ __forceinline__ int row_pages(int32_t seq_len, int64_t stride) {
+    if (seq_len <= 0) return 0;
+    const int64_t n = (static_cast<int64_t>(seq_len) + kPageTokens - 1) / kPageTokens;
+    return static_cast<int>(n < stride ? n : stride);
+}
+
+// s_pref[b] = sum of row_pages over rows < b, for b = 0 .. batch (exclusive
+// prefix sum plus the total).  All 256 threads of the block must call it; the
+// caller synchronises before reading s_pref.
+__device__ inline void block_prefix_pages(const int32_t* __restrict__ seq_lens, int batch,
+                                          int64_t stride, int32_t* s_pref) {
+    __shared__ int32_t s_wave_sum[kBlockWaves];
+    const int tid = threadIdx.x;
+    const int per = (batch + kBlockThreads - 1) / kBlockThreads;
+    const int lo = min(batch, tid * per);
+    const int hi = min(batch, lo + per);
+    int sum = 0;
+    for (int b = lo; b < hi; ++b) sum += row_pages(seq_lens[b], stride);
+    int x = sum;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if ((tid & (kWave - 1)) >= o) x += y;
+    }
+    if ((tid & (kWave - 1)) == kWave - 1) s_wave_sum[tid / kWave] = x;
+    __syncthreads();
+    int base = 0;
+    for (int w = 0; w < tid / kWave; ++w) base += s_wave_sum[w];
+    int run = base + x - sum;
+    for (int b = lo; b < hi; ++b) {
+        s_pref[b] = run;
+        run += row_pages(seq_lens[b], stride);
+    }
+    if (tid == kBlockThreads - 1) s_pref[batch] = run;
+}
+
+// One piece of the decode work split: wave `wave` handles pages [p0, p1) of
+// row b, KV head g; its partial result goes to slot wave + b * Hkv + g.
+struct Piece {
+    int b, g, p0, p1, slot;
+};
+
+// Wave-uniform read of an LDS word (all lanes read the same address); keeps
+// values derived from it in scalar registers.
+__device__ __forceinline__ int32_t lds_uniform(const int32_t* p) {
+    return __builtin_amdgcn_readfirstlane(*p);
+}
+
+// Units are (row, KV head, page) triples ordered by row, then head, then page;
+// wave k of `waves` owns units [floor(k T / waves), floor((k + 1) T / waves)).
+__device__ __forceinline__ void wave_units(int64_t total_units, int wave, int waves, int64_t& u0,
+                                           int64_t& u1) {
+    u0 = static_cast<int64_t>(wave) * total_units / waves;
+    u1 = static_cast<int64_t>(wave + 1) * total_units / waves;
+}
+
+// The piece that starts at unit u (< total), ending no later than u_end.
+__device__ __forceinline__ Piece piece_at(const int32_t* s_pref, int batch, int num_kv_heads,
+                                          int wave, int64_t u, int64_t u_end) {
+    // largest row b with Hkv * s_pref[b] <= u; it has at least one page
+    const int64_t target = u / num_kv_heads;
+    int lo = 0, hi = batch - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (lds_uniform(s_pref + mid) <= target) lo = mid; else hi = mid - 1;
+    }
+    Piece pc;
+    pc.b = lo;
+    const int32_t first = lds_uniform(s_pref + lo);
+    const int nb = lds_uniform(s_pref + lo + 1) - first;
+    const int64_t rel = u - static_cast<int64_t>(first) * num_kv_heads;
+    pc.g = static_cast<int>(rel / nb);
+    pc.p0 = static_cast<int>(rel % nb);
+    const int64_t seg_end = u + (nb - pc.p0);
+    const int64_t e = seg_end < u_end ? seg_end : u_end;
+    pc.p1 = pc.p0 + static_cast<int>(e - u);
+    pc.slot = wave + lo * num_kv_heads + pc.g;
+    return pc;
+}
+
+}  // namespace hck

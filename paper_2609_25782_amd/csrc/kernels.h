@@ -1,0 +1,88 @@
+// Host-side launchers for the library's HIP kernels (internal interface).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hck {
+
+enum { kDtypeBf16 = 0, kDtypeF32 = 1 };
+
+// Waves per 256-thread block of the decode kernel.
+constexpr int kBlockWavesHost = 4;
+
+// Everything the split-K decode kernel and its combine read.
+struct DecodeArgs {
+    const char* hot;          // hot pool base
+    int64_t page_bytes;       // bytes per page
+    int64_t layer_offset;     // byte offset of the layer inside a page
+    int32_t num_pages;        // hot pages; ids outside [0, num_pages) are rejected
+    int32_t num_kv_heads;
+    int32_t group;            // query heads per KV head (1..16)
+    int32_t num_q_heads;
+    const void* q;            // [batch][num_q_heads][head_dim]
+    const int32_t* page_table;
+    int64_t pt_stride;
+    const int32_t* seq_lens;  // [batch]
+    int32_t batch;
+    int32_t waves;            // number of waves the work is split over
+    float scale_log2;         // softmax scale * log2(e)
+    float* part_o;            // [slots][group][head_dim] unnormalised partial outputs
+    float* part_ml;           // [slots][2][group] running max (log2 domain) and weight sum
+    void* out;                // [batch][num_q_heads][head_dim]
+};
+
+// Bytes of partial results for `slots` slots.
+inline size_t decode_partials_bytes(int64_t slots, int group, int head_dim) {
+    return static_cast<size_t>(slots) * group * (head_dim + 2) * sizeof(float);
+}
+
+hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s);
+hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s);
+// Resident 256-thread blocks per CU of the split kernel (0 if unsupported shape).
+int decode_split_blocks_per_cu(int head_dim, int dtype, int batch);
+
+// (waves + batch * num_kv_heads) records of 4 int32: (b, g, first page, end page).
+hipError_t launch_partition(const int32_t* seq_lens, int batch, int num_kv_heads, int waves,
+                            int64_t pt_stride, int32_t* slots, hipStream_t s);
+
+struct CopyEntry {
+    int32_t src;       // source page id
+    int32_t dst;       // destination page id
+    int32_t pt_index;  // page-table element to set to dst, or -1
+    int32_t pad;
+};
+
+// Copies whole pages src_base[e.src] -> dst_base[e.dst] for n entries (device
+// array) and writes page_table[e.pt_index] = e.dst where pt_index >= 0.
+hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_bytes,
+                            const CopyEntry* entries, int32_t n, int32_t* page_table,
+                            hipStream_t s);
+
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t s);
+
+struct SynthArgs {
+    char* hot;
+    int64_t page_bytes;
+    const int32_t* row;  // device page-table row of the session
+    int32_t num_pages;   // pages of the session
+    int32_t num_layers, num_kv_heads, head_dim, dtype;
+    int32_t gen_sid;
+    uint64_t seed;
+    float value_mult;
+};
+hipError_t launch_fill_synthetic(const SynthArgs& a, hipStream_t s);
+
+struct WriteArgs {
+    char* hot;
+    int64_t page_bytes;
+    const int32_t* row;  // device page-table row of the session
+    int32_t num_kv_heads, head_dim, dtype, layer;
+    int32_t tok_begin, n_tok;
+    const void* k;       // [n_tok][num_kv_heads][head_dim]
+    const void* v;
+};
+hipError_t launch_write_tokens(const WriteArgs& a, hipStream_t s);
+
+}  // namespace hck

@@ -1,0 +1,814 @@
+// Host runtime of the hot-cold KV library: pool bookkeeping, session state
+// machine, deterministic page allocation and the C ABI declared in hotcold_kv.h.
+//
+// Bookkeeping lives on the host.  Device work (page copies, page-table writes,
+// decode) is enqueued on the caller's stream through the launchers in
+// kernels.h.  Every call validates and plans first and commits its bookkeeping
+// only after its device work was enqueued, so a failing call changes nothing.
+
+#include "hotcold_kv.h"
+#include "kernels.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(KV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Free-page set with lowest-id-first allocation (a bitmap; bit set = free).
+class PageSet {
+  public:
+    void init(int32_t n) {
+        n_ = n;
+        free_ = n;
+        bits_.assign((static_cast<size_t>(n) + 63) / 64, ~0ull);
+        if (n % 64) bits_.back() = (1ull << (n % 64)) - 1;
+        hint_ = 0;
+    }
+    int32_t size() const { return n_; }
+    int32_t free_count() const { return free_; }
+    bool is_free(int32_t p) const { return (bits_[p >> 6] >> (p & 63)) & 1ull; }
+    void take(int32_t p) {
+        bits_[p >> 6] &= ~(1ull << (p & 63));
+        --free_;
+    }
+    void give(int32_t p) {
+        bits_[p >> 6] |= 1ull << (p & 63);
+        ++free_;
+        if (static_cast<size_t>(p >> 6) < hint_) hint_ = p >> 6;
+    }
+    // The k lowest free ids, ascending, without taking them.
+    void lowest(int32_t k, std::vector<int32_t>& out) {
+        out.clear();
+        out.reserve(k);
+        while (hint_ < bits_.size() && bits_[hint_] == 0) ++hint_;
+        for (size_t w = hint_; w < bits_.size() && static_cast<int32_t>(out.size()) < k; ++w) {
+            uint64_t x = bits_[w];
+            while (x && static_cast<int32_t>(out.size()) < k) {
+                const int b = __builtin_ctzll(x);
+                out.push_back(static_cast<int32_t>(w * 64 + b));
+                x &= x - 1;
+            }
+        }
+    }
+
+  private:
+    std::vector<uint64_t> bits_;
+    int32_t n_ = 0, free_ = 0;
+    size_t hint_ = 0;
+};
+
+struct Session {
+    int32_t state = KV_SESSION_FREE;
+    int32_t seq_len = 0;
+    std::vector<int32_t> hot;   // hot page per logical page (ACTIVE only)
+    std::vector<int32_t> cold;  // cold page per logical page, -1 = no valid copy
+};
+
+constexpr int kStagingSlots = 4;
+constexpr size_t kStagingBytes = size_t(1) << 20;
+constexpr int32_t kStagingEntries = static_cast<int32_t>(kStagingBytes / sizeof(hck::CopyEntry));
+constexpr int32_t kMaxDecodeBatch = 8192;
+
+struct StagingSlot {
+    void* host = nullptr;  // pinned
+    void* dev = nullptr;
+    hipEvent_t done = nullptr;
+    bool pending = false;
+};
+
+struct ProfRec {
+    hipEvent_t start, stop;
+};
+
+int32_t pages_of(int64_t seq_len) {
+    return static_cast<int32_t>((seq_len + KV_PAGE_TOKENS - 1) / KV_PAGE_TOKENS);
+}
+
+size_t elt_size(int32_t dtype) { return dtype == KV_DTYPE_BF16 ? 2 : 4; }
+
+size_t layout_page_bytes(const kv_pool_desc* d) {
+    return static_cast<size_t>(d->num_layers) * d->num_kv_heads * 2 * KV_PAGE_TOKENS * d->head_dim *
+           elt_size(d->dtype);
+}
+
+bool desc_valid(const kv_pool_desc* d) {
+    return d && d->num_layers >= 1 && d->num_layers <= 64 && d->num_kv_heads >= 1 &&
+           d->num_kv_heads <= 16 && (d->head_dim == 64 || d->head_dim == 128) &&
+           d->page_size == KV_PAGE_TOKENS &&
+           (d->dtype == KV_DTYPE_BF16 || d->dtype == KV_DTYPE_F32) && d->num_hot_pages >= 0 &&
+           d->num_cold_pages >= 0 &&
+           (d->cold_location == KV_COLD_DEVICE || d->cold_location == KV_COLD_PINNED_HOST) &&
+           d->max_sessions >= 1 && d->max_pages_per_session >= 1 &&
+           static_cast<int64_t>(d->max_sessions) * d->max_pages_per_session < (int64_t(1) << 31) &&
+           d->max_pages_per_session <= kStagingEntries;
+}
+
+class DeviceGuard {
+  public:
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev_) == hipSuccess && prev_ != dev) {
+            changed_ = hipSetDevice(dev) == hipSuccess;
+        }
+    }
+    ~DeviceGuard() {
+        if (changed_) (void)hipSetDevice(prev_);
+    }
+
+  private:
+    int prev_ = -1;
+    bool changed_ = false;
+};
+
+}  // namespace
+
+struct kv_pool {
+    kv_pool_desc d{};
+    bool meta = false;
+    char* hot = nullptr;
+    char* cold = nullptr;  // device-visible address of the cold pool
+    int32_t* pt = nullptr;
+    int64_t page_bytes = 0;
+    PageSet hot_free, cold_free;
+    std::vector<int32_t> cold_ref;
+    std::vector<Session> sessions;
+    kv_pool_stats st{};
+    int cus = 0;
+    int32_t waves_override = 0;
+    StagingSlot ring[kStagingSlots];
+    int ring_next = 0;
+    hipEvent_t free_event = nullptr;
+    bool free_pending = false;
+    bool profiling = false;
+    std::vector<ProfRec> prof[KV_KERNEL_COUNT];
+    std::vector<hipEvent_t> spare_events;
+
+    ~kv_pool() {
+        if (meta) return;
+        DeviceGuard g(d.device);
+        for (auto& s : ring) {
+            if (s.done) (void)hipEventSynchronize(s.done);
+            if (s.host) (void)hipHostFree(s.host);
+            if (s.dev) (void)hipFree(s.dev);
+            if (s.done) (void)hipEventDestroy(s.done);
+        }
+        if (free_event) (void)hipEventDestroy(free_event);
+        for (auto& v : prof)
+            for (auto& r : v) {
+                (void)hipEventDestroy(r.start);
+                (void)hipEventDestroy(r.stop);
+            }
+        for (auto e : spare_events) (void)hipEventDestroy(e);
+    }
+
+    hipStream_t strm(kv_stream_t s) const { return static_cast<hipStream_t>(s); }
+
+    // Make `stream` wait for device work of calls that freed hot pages.
+    int order_after_frees(hipStream_t s) {
+        if (!free_pending) return KV_OK;
+        hipError_t e = hipStreamWaitEvent(s, free_event, 0);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        return KV_OK;
+    }
+
+    int note_frees(hipStream_t s) {
+        hipError_t e = hipEventRecord(free_event, s);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+        free_pending = true;
+        return KV_OK;
+    }
+
+    int acquire_slot(StagingSlot** out) {
+        StagingSlot& s = ring[ring_next];
+        ring_next = (ring_next + 1) % kStagingSlots;
+        if (s.pending) {
+            hipError_t e = hipEventSynchronize(s.done);
+            if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(staging)");
+            s.pending = false;
+        }
+        *out = &s;
+        return KV_OK;
+    }
+
+    hipEvent_t take_event() {
+        if (!spare_events.empty()) {
+            hipEvent_t e = spare_events.back();
+            spare_events.pop_back();
+            return e;
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+
+    // Bracket a launch with profiling events when profiling is on.
+    hipEvent_t prof_begin(hipStream_t s) {
+        if (!profiling) return nullptr;
+        hipEvent_t e = take_event();
+        if (e) (void)hipEventRecord(e, s);
+        return e;
+    }
+    void prof_end(int kernel, hipEvent_t start, hipStream_t s) {
+        if (!start) return;
+        hipEvent_t e = take_event();
+        if (!e) return;
+        (void)hipEventRecord(e, s);
+        prof[kernel].push_back(ProfRec{start, e});
+    }
+
+    // Enqueue page copies (in chunks that fit a staging slot).
+    int submit_copies(const char* src, char* dst, const std::vector<hck::CopyEntry>& entries,
+                      hipStream_t s) {
+        for (size_t off = 0; off < entries.size(); off += kStagingEntries) {
+            const int32_t n = static_cast<int32_t>(
+                std::min<size_t>(kStagingEntries, entries.size() - off));
+            StagingSlot* slot;
+            int rc = acquire_slot(&slot);
+            if (rc) return rc;
+            std::memcpy(slot->host, entries.data() + off, n * sizeof(hck::CopyEntry));
+            hipError_t e = hipMemcpyAsync(slot->dev, slot->host, n * sizeof(hck::CopyEntry),
+                                          hipMemcpyHostToDevice, s);
+            if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(copy list)");
+            hipEvent_t p = prof_begin(s);
+            e = hck::launch_page_copy(src, dst, page_bytes,
+                                      static_cast<const hck::CopyEntry*>(slot->dev), n, pt, s);
+            prof_end(KV_KERNEL_PAGE_COPY, p, s);
+            if (e != hipSuccess) return hip_fail(e, "page copy launch");
+            e = hipEventRecord(slot->done, s);
+            if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
+            slot->pending = true;
+        }
+        return KV_OK;
+    }
+
+    // Write `n` page ids into page-table row `sid` (entries 0..n-1).
+    int submit_row(int32_t sid, const int32_t* vals, int32_t n, hipStream_t s) {
+        if (n <= 0) return KV_OK;
+        StagingSlot* slot;
+        int rc = acquire_slot(&slot);
+        if (rc) return rc;
+        std::memcpy(slot->host, vals, n * sizeof(int32_t));
+        hipError_t e = hipMemcpyAsync(pt + static_cast<int64_t>(sid) * d.max_pages_per_session,
+                                      slot->host, n * sizeof(int32_t), hipMemcpyHostToDevice, s);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(page-table row)");
+        e = hipEventRecord(slot->done, s);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
+        slot->pending = true;
+        return KV_OK;
+    }
+
+    int clear_row(int32_t sid, int32_t n, hipStream_t s) {
+        if (n <= 0) return KV_OK;
+        hipError_t e =
+            hck::launch_fill_i32(pt + static_cast<int64_t>(sid) * d.max_pages_per_session, n, -1, s);
+        if (e != hipSuccess) return hip_fail(e, "page-table clear");
+        return KV_OK;
+    }
+
+    int32_t new_sid() const {
+        for (int32_t i = 0; i < d.max_sessions; ++i)
+            if (sessions[i].state == KV_SESSION_FREE) return i;
+        return -1;
+    }
+
+    Session* session(int32_t sid) {
+        if (sid < 0 || sid >= d.max_sessions) return nullptr;
+        return &sessions[sid];
+    }
+
+    void release_cold(int32_t c) {
+        if (--cold_ref[c] == 0) cold_free.give(c);
+    }
+
+    int32_t auto_waves() const {
+        const int per_cu = hck::decode_split_blocks_per_cu(d.head_dim, d.dtype, 0);
+        const int32_t w = cus * std::max(1, per_cu) * hck::kBlockWavesHost;
+        return std::max<int32_t>(w, 1);
+    }
+    int32_t decode_waves() const { return waves_override > 0 ? waves_override : auto_waves(); }
+};
+
+extern "C" {
+
+size_t kv_page_bytes(const kv_pool_desc* desc) {
+    if (!desc_valid(desc)) return 0;
+    return layout_page_bytes(desc);
+}
+
+int kv_pool_create(const kv_pool_desc* desc, void* hot_base, size_t hot_bytes, void* cold_base,
+                   size_t cold_bytes, int32_t* page_table, kv_stream_t stream, kv_pool** out) {
+    if (!out) return fail(KV_ERR_INVALID, "out is NULL");
+    *out = nullptr;
+    if (!desc_valid(desc)) return fail(KV_ERR_INVALID, "invalid pool descriptor");
+    const bool meta = (desc->flags & KV_POOL_METADATA_ONLY) != 0;
+    const size_t pb = layout_page_bytes(desc);
+    if (!meta) {
+        if (desc->num_hot_pages > 0 && (!hot_base || hot_bytes < pb * desc->num_hot_pages))
+            return fail(KV_ERR_INVALID, "hot pool smaller than %d pages of %zu bytes",
+                        desc->num_hot_pages, pb);
+        if (desc->num_cold_pages > 0 && (!cold_base || cold_bytes < pb * desc->num_cold_pages))
+            return fail(KV_ERR_INVALID, "cold pool smaller than %d pages of %zu bytes",
+                        desc->num_cold_pages, pb);
+        if (!page_table) return fail(KV_ERR_INVALID, "page table is NULL");
+        if ((reinterpret_cast<uintptr_t>(hot_base) | reinterpret_cast<uintptr_t>(cold_base)) & 255)
+            return fail(KV_ERR_INVALID, "pools must be 256-byte aligned");
+    }
+    kv_pool* p = new (std::nothrow) kv_pool();
+    if (!p) return fail(KV_ERR_OOM, "out of host memory");
+    p->d = *desc;
+    p->meta = meta;
+    p->page_bytes = static_cast<int64_t>(pb);
+    p->hot_free.init(desc->num_hot_pages);
+    p->cold_free.init(desc->num_cold_pages);
+    p->cold_ref.assign(desc->num_cold_pages, 0);
+    p->sessions.assign(desc->max_sessions, Session());
+    if (!meta) {
+        DeviceGuard g(desc->device);
+        p->hot = static_cast<char*>(hot_base);
+        p->pt = page_table;
+        hipError_t e = hipSuccess;
+        if (desc->cold_location == KV_COLD_PINNED_HOST && cold_base) {
+            void* dp = nullptr;
+            e = hipHostGetDevicePointer(&dp, cold_base, 0);
+            if (e != hipSuccess) {
+                delete p;
+                return hip_fail(e, "hipHostGetDevicePointer(cold pool)");
+            }
+            p->cold = static_cast<char*>(dp);
+        } else {
+            p->cold = static_cast<char*>(cold_base);
+        }
+        e = hipDeviceGetAttribute(&p->cus, hipDeviceAttributeMultiprocessorCount, desc->device);
+        if (e != hipSuccess) {
+            delete p;
+            return hip_fail(e, "hipDeviceGetAttribute");
+        }
+        for (auto& s : p->ring) {
+            if (hipHostMalloc(&s.host, kStagingBytes, hipHostMallocDefault) != hipSuccess ||
+                hipMalloc(&s.dev, kStagingBytes) != hipSuccess ||
+                hipEventCreateWithFlags(&s.done, hipEventDisableTiming) != hipSuccess) {
+                delete p;
+                return fail(KV_ERR_OOM, "staging allocation failed");
+            }
+        }
+        if (hipEventCreateWithFlags(&p->free_event, hipEventDisableTiming) != hipSuccess) {
+            delete p;
+            return fail(KV_ERR_OOM, "event creation failed");
+        }
+        e = hck::launch_fill_i32(page_table,
+                                 static_cast<int64_t>(desc->max_sessions) * desc->max_pages_per_session,
+                                 -1, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) {
+            delete p;
+            return hip_fail(e, "page-table fill");
+        }
+    }
+    p->st.free_hot_pages = desc->num_hot_pages;
+    p->st.free_cold_pages = desc->num_cold_pages;
+    *out = p;
+    return KV_OK;
+}
+
+void kv_pool_destroy(kv_pool* pool) { delete pool; }
+
+int kv_pool_stats_get(const kv_pool* pool, kv_pool_stats* out) {
+    if (!pool || !out) return fail(KV_ERR_INVALID, "NULL argument");
+    *out = pool->st;
+    out->free_hot_pages = pool->hot_free.free_count();
+    out->free_cold_pages = pool->cold_free.free_count();
+    int32_t a = 0, p = 0;
+    for (const auto& s : pool->sessions) {
+        a += s.state == KV_SESSION_ACTIVE;
+        p += s.state == KV_SESSION_PAUSED;
+    }
+    out->active_sessions = a;
+    out->paused_sessions = p;
+    return KV_OK;
+}
+
+int kv_session_create(kv_pool* pool, int32_t seq_len, const int32_t* hot_pages, kv_stream_t stream,
+                      int32_t* sid_out) {
+    if (!pool || !sid_out) return fail(KV_ERR_INVALID, "NULL argument");
+    if (seq_len < 0) return fail(KV_ERR_INVALID, "negative length");
+    const int32_t n = pages_of(seq_len);
+    if (n > pool->d.max_pages_per_session)
+        return fail(KV_ERR_INVALID, "%d pages exceed the row stride %d", n,
+                    pool->d.max_pages_per_session);
+    std::vector<int32_t> pages;
+    if (hot_pages) {
+        pages.assign(hot_pages, hot_pages + n);
+        std::vector<int32_t> sorted = pages;
+        std::sort(sorted.begin(), sorted.end());
+        if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end())
+            return fail(KV_ERR_INVALID, "duplicate hot page");
+        for (int32_t p : pages)
+            if (p < 0 || p >= pool->d.num_hot_pages || !pool->hot_free.is_free(p))
+                return fail(KV_ERR_INVALID, "hot page %d is not free", p);
+    } else {
+        if (n > pool->hot_free.free_count())
+            return fail(KV_ERR_NO_HOT_PAGES, "need %d hot pages, %d free", n,
+                        pool->hot_free.free_count());
+        pool->hot_free.lowest(n, pages);
+    }
+    const int32_t sid = pool->new_sid();
+    if (sid < 0) return fail(KV_ERR_INVALID, "no free session slot");
+    if (!pool->meta && n > 0) {
+        DeviceGuard g(pool->d.device);
+        hipStream_t s = pool->strm(stream);
+        int rc = pool->order_after_frees(s);
+        if (!rc) rc = pool->submit_row(sid, pages.data(), n, s);
+        if (rc) return rc;
+    }
+    for (int32_t p : pages) pool->hot_free.take(p);
+    Session& ss = pool->sessions[sid];
+    ss.state = KV_SESSION_ACTIVE;
+    ss.seq_len = seq_len;
+    ss.hot = pages;
+    ss.cold.assign(n, -1);
+    *sid_out = sid;
+    return KV_OK;
+}
+
+int kv_session_import_cold(kv_pool* pool, int32_t seq_len, const int32_t* cold_pages,
+                           int32_t* sid_out) {
+    if (!pool || !sid_out || (seq_len > 0 && !cold_pages)) return fail(KV_ERR_INVALID, "NULL argument");
+    if (seq_len < 0) return fail(KV_ERR_INVALID, "negative length");
+    const int32_t n = pages_of(seq_len);
+    if (n > pool->d.max_pages_per_session) return fail(KV_ERR_INVALID, "too many pages");
+    std::vector<int32_t> pages(cold_pages, cold_pages + n);
+    std::vector<int32_t> sorted = pages;
+    std::sort(sorted.begin(), sorted.end());
+    if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end())
+        return fail(KV_ERR_INVALID, "duplicate cold page");
+    for (int32_t p : pages)
+        if (p < 0 || p >= pool->d.num_cold_pages) return fail(KV_ERR_INVALID, "bad cold page %d", p);
+    const int32_t sid = pool->new_sid();
+    if (sid < 0) return fail(KV_ERR_INVALID, "no free session slot");
+    for (int32_t p : pages) {
+        if (pool->cold_ref[p]++ == 0) pool->cold_free.take(p);
+    }
+    Session& ss = pool->sessions[sid];
+    ss.state = KV_SESSION_PAUSED;
+    ss.seq_len = seq_len;
+    ss.hot.clear();
+    ss.cold = pages;
+    *sid_out = sid;
+    return KV_OK;
+}
+
+int kv_session_destroy(kv_pool* pool, int32_t sid, kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    Session* s = pool->session(sid);
+    if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+    if (s->state == KV_SESSION_FREE) return fail(KV_ERR_STATE, "session %d is not in use", sid);
+    if (!pool->meta && s->state == KV_SESSION_ACTIVE && !s->hot.empty()) {
+        DeviceGuard g(pool->d.device);
+        hipStream_t st = pool->strm(stream);
+        int rc = pool->clear_row(sid, static_cast<int32_t>(s->hot.size()), st);
+        if (!rc) rc = pool->note_frees(st);
+        if (rc) return rc;
+    }
+    for (int32_t p : s->hot) pool->hot_free.give(p);
+    for (int32_t c : s->cold)
+        if (c >= 0) pool->release_cold(c);
+    *s = Session();
+    return KV_OK;
+}
+
+int kv_session_info(const kv_pool* pool, int32_t sid, int32_t* state, int32_t* seq_len,
+                    int32_t* hot_pages, int32_t* cold_pages, int32_t cap) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    if (sid < 0 || sid >= pool->d.max_sessions) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+    const Session& s = pool->sessions[sid];
+    if (state) *state = s.state;
+    if (seq_len) *seq_len = s.seq_len;
+    if (hot_pages)
+        for (int32_t i = 0; i < cap && i < static_cast<int32_t>(s.hot.size()); ++i) hot_pages[i] = s.hot[i];
+    if (cold_pages)
+        for (int32_t i = 0; i < cap && i < static_cast<int32_t>(s.cold.size()); ++i) cold_pages[i] = s.cold[i];
+    return KV_OK;
+}
+
+int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin, int32_t n_tok,
+                    const void* k, const void* v, kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    if (pool->meta) return fail(KV_ERR_INVALID, "metadata-only pool has no pages");
+    Session* s = pool->session(sid);
+    if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+    if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sid);
+    if (layer < 0 || layer >= pool->d.num_layers) return fail(KV_ERR_INVALID, "bad layer %d", layer);
+    if (tok_begin < 0 || n_tok < 0 || static_cast<int64_t>(tok_begin) + n_tok > s->seq_len)
+        return fail(KV_ERR_INVALID, "token range outside the session");
+    if (n_tok == 0) return KV_OK;
+    if (!k || !v) return fail(KV_ERR_INVALID, "NULL k or v");
+    DeviceGuard g(pool->d.device);
+    hck::WriteArgs a;
+    a.hot = pool->hot;
+    a.page_bytes = pool->page_bytes;
+    a.row = pool->pt + static_cast<int64_t>(sid) * pool->d.max_pages_per_session;
+    a.num_kv_heads = pool->d.num_kv_heads;
+    a.head_dim = pool->d.head_dim;
+    a.dtype = pool->d.dtype;
+    a.layer = layer;
+    a.tok_begin = tok_begin;
+    a.n_tok = n_tok;
+    a.k = k;
+    a.v = v;
+    hipError_t e = hck::launch_write_tokens(a, pool->strm(stream));
+    if (e != hipSuccess) return hip_fail(e, "write_tokens launch");
+    for (int32_t i = tok_begin / KV_PAGE_TOKENS; i <= (tok_begin + n_tok - 1) / KV_PAGE_TOKENS; ++i) {
+        if (s->cold[i] >= 0) {
+            pool->release_cold(s->cold[i]);
+            s->cold[i] = -1;
+        }
+    }
+    return KV_OK;
+}
+
+int kv_fill_synthetic(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed, float value_mult,
+                      kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    if (pool->meta) return fail(KV_ERR_INVALID, "metadata-only pool has no pages");
+    Session* s = pool->session(sid);
+    if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+    if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sid);
+    if (gen_sid < 0 || gen_sid >= (1 << 20)) return fail(KV_ERR_INVALID, "gen_sid out of range");
+    if (s->hot.empty()) return KV_OK;
+    DeviceGuard g(pool->d.device);
+    hck::SynthArgs a;
+    a.hot = pool->hot;
+    a.page_bytes = pool->page_bytes;
+    a.row = pool->pt + static_cast<int64_t>(sid) * pool->d.max_pages_per_session;
+    a.num_pages = static_cast<int32_t>(s->hot.size());
+    a.num_layers = pool->d.num_layers;
+    a.num_kv_heads = pool->d.num_kv_heads;
+    a.head_dim = pool->d.head_dim;
+    a.dtype = pool->d.dtype;
+    a.gen_sid = gen_sid;
+    a.seed = seed;
+    a.value_mult = value_mult;
+    hipError_t e = hck::launch_fill_synthetic(a, pool->strm(stream));
+    if (e != hipSuccess) return hip_fail(e, "fill_synthetic launch");
+    for (auto& c : s->cold)
+        if (c >= 0) {
+            pool->release_cold(c);
+            c = -1;
+        }
+    return KV_OK;
+}
+
+int kv_evict_session(kv_pool* pool, int32_t sid, kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    Session* s = pool->session(sid);
+    if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+    if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sid);
+    std::vector<int32_t> dirty;
+    for (size_t i = 0; i < s->cold.size(); ++i)
+        if (s->cold[i] < 0) dirty.push_back(static_cast<int32_t>(i));
+    if (static_cast<int32_t>(dirty.size()) > pool->cold_free.free_count())
+        return fail(KV_ERR_NO_COLD_PAGES, "need %zu cold pages, %d free", dirty.size(),
+                    pool->cold_free.free_count());
+    std::vector<int32_t> dst;
+    pool->cold_free.lowest(static_cast<int32_t>(dirty.size()), dst);
+    if (!pool->meta) {
+        DeviceGuard g(pool->d.device);
+        hipStream_t st = pool->strm(stream);
+        std::vector<hck::CopyEntry> entries(dirty.size());
+        for (size_t j = 0; j < dirty.size(); ++j)
+            entries[j] = hck::CopyEntry{s->hot[dirty[j]], dst[j], -1, 0};
+        int rc = pool->submit_copies(pool->hot, pool->cold, entries, st);
+        if (!rc) rc = pool->clear_row(sid, static_cast<int32_t>(s->hot.size()), st);
+        if (!rc) rc = pool->note_frees(st);
+        if (rc) return rc;
+    }
+    for (size_t j = 0; j < dirty.size(); ++j) {
+        pool->cold_free.take(dst[j]);
+        pool->cold_ref[dst[j]] = 1;
+        s->cold[dirty[j]] = dst[j];
+    }
+    for (int32_t p : s->hot) pool->hot_free.give(p);
+    s->hot.clear();
+    s->state = KV_SESSION_PAUSED;
+    pool->st.pages_to_cold += static_cast<int64_t>(dirty.size());
+    pool->st.bytes_to_cold += static_cast<int64_t>(dirty.size()) * pool->page_bytes;
+    pool->st.evicts += 1;
+    return KV_OK;
+}
+
+int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t stream) {
+    if (!pool || (n > 0 && !sids) || n < 0) return fail(KV_ERR_INVALID, "bad arguments");
+    if (n == 0) return KV_OK;
+    std::vector<int32_t> ids(sids, sids + n);
+    {
+        std::vector<int32_t> sorted = ids;
+        std::sort(sorted.begin(), sorted.end());
+        if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end())
+            return fail(KV_ERR_INVALID, "duplicate session in batch");
+    }
+    int64_t need = 0;
+    for (int32_t sid : ids) {
+        Session* s = pool->session(sid);
+        if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+        if (s->state != KV_SESSION_PAUSED) return fail(KV_ERR_STATE, "session %d is not paused", sid);
+        need += static_cast<int64_t>(s->cold.size());
+    }
+    if (need > pool->hot_free.free_count())
+        return fail(KV_ERR_NO_HOT_PAGES, "need %lld hot pages, %d free", static_cast<long long>(need),
+                    pool->hot_free.free_count());
+    std::vector<int32_t> dst;
+    pool->hot_free.lowest(static_cast<int32_t>(need), dst);
+    if (!pool->meta) {
+        DeviceGuard g(pool->d.device);
+        hipStream_t st = pool->strm(stream);
+        std::vector<hck::CopyEntry> entries;
+        entries.reserve(need);
+        size_t k = 0;
+        for (int32_t sid : ids) {
+            const Session& s = pool->sessions[sid];
+            const int32_t row = sid * pool->d.max_pages_per_session;
+            for (size_t i = 0; i < s.cold.size(); ++i, ++k)
+                entries.push_back(hck::CopyEntry{s.cold[i], dst[k], row + static_cast<int32_t>(i), 0});
+        }
+        int rc = pool->order_after_frees(st);
+        if (!rc) rc = pool->submit_copies(pool->cold, pool->hot, entries, st);
+        if (rc) return rc;
+    }
+    size_t k = 0;
+    for (int32_t sid : ids) {
+        Session& s = pool->sessions[sid];
+        s.hot.assign(dst.begin() + k, dst.begin() + k + s.cold.size());
+        for (int32_t p : s.hot) pool->hot_free.take(p);
+        k += s.cold.size();
+        s.state = KV_SESSION_ACTIVE;
+        pool->st.pages_to_hot += static_cast<int64_t>(s.hot.size());
+        pool->st.bytes_to_hot += static_cast<int64_t>(s.hot.size()) * pool->page_bytes;
+        pool->st.resumes += 1;
+    }
+    return KV_OK;
+}
+
+int kv_resume_session(kv_pool* pool, int32_t sid, kv_stream_t stream) {
+    return kv_resume_sessions(pool, &sid, 1, stream);
+}
+
+int32_t paged_decode_waves(const kv_pool* pool) {
+    if (!pool || pool->meta) return 0;
+    DeviceGuard g(pool->d.device);
+    return pool->decode_waves();
+}
+
+int kv_pool_set_decode_waves(kv_pool* pool, int32_t waves) {
+    if (!pool || waves < 0) return fail(KV_ERR_INVALID, "bad arguments");
+    pool->waves_override = waves;
+    return KV_OK;
+}
+
+size_t paged_decode_workspace_bytes(const kv_pool* pool, int32_t batch, int32_t num_q_heads) {
+    if (!pool || pool->meta || batch < 0 || num_q_heads <= 0 || num_q_heads % pool->d.num_kv_heads)
+        return 0;
+    const int32_t group = num_q_heads / pool->d.num_kv_heads;
+    DeviceGuard g(pool->d.device);
+    const int64_t slots = static_cast<int64_t>(pool->decode_waves()) +
+                          static_cast<int64_t>(batch) * pool->d.num_kv_heads;
+    return hck::decode_partials_bytes(slots, group, pool->d.head_dim);
+}
+
+int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const int32_t* page_table,
+                           int64_t pt_stride, const int32_t* seq_lens, int32_t batch,
+                           int32_t num_q_heads, float scale, void* out, void* workspace,
+                           size_t ws_bytes, kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    if (pool->meta) return fail(KV_ERR_INVALID, "metadata-only pool cannot decode");
+    if (layer < 0 || layer >= pool->d.num_layers) return fail(KV_ERR_INVALID, "bad layer %d", layer);
+    if (batch < 0 || batch > kMaxDecodeBatch)
+        return fail(KV_ERR_INVALID, "batch %d outside [0, %d]", batch, kMaxDecodeBatch);
+    if (batch == 0) return KV_OK;
+    if (!q || !page_table || !seq_lens || !out || !workspace) return fail(KV_ERR_INVALID, "NULL buffer");
+    if (num_q_heads <= 0 || num_q_heads % pool->d.num_kv_heads)
+        return fail(KV_ERR_INVALID, "query heads %d not a multiple of KV heads %d", num_q_heads,
+                    pool->d.num_kv_heads);
+    const int32_t group = num_q_heads / pool->d.num_kv_heads;
+    if (group > 16) return fail(KV_ERR_INVALID, "more than 16 query heads per KV head");
+    if (pt_stride < 1 || static_cast<int64_t>(batch) * pt_stride >= (int64_t(1) << 31))
+        return fail(KV_ERR_INVALID, "bad page-table stride");
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+        return fail(KV_ERR_INVALID, "workspace must be 256-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(out)) & 15)
+        return fail(KV_ERR_INVALID, "q and out must be 16-byte aligned");
+    DeviceGuard g(pool->d.device);
+    const int32_t waves = pool->decode_waves();
+    const int64_t slots = static_cast<int64_t>(waves) + static_cast<int64_t>(batch) * pool->d.num_kv_heads;
+    const size_t need = hck::decode_partials_bytes(slots, group, pool->d.head_dim);
+    if (ws_bytes < need) return fail(KV_ERR_INVALID, "workspace %zu bytes, need %zu", ws_bytes, need);
+    hck::DecodeArgs a;
+    a.hot = pool->hot;
+    a.page_bytes = pool->page_bytes;
+    a.layer_offset = static_cast<int64_t>(layer) * pool->d.num_kv_heads * 2 * KV_PAGE_TOKENS *
+                     pool->d.head_dim * static_cast<int64_t>(elt_size(pool->d.dtype));
+    a.num_pages = pool->d.num_hot_pages;
+    a.num_kv_heads = pool->d.num_kv_heads;
+    a.group = group;
+    a.num_q_heads = num_q_heads;
+    a.q = q;
+    a.page_table = page_table;
+    a.pt_stride = pt_stride;
+    a.seq_lens = seq_lens;
+    a.batch = batch;
+    a.waves = waves;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.part_o = static_cast<float*>(workspace);
+    a.part_ml = a.part_o + slots * group * pool->d.head_dim;
+    a.out = out;
+    hipStream_t st = pool->strm(stream);
+    hipEvent_t p = pool->prof_begin(st);
+    hipError_t e = hck::launch_decode_split(a, pool->d.head_dim, pool->d.dtype, st);
+    pool->prof_end(KV_KERNEL_DECODE_SPLIT, p, st);
+    if (e != hipSuccess) return hip_fail(e, "decode split launch");
+    p = pool->prof_begin(st);
+    e = hck::launch_decode_combine(a, pool->d.head_dim, pool->d.dtype, st);
+    pool->prof_end(KV_KERNEL_DECODE_COMBINE, p, st);
+    if (e != hipSuccess) return hip_fail(e, "decode combine launch");
+    return KV_OK;
+}
+
+int paged_decode_partition(kv_pool* pool, const int32_t* seq_lens, int32_t batch, int32_t waves,
+                           int32_t* slots_out, kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    if (pool->meta) return fail(KV_ERR_INVALID, "metadata-only pool");
+    if (batch < 0 || batch > kMaxDecodeBatch || waves < 1 || !slots_out || (batch > 0 && !seq_lens))
+        return fail(KV_ERR_INVALID, "bad arguments");
+    DeviceGuard g(pool->d.device);
+    hipError_t e = hck::launch_partition(seq_lens, batch, pool->d.num_kv_heads, waves,
+                                         pool->d.max_pages_per_session, slots_out,
+                                         pool->strm(stream));
+    if (e != hipSuccess) return hip_fail(e, "partition launch");
+    return KV_OK;
+}
+
+const char* kv_strerror(int status) {
+    switch (status) {
+        case KV_OK: return "ok";
+        case KV_ERR_INVALID: return "invalid argument";
+        case KV_ERR_STATE: return "session in the wrong state";
+        case KV_ERR_NO_HOT_PAGES: return "hot pool exhausted";
+        case KV_ERR_NO_COLD_PAGES: return "cold pool exhausted";
+        case KV_ERR_HIP: return "HIP runtime error";
+        case KV_ERR_OOM: return "out of memory";
+        default: return "unknown status";
+    }
+}
+
+const char* kv_last_error(void) { return g_err.c_str(); }
+
+int kv_pool_set_profiling(kv_pool* pool, int enable) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    if (pool->meta && enable) return fail(KV_ERR_INVALID, "metadata-only pool launches nothing");
+    pool->profiling = enable != 0;
+    return KV_OK;
+}
+
+int kv_pool_profile_read(kv_pool* pool, int32_t kernel_id, int32_t* launches, double* total_ms) {
+    if (!pool || kernel_id < 0 || kernel_id >= KV_KERNEL_COUNT) return fail(KV_ERR_INVALID, "bad arguments");
+    DeviceGuard g(pool->d.device);
+    double sum = 0.0;
+    int32_t count = 0;
+    int rc = KV_OK;
+    for (auto& r : pool->prof[kernel_id]) {
+        float ms = 0.f;
+        hipError_t e = hipEventSynchronize(r.stop);
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.start, r.stop);
+        if (e != hipSuccess && rc == KV_OK) rc = hip_fail(e, "profiling event");
+        sum += ms;
+        ++count;
+        pool->spare_events.push_back(r.start);
+        pool->spare_events.push_back(r.stop);
+    }
+    pool->prof[kernel_id].clear();
+    if (launches) *launches = count;
+    if (total_ms) *total_ms = sum;
+    return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,254 @@
+// Page movement and page-content kernels for gfx950.
+//
+//  - page_copy_kernel: whole-page copies between pools with an optional
+//    page-table write per page.  Resume (data path 2) gathers cold pages into
+//    free hot pages and rewrites the session's row in the same launch; eviction
+//    (data path 4) scatters the pages that have no valid cold copy.  The copy
+//    is byte for byte, 16-byte vector loads and stores, several loads in
+//    flight per thread before the first store.
+//  - fill kernels for page tables and for synthetic page contents.
+//  - write_tokens_kernel: fresh K/V into a session's hot pages (data path 3).
+//  - partition kernels: the decode work split written out as a table.
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace hck {
+namespace {
+
+constexpr int kCopyUnroll = 8;  // 16-byte loads in flight per thread
+constexpr int64_t kCopyChunk = static_cast<int64_t>(kBlockThreads) * kCopyUnroll * 16;
+
+__global__ __launch_bounds__(kBlockThreads) void page_copy_kernel(
+    const char* __restrict__ src_base, char* __restrict__ dst_base, int64_t page_bytes,
+    const CopyEntry* __restrict__ entries, int32_t n, int chunks_per_page,
+    int32_t* __restrict__ page_table) {
+    const int64_t flat = blockIdx.x;
+    const int ent = static_cast<int>(flat / chunks_per_page);
+    const int chunk = static_cast<int>(flat % chunks_per_page);
+    if (ent >= n) return;
+    const CopyEntry e = entries[ent];
+    const int64_t base = static_cast<int64_t>(chunk) * kCopyChunk;
+    const u32x4* s = reinterpret_cast<const u32x4*>(src_base + e.src * page_bytes + base);
+    u32x4* d = reinterpret_cast<u32x4*>(dst_base + e.dst * page_bytes + base);
+    const int64_t left = (page_bytes - base) / 16;  // 16-byte words left in this page
+    u32x4 buf[kCopyUnroll];
+#pragma unroll
+    for (int i = 0; i < kCopyUnroll; ++i) {
+        const int64_t w = static_cast<int64_t>(i) * kBlockThreads + threadIdx.x;
+        if (w < left) buf[i] = __builtin_nontemporal_load(s + w);
+    }
+#pragma unroll
+    for (int i = 0; i < kCopyUnroll; ++i) {
+        const int64_t w = static_cast<int64_t>(i) * kBlockThreads + threadIdx.x;
+        if (w < left) __builtin_nontemporal_store(buf[i], d + w);
+    }
+    if (chunk == 0 && threadIdx.x == 0 && e.pt_index >= 0) page_table[e.pt_index] = e.dst;
+}
+
+__global__ __launch_bounds__(kBlockThreads) void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * kBlockThreads)
+        p[i] = v;
+}
+
+// SplitMix64 output function of x + golden ratio (Steele, Lea and Flood 2014).
+__device__ __forceinline__ uint64_t splitmix_mix(uint64_t x) {
+    uint64_t z = x + 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ float synth_value(uint64_t key, uint64_t coord, float mult) {
+    const uint64_t h = splitmix_mix(key ^ coord);
+    const int s = static_cast<int>(h & 0xFFFF) + static_cast<int>((h >> 16) & 0xFFFF) +
+                  static_cast<int>((h >> 32) & 0xFFFF) + static_cast<int>(h >> 48) - 131070;
+    return static_cast<float>(s) * mult;
+}
+
+__device__ __forceinline__ uint64_t synth_coord(int kind, int sid, int layer, int head, int token,
+                                                int dim) {
+    return (static_cast<uint64_t>(kind) << 62) | (static_cast<uint64_t>(sid) << 42) |
+           (static_cast<uint64_t>(layer) << 36) | (static_cast<uint64_t>(head) << 32) |
+           (static_cast<uint64_t>(token) << 8) | static_cast<uint64_t>(dim);
+}
+
+__device__ __forceinline__ unsigned short bf16_rne(float f) {
+    const unsigned b = __builtin_bit_cast(unsigned, f);
+    return static_cast<unsigned short>((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+}
+
+// One thread per 16-byte group of a session's pages.
+__global__ __launch_bounds__(kBlockThreads) void fill_synthetic_kernel(SynthArgs a) {
+    const bool bf16 = a.dtype == kDtypeBf16;
+    const int elt = bf16 ? 2 : 4;
+    const int x = 16 / elt;
+    const int64_t tile = static_cast<int64_t>(kPageTokens) * a.head_dim * elt;
+    const int64_t groups_per_page = a.page_bytes / 16;
+    const int64_t total = groups_per_page * a.num_pages;
+    const uint64_t key = splitmix_mix(a.seed);
+    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; gi < total;
+         gi += static_cast<int64_t>(gridDim.x) * kBlockThreads) {
+        const int page_idx = static_cast<int>(gi / groups_per_page);
+        const int64_t byte = (gi % groups_per_page) * 16;
+        const int32_t pid = a.row[page_idx];
+        const int64_t lh = byte / (2 * tile);
+        const int layer = static_cast<int>(lh / a.num_kv_heads);
+        const int head = static_cast<int>(lh % a.num_kv_heads);
+        const int64_t in_lh = byte % (2 * tile);
+        const int kind = static_cast<int>(in_lh / tile);
+        const int e0 = static_cast<int>((in_lh % tile) / elt);  // first element of the group
+        unsigned words[4];
+        if (bf16) {
+            unsigned short v[8];
+            for (int j = 0; j < 8; ++j) {
+                int t, d;
+                if (kind == 0) {
+                    t = (e0 / x) % kPageTokens;
+                    d = (e0 / (x * kPageTokens)) * x + j;
+                } else {
+                    t = (e0 + j) % kPageTokens;
+                    d = (e0 + j) / kPageTokens;
+                }
+                v[j] = bf16_rne(synth_value(
+                    key, synth_coord(kind, a.gen_sid, layer, head, page_idx * kPageTokens + t, d),
+                    a.value_mult));
+            }
+            for (int j = 0; j < 4; ++j) words[j] = v[2 * j] | (static_cast<unsigned>(v[2 * j + 1]) << 16);
+        } else {
+            for (int j = 0; j < 4; ++j) {
+                int t, d;
+                if (kind == 0) {
+                    t = (e0 / x) % kPageTokens;
+                    d = (e0 / (x * kPageTokens)) * x + j;
+                } else {
+                    t = (e0 + j) % kPageTokens;
+                    d = (e0 + j) / kPageTokens;
+                }
+                words[j] = __builtin_bit_cast(
+                    unsigned, synth_value(key,
+                                          synth_coord(kind, a.gen_sid, layer, head,
+                                                      page_idx * kPageTokens + t, d),
+                                          a.value_mult));
+            }
+        }
+        *reinterpret_cast<u32x4*>(a.hot + static_cast<int64_t>(pid) * a.page_bytes + byte) =
+            u32x4{words[0], words[1], words[2], words[3]};
+    }
+}
+
+// One thread per (token, KV head, 16-byte group of dims).
+__global__ __launch_bounds__(kBlockThreads) void write_tokens_kernel(WriteArgs a) {
+    const int elt = a.dtype == kDtypeBf16 ? 2 : 4;
+    const int x = 16 / elt;
+    const int groups = a.head_dim / x;
+    const int64_t tile = static_cast<int64_t>(kPageTokens) * a.head_dim * elt;
+    const int64_t total = static_cast<int64_t>(a.n_tok) * a.num_kv_heads * groups;
+    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; gi < total;
+         gi += static_cast<int64_t>(gridDim.x) * kBlockThreads) {
+        const int cd = static_cast<int>(gi % groups);
+        const int head = static_cast<int>((gi / groups) % a.num_kv_heads);
+        const int tok = static_cast<int>(gi / (static_cast<int64_t>(groups) * a.num_kv_heads));
+        const int t = a.tok_begin + tok;
+        const int32_t pid = a.row[t / kPageTokens];
+        const int slot = t % kPageTokens;
+        char* lh = a.hot + static_cast<int64_t>(pid) * a.page_bytes +
+                   (static_cast<int64_t>(a.layer) * a.num_kv_heads + head) * 2 * tile;
+        const int64_t src_elem = (static_cast<int64_t>(tok) * a.num_kv_heads + head) * a.head_dim + cd * x;
+        // K: the group's x dims are contiguous in the tile
+        const u32x4 kv = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.k) + src_elem * elt);
+        *reinterpret_cast<u32x4*>(lh + (static_cast<int64_t>(cd) * kPageTokens + slot) * x * elt) = kv;
+        // V: dims-major, token-minor
+        const char* vs = static_cast<const char*>(a.v) + src_elem * elt;
+        char* vt = lh + tile;
+        for (int j = 0; j < x; ++j) {
+            const int64_t e = static_cast<int64_t>(cd * x + j) * kPageTokens + slot;
+            if (elt == 2)
+                *reinterpret_cast<unsigned short*>(vt + e * 2) = reinterpret_cast<const unsigned short*>(vs)[j];
+            else
+                *reinterpret_cast<unsigned*>(vt + e * 4) = reinterpret_cast<const unsigned*>(vs)[j];
+        }
+    }
+}
+
+__global__ __launch_bounds__(kBlockThreads) void partition_holes_kernel(int32_t* slots, int64_t n) {
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * kBlockThreads) {
+        reinterpret_cast<int4*>(slots)[i] = make_int4(-1, -1, 0, 0);
+    }
+}
+
+// One thread per wave: enumerate its pieces exactly as the decode kernel does.
+__global__ __launch_bounds__(kBlockThreads) void partition_kernel(const int32_t* seq_lens, int batch,
+                                                                  int num_kv_heads, int waves,
+                                                                  int64_t stride, int32_t* slots) {
+    extern __shared__ int32_t s_pref[];
+    block_prefix_pages(seq_lens, batch, stride, s_pref);
+    __syncthreads();
+    const int64_t total = static_cast<int64_t>(lds_uniform(s_pref + batch)) * num_kv_heads;
+    for (int k = blockIdx.x * kBlockThreads + threadIdx.x; k < waves; k += gridDim.x * kBlockThreads) {
+        int64_t u, u1;
+        wave_units(total, k, waves, u, u1);
+        while (u < u1) {
+            const Piece pc = piece_at(s_pref, batch, num_kv_heads, k, u, u1);
+            if (pc.p1 <= pc.p0) break;  // cannot happen for a consistent prefix; never spin
+            reinterpret_cast<int4*>(slots)[pc.slot] = make_int4(pc.b, pc.g, pc.p0, pc.p1);
+            u += pc.p1 - pc.p0;
+        }
+    }
+}
+
+int grid_for(int64_t work, int cap) {
+    const int64_t b = (work + kBlockThreads - 1) / kBlockThreads;
+    return static_cast<int>(b < 1 ? 1 : (b > cap ? cap : b));
+}
+
+}  // namespace
+
+hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_bytes,
+                            const CopyEntry* entries, int32_t n, int32_t* page_table,
+                            hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const int chunks = static_cast<int>((page_bytes + kCopyChunk - 1) / kCopyChunk);
+    const int64_t blocks = static_cast<int64_t>(chunks) * n;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(page_copy_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kBlockThreads), 0,
+                       s, src_base, dst_base, page_bytes, entries, n, chunks, page_table);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(n, 4096)), dim3(kBlockThreads), 0, s, p, n, value);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_synthetic(const SynthArgs& a, hipStream_t s) {
+    const int64_t groups = a.page_bytes / 16 * a.num_pages;
+    if (groups <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_synthetic_kernel, dim3(grid_for(groups, 16384)), dim3(kBlockThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_write_tokens(const WriteArgs& a, hipStream_t s) {
+    const int x = a.dtype == kDtypeBf16 ? 8 : 4;
+    const int64_t work = static_cast<int64_t>(a.n_tok) * a.num_kv_heads * (a.head_dim / x);
+    if (work <= 0) return hipSuccess;
+    hipLaunchKernelGGL(write_tokens_kernel, dim3(grid_for(work, 16384)), dim3(kBlockThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_partition(const int32_t* seq_lens, int batch, int num_kv_heads, int waves,
+                            int64_t pt_stride, int32_t* slots, hipStream_t s) {
+    const int64_t n = static_cast<int64_t>(waves) + static_cast<int64_t>(batch) * num_kv_heads;
+    hipLaunchKernelGGL(partition_holes_kernel, dim3(grid_for(n, 4096)), dim3(kBlockThreads), 0, s, slots, n);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || batch == 0) return e;
+    const size_t lds = static_cast<size_t>(batch + 1) * sizeof(int32_t);
+    hipLaunchKernelGGL(partition_kernel, dim3(grid_for(waves, 1024)), dim3(kBlockThreads), lds, s,
+                       seq_lens, batch, num_kv_heads, waves, pt_stride, slots);
+    return hipGetLastError();
+}
+
+}  // namespace hck

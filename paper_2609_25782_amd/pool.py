@@ -1,0 +1,137 @@
+"""A pool object over the C ABI: torch supplies device memory and streams,
+every operation is a call into the HIP library."""
+
+from __future__ import annotations
+
+from typing import Optional, Sequence
+
+import torch
+
+from . import hotcold_kv as kv
+
+_DTYPES = {"bf16": (kv.KV_DTYPE_BF16, torch.bfloat16), "f32": (kv.KV_DTYPE_F32, torch.float32)}
+
+
+def _stream(stream: Optional[torch.cuda.Stream]) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+class HotColdPool:
+    """Hot and cold page pools plus the pool's page table, all caller-owned torch
+    tensors, bound to one library pool handle."""
+
+    def __init__(self, num_layers: int, num_kv_heads: int, head_dim: int, dtype: str,
+                 num_hot_pages: int, num_cold_pages: int, max_sessions: int,
+                 max_pages_per_session: int, device: int = 0, cold_location: str = "device",
+                 stream: Optional[torch.cuda.Stream] = None):
+        kdtype, self.torch_dtype = _DTYPES[dtype]
+        self.dtype = dtype
+        self.device = torch.device("cuda", device)
+        self.desc = kv.kv_pool_desc(num_layers, num_kv_heads, head_dim, kv.KV_PAGE_TOKENS, kdtype,
+                                    num_hot_pages, num_cold_pages,
+                                    kv.KV_COLD_PINNED_HOST if cold_location == "host" else kv.KV_COLD_DEVICE,
+                                    max_sessions, max_pages_per_session, device, 0)
+        self.page_bytes = kv.kv_page_bytes(self.desc)
+        if self.page_bytes == 0:
+            raise ValueError("invalid pool shape")
+        self.num_layers, self.num_kv_heads, self.head_dim = num_layers, num_kv_heads, head_dim
+        self.num_hot_pages, self.num_cold_pages = num_hot_pages, num_cold_pages
+        self.max_sessions, self.stride = max_sessions, max_pages_per_session
+        self.hot = torch.empty(max(num_hot_pages, 1) * self.page_bytes, dtype=torch.uint8,
+                               device=self.device)
+        if cold_location == "host":
+            self.cold = torch.empty(max(num_cold_pages, 1) * self.page_bytes, dtype=torch.uint8,
+                                    pin_memory=True)
+        else:
+            self.cold = torch.empty(max(num_cold_pages, 1) * self.page_bytes, dtype=torch.uint8,
+                                    device=self.device)
+        self.page_table = torch.empty((max_sessions, max_pages_per_session), dtype=torch.int32,
+                                      device=self.device)
+        self.handle = kv.kv_pool_create(self.desc, self.hot.data_ptr(), self.hot.numel(),
+                                        self.cold.data_ptr(), self.cold.numel(),
+                                        self.page_table.data_ptr(), _stream(stream))
+        self._ws = None
+
+    # -- lifetime ----------------------------------------------------------
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            torch.cuda.synchronize(self.device)
+            kv.kv_pool_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- sessions ----------------------------------------------------------
+    def create_session(self, seq_len: int, hot_pages: Optional[Sequence[int]] = None, stream=None) -> int:
+        return kv.kv_session_create(self.handle, int(seq_len), hot_pages, _stream(stream))
+
+    def import_cold(self, seq_len: int, cold_pages: Sequence[int]) -> int:
+        return kv.kv_session_import_cold(self.handle, int(seq_len), cold_pages)
+
+    def destroy_session(self, sid: int, stream=None) -> None:
+        kv.kv_session_destroy(self.handle, sid, _stream(stream))
+
+    def info(self, sid: int):
+        return kv.kv_session_info(self.handle, sid)
+
+    def write_tokens(self, sid: int, layer: int, tok_begin: int, k: torch.Tensor, v: torch.Tensor,
+                     stream=None) -> None:
+        assert k.is_contiguous() and v.is_contiguous() and k.shape == v.shape
+        assert k.dtype == self.torch_dtype and k.device == self.device
+        kv.kv_write_tokens(self.handle, sid, layer, tok_begin, k.shape[0], k.data_ptr(), v.data_ptr(),
+                           _stream(stream))
+
+    def fill_synthetic(self, sid: int, gen_sid: int, seed: int, value_mult: float, stream=None) -> None:
+        kv.kv_fill_synthetic(self.handle, sid, gen_sid, seed, float(value_mult), _stream(stream))
+
+    def evict(self, sid: int, stream=None) -> None:
+        kv.kv_evict_session(self.handle, sid, _stream(stream))
+
+    def resume(self, sids, stream=None) -> None:
+        if isinstance(sids, int):
+            kv.kv_resume_session(self.handle, sids, _stream(stream))
+        else:
+            kv.kv_resume_sessions(self.handle, list(sids), _stream(stream))
+
+    def stats(self) -> dict:
+        return kv.kv_pool_stats_get(self.handle)
+
+    # -- decode ------------------------------------------------------------
+    def workspace(self, batch: int, num_q_heads: int) -> torch.Tensor:
+        need = kv.paged_decode_workspace_bytes(self.handle, batch, num_q_heads)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        return self._ws
+
+    def decode(self, layer: int, q: torch.Tensor, seq_lens: torch.Tensor,
+               page_table: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+               out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        pt = self.page_table if page_table is None else page_table
+        assert q.is_contiguous() and q.dtype == self.torch_dtype and q.dim() == 3
+        assert pt.dtype == torch.int32 and pt.is_contiguous() and seq_lens.dtype == torch.int32
+        B, Hq, D = q.shape
+        if out is None:
+            out = torch.empty_like(q)
+        ws = self.workspace(B, Hq)
+        kv.paged_decode_attention(self.handle, layer, q.data_ptr(), pt.data_ptr(), pt.shape[1],
+                                  seq_lens.data_ptr(), B, Hq, float(scale if scale is not None else D ** -0.5),
+                                  out.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream))
+        return out
+
+    def partition(self, seq_lens: torch.Tensor, waves: int, stream=None) -> torch.Tensor:
+        B = seq_lens.shape[0]
+        slots = torch.empty((waves + B * self.num_kv_heads, 4), dtype=torch.int32, device=self.device)
+        kv.paged_decode_partition(self.handle, seq_lens.data_ptr(), B, waves, slots.data_ptr(),
+                                  _stream(stream))
+        return slots
+
+    def waves(self) -> int:
+        return kv.paged_decode_waves(self.handle)
+
+    def set_waves(self, waves: int) -> None:
+        kv.kv_pool_set_decode_waves(self.handle, waves)

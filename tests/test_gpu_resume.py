@@ -1,0 +1,309 @@
+"""GPU parity of resume (cold -> hot gather + page-table rewrite) and eviction
+(write-on-evict scatter): page tables must equal the oracle pool model's
+prediction and page bytes must match bit for bit."""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from helpers import Case, build_gpu, to_device, to_host
+from oracle.pool_model import PoolModel
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch.device("cuda", 0)
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _pages(t: torch.Tensor, page_bytes: int, ids) -> np.ndarray:
+    """Host copy of the given pages of a pool tensor (uint8 rows)."""
+    idx = torch.tensor([int(i) for i in ids], dtype=torch.long, device=t.device)
+    return t.view(-1, page_bytes).index_select(0, idx).cpu().numpy() if len(ids) else \
+        np.zeros((0, page_bytes), np.uint8)
+
+
+def _random_fill(pool, seed):
+    g = torch.Generator(device=pool.device)
+    g.manual_seed(seed)
+    pool.hot.copy_(torch.randint(0, 256, pool.hot.shape, dtype=torch.uint8, device=pool.device, generator=g))
+    pool.cold.copy_(torch.randint(0, 256, pool.cold.shape, dtype=torch.uint8, device=pool.device, generator=g))
+
+
+def _check_table(pool, model: PoolModel):
+    got = pool.page_table.cpu().numpy()
+    want = np.array(model.table(), dtype=np.int32)
+    assert np.array_equal(got, want)
+
+
+def test_tiny_resume_config(dev):
+    """Two paused sessions of 256 tokens resumed from a 64-page cold pool (fp32,
+    d=64, one layer): exact page table and bytes."""
+    from paper_2609_25782_amd.pool import HotColdPool
+    _say("tiny resume config")
+    pool = HotColdPool(1, 1, 64, "f32", 80, 64, 8, 32)
+    model = PoolModel(80, 64, 8, 32)
+    _random_fill(pool, 1)
+    torch.cuda.synchronize()
+    cold_before = pool.cold.clone()
+    # the paused sessions' KV already sits in the cold tier at known pages
+    rng = np.random.default_rng(0)
+    cold_lists = [rng.choice(64, 16, replace=False), rng.choice(64, 16, replace=False)]
+    sids = [pool.import_cold(256, c) for c in cold_lists]
+    assert sids == [model.import_cold(256, c) for c in cold_lists]
+    # some active sessions first so the resumed pages are not simply 0..31
+    for L in (100, 37):
+        assert pool.create_session(L) == model.create(L)
+    pool.resume(sids)
+    copies = model.resume(sids)
+    torch.cuda.synchronize()
+    _check_table(pool, model)
+    pb = pool.page_bytes
+    for per in copies:
+        src = [c for c, _ in per]
+        dst = [h for _, h in per]
+        assert np.array_equal(_pages(pool.hot, pb, dst), _pages(cold_before, pb, src))
+    assert torch.equal(pool.cold, cold_before)  # resume never writes the cold tier
+    st = pool.stats()
+    assert st["pages_to_hot"] == 32 and st["resumes"] == 2
+    pool.close()
+
+
+def test_evict_resume_round_trip_decode_bitwise(dev):
+    """Decode before eviction equals decode after resume into other pages (P8)."""
+    case = Case(1, 32, 4, 128, "bf16", [3000, 700, 16, 4099], seed=21, slack=1.3)
+    pool = build_gpu(case, dev, num_cold_pages=sum(synth.pages_for(L) for L in case.seq_lens),
+                     pool_kwargs={"max_sessions": 8})
+    q = to_device(case.q, "bf16", dev)
+    sl = torch.tensor(case.seq_lens, dtype=torch.int32, device=dev)
+    before = to_host(pool.decode(0, q, sl))
+    rows_before = pool.page_table[:4].clone()
+    for sid in (0, 2):
+        pool.evict(sid)
+    # occupy the freed pages so the resume must land elsewhere
+    blocker = pool.create_session(16 * 200)
+    pool.resume([2, 0])
+    torch.cuda.synchronize()
+    assert not torch.equal(pool.page_table[:4], rows_before)
+    after = to_host(pool.decode(0, q, sl, page_table=pool.page_table[:4].contiguous()))
+    torch.cuda.synchronize()
+    assert np.array_equal(before, after)
+    pool.destroy_session(blocker)
+    pool.close()
+
+
+def test_write_on_evict_writes_each_page_once(dev):
+    """Sec. III: an unmodified page reaches the cold tier at most once; a page
+    written to after its cold copy was made is written again."""
+    case = Case(1, 8, 2, 64, "bf16", [16 * 9 + 5], seed=22)
+    pool = build_gpu(case, dev, num_cold_pages=64, pool_kwargs={"max_sessions": 2})
+    model = PoolModel(case.hot_pages, 64, 2, case.stride)
+    model.create(case.seq_lens[0], case.placement[0])
+    for _ in range(3):
+        pool.evict(0), model.evict(0)
+        pool.resume(0), model.resume([0])
+    st = pool.stats()
+    assert st["pages_to_cold"] == 10 == model.cold_writes
+    # rewrite token 40 (page 2) -> only that page is written on the next eviction
+    k, v = case.kv[0]
+    pool.write_tokens(0, 0, 40, to_device(k[40:41], "bf16", dev), to_device(v[40:41], "bf16", dev))
+    model.write_tokens(0, 40, 1)
+    copies = model.evict(0)
+    pool.evict(0)
+    assert len(copies) == 1 and pool.stats()["pages_to_cold"] == 11
+    pool.resume(0), model.resume([0])
+    torch.cuda.synchronize()
+    _check_table(pool, model)
+    pool.close()
+
+
+def test_resume_exhaustion_changes_nothing(dev):
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+    pool = HotColdPool(2, 2, 64, "bf16", 10, 20, 4, 8)
+    a = pool.create_session(16 * 6)
+    pool.evict(a)
+    b = pool.create_session(16 * 6)  # 6 of 10 hot pages used: a (6 pages) cannot come back
+    torch.cuda.synchronize()
+    table = pool.page_table.clone()
+    st = pool.stats()
+    with pytest.raises(kv.KVError) as e:
+        pool.resume(a)
+    assert e.value.status == kv.KV_ERR_NO_HOT_PAGES
+    with pytest.raises(kv.KVError) as e:
+        pool.resume([a, b])
+    assert e.value.status == kv.KV_ERR_STATE
+    torch.cuda.synchronize()
+    assert torch.equal(pool.page_table, table) and pool.stats() == st
+    pool.close()
+
+
+def test_aliased_cold_pages_resume(dev):
+    """Paused sessions sharing cold pages (virtualised cold pool) resume correctly."""
+    from paper_2609_25782_amd.pool import HotColdPool
+    pool = HotColdPool(1, 4, 128, "bf16", 64, 16, 4, 16)
+    _random_fill(pool, 2)
+    torch.cuda.synchronize()
+    cold_before = pool.cold.clone()
+    a = pool.import_cold(16 * 10, list(range(10)))
+    b = pool.import_cold(16 * 8 + 3, [9, 8, 7, 15, 14, 13, 0, 1, 2])
+    model = PoolModel(64, 16, 4, 16)
+    model.import_cold(16 * 10, list(range(10)))
+    model.import_cold(16 * 8 + 3, [9, 8, 7, 15, 14, 13, 0, 1, 2])
+    copies = model.resume([b, a])
+    pool.resume([b, a])
+    torch.cuda.synchronize()
+    _check_table(pool, model)
+    pb = pool.page_bytes
+    for per in copies:
+        assert np.array_equal(_pages(pool.hot, pb, [h for _, h in per]),
+                              _pages(cold_before, pb, [c for c, _ in per]))
+    pool.close()
+
+
+def test_random_sequences_match_model(dev):
+    """Random create / write / evict / resume / destroy sequences: page tables,
+    statistics and every active page's bytes follow the model exactly."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+    nh, nc, ms, stride = 48, 40, 6, 8
+    pool = HotColdPool(2, 2, 64, "bf16", nh, nc, ms, stride)
+    model = PoolModel(nh, nc, ms, stride)
+    _random_fill(pool, 3)
+    torch.cuda.synchronize()
+    # expected content of every hot and cold page, tracked through the copies
+    hot_img = pool.hot.view(nh, -1).cpu().numpy().copy()
+    cold_img = pool.cold.view(nc, -1).cpu().numpy().copy()
+    rng = np.random.default_rng(4)
+    for step in range(300):
+        op = int(rng.integers(0, 5))
+        sid = int(rng.integers(0, ms))
+        try:
+            if op == 0:
+                L = int(rng.integers(0, 16 * stride + 1))
+                try:
+                    model_sid = model.create(L)
+                except Exception as e:
+                    with pytest.raises(kv.KVError):
+                        pool.create_session(L)
+                    raise e
+                assert pool.create_session(L) == model_sid
+            elif op == 1:
+                try:
+                    copies = model.evict(sid)
+                except Exception as e:
+                    with pytest.raises(kv.KVError):
+                        pool.evict(sid)
+                    raise e
+                pool.evict(sid)
+                for h, c in copies:
+                    cold_img[c] = hot_img[h]
+            elif op == 2:
+                sids = [int(x) for x in rng.choice(ms, size=int(rng.integers(1, 3)), replace=False)]
+                try:
+                    res = model.resume(sids)
+                except Exception as e:
+                    with pytest.raises(kv.KVError):
+                        pool.resume(sids)
+                    raise e
+                pool.resume(sids)
+                for per in res:
+                    for c, h in per:
+                        hot_img[h] = cold_img[c]
+            elif op == 3:
+                try:
+                    model.destroy(sid)
+                except Exception as e:
+                    with pytest.raises(kv.KVError):
+                        pool.destroy_session(sid)
+                    raise e
+                pool.destroy_session(sid)
+            else:
+                s = model.sessions[sid]
+                if s.state == 1 and s.seq_len > 0:
+                    t0 = int(rng.integers(0, s.seq_len))
+                    n = int(rng.integers(1, min(20, s.seq_len - t0) + 1))
+                    layer = int(rng.integers(0, 2))
+                    kk = rng.integers(0, 65535, size=(n, 2, 64), dtype=np.uint16)
+                    vv = rng.integers(0, 65535, size=(n, 2, 64), dtype=np.uint16)
+                    pool.write_tokens(sid, layer, t0, to_device(kk, "bf16", dev), to_device(vv, "bf16", dev))
+                    model.write_tokens(sid, t0, n)
+                    # mirror the writes on the host image with the oracle's packer
+                    import oracle
+                    flat = hot_img.reshape(-1)
+                    pages = np.array(model.sessions[sid].hot, dtype=np.int64)
+                    full_k = np.zeros((t0 + n, 2, 64), np.uint16)
+                    full_v = np.zeros((t0 + n, 2, 64), np.uint16)
+                    full_k[t0:] = kk
+                    full_v[t0:] = vv
+                    tmp = flat.copy()
+                    oracle.pack_pool(tmp, 2, 2, 64, oracle.BF16, layer, pages, full_k, full_v)
+                    # only tokens t0.. are written: copy those elements back
+                    for t in range(t0, t0 + n):
+                        for g in range(2):
+                            for d in range(64):
+                                for kind in (0, 1):
+                                    off = oracle.elem_offset(2, 2, 64, oracle.BF16, int(pages[t // 16]),
+                                                             layer, g, kind, t % 16, d)
+                                    flat[off:off + 2] = tmp[off:off + 2]
+        except Exception as e:  # the model refused: the library refused as well
+            if not hasattr(e, "code"):
+                raise
+        if step % 25 == 24:
+            torch.cuda.synchronize()
+            _check_table(pool, model)
+            st = pool.stats()
+            assert st["free_hot_pages"] == model.free_hot() and st["free_cold_pages"] == model.free_cold()
+            assert st["pages_to_cold"] == model.cold_writes
+            gpu_hot = pool.hot.view(nh, -1).cpu().numpy()
+            for s in model.sessions:
+                if s.state == 1:
+                    for p in s.hot:
+                        assert np.array_equal(gpu_hot[p], hot_img[p])
+    pool.close()
+
+
+def test_resume_48_layer_pages(dev):
+    """1.5 MiB pages (48 layers x 4 KV heads x 128 x bf16): a resumed session's
+    pages are bit-exact copies and its decode matches the oracle on a sampled layer."""
+    from paper_2609_25782_amd.pool import HotColdPool
+    lens = [16 * 300 + 7, 16 * 120]
+    n_pages = sum(synth.pages_for(L) for L in lens)
+    pool = HotColdPool(48, 4, 128, "bf16", n_pages + 50, n_pages, 4, 320)
+    assert pool.page_bytes == 1536 * 1024
+    for b, L in enumerate(lens):
+        sid = pool.create_session(L)
+        pool.fill_synthetic(sid, b, 77, float(synth.value_multiplier(1.0)))
+    for sid in range(2):
+        pool.evict(sid)
+    blocker = pool.create_session(16 * 40)
+    pool.resume([1, 0])
+    torch.cuda.synchronize()
+    st0, L0, hot0, cold0 = pool.info(0)
+    pb = pool.page_bytes
+    for i in (0, 1, len(hot0) - 1, 150):
+        assert torch.equal(pool.hot.view(-1, pb)[hot0[i]], pool.cold.view(-1, pb)[cold0[i]])
+    # decode layer 31 of both sessions against the oracle on regenerated KV
+    from helpers import Case
+    case = Case(48, 32, 4, 128, "bf16", lens, seed=77, layer=31,
+                placement=[np.array(pool.info(s)[2], np.int32) for s in range(2)],
+                hot_pages=n_pages + 50)
+    case.kv = [synth.session_kv(77, b, L, 31, 4, 128, 1.0, "bf16") for b, L in enumerate(lens)]
+    q = to_device(case.q, "bf16", dev)
+    sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+    got = to_host(pool.decode(31, q, sl, page_table=pool.page_table[:2].contiguous()))
+    torch.cuda.synchronize()
+    from helpers import tolerance_check
+    tolerance_check(got, case.oracle_out())
+    pool.destroy_session(blocker)
+    pool.close()

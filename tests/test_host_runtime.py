@@ -1,0 +1,108 @@
+"""Host bookkeeping of the library (a metadata-only pool: no device work) against
+the oracle's pool model: same session ids, page lists, errors and counters on
+random call sequences, and no state change on any failing call (CPU only)."""
+
+import numpy as np
+import pytest
+
+from oracle.pool_model import ACTIVE, ModelError, PoolModel
+
+
+def _lib():
+    from paper_2609_25782_amd import hotcold_kv as kv
+    return kv
+
+
+def _meta_pool(kv, nh, nc, ms, stride):
+    d = kv.kv_pool_desc(1, 1, 64, 16, kv.KV_DTYPE_F32, nh, nc, 0, ms, stride, 0,
+                        kv.KV_POOL_METADATA_ONLY)
+    return kv.kv_pool_create(d, 0, 0, 0, 0, 0)
+
+
+def _snapshot(kv, pool, ms):
+    return [kv.kv_session_info(pool, s) for s in range(ms)], kv.kv_pool_stats_get(pool)
+
+
+def _same(kv, pool, model, ms):
+    for sid in range(ms):
+        state, L, hot, cold = kv.kv_session_info(pool, sid)
+        s = model.sessions[sid]
+        assert state == s.state
+        if state:
+            assert L == s.seq_len and cold == s.cold
+            assert hot == (s.hot if state == ACTIVE else [])
+    st = kv.kv_pool_stats_get(pool)
+    assert st["free_hot_pages"] == model.free_hot()
+    assert st["free_cold_pages"] == model.free_cold()
+    assert st["pages_to_cold"] == model.cold_writes
+    assert st["pages_to_hot"] == model.pages_to_hot
+    assert st["resumes"] == model.resumes and st["evicts"] == model.evicts
+
+
+def _random_call(kv, pool, rng, nh, nc, ms, stride):
+    """One random call as a (model call, library call) pair."""
+    op = int(rng.integers(0, 5))
+    sid = int(rng.integers(-1, ms + 1))
+    if op == 0:
+        L = int(rng.integers(-2, 16 * stride + 20))
+        pages = None
+        if rng.random() < 0.3 and 0 <= L <= 16 * stride:
+            pages = [int(p) for p in rng.choice(nh, size=(L + 15) // 16, replace=False)]
+        return (lambda m: m.create(L, pages)), (lambda: kv.kv_session_create(pool, L, pages))
+    if op == 1:
+        return (lambda m: (m.evict(sid), None)[1]), (lambda: kv.kv_evict_session(pool, sid))
+    if op == 2:
+        sids = [int(x) for x in rng.integers(-1, ms + 1, size=int(rng.integers(1, 4)))]
+        return (lambda m: (m.resume(sids), None)[1]), (lambda: kv.kv_resume_sessions(pool, sids))
+    if op == 3:
+        return (lambda m: m.destroy(sid)), (lambda: kv.kv_session_destroy(pool, sid))
+    n = int(rng.integers(0, stride + 1))
+    cold = [int(p) for p in rng.choice(nc, size=n, replace=False)]
+    L = 16 * n - (int(rng.integers(0, 16)) if n else 0)
+    return (lambda m: m.import_cold(L, cold)), (lambda: kv.kv_session_import_cold(pool, L, cold))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_random_sequences_follow_the_model(seed):
+    kv = _lib()
+    nh, nc, ms, stride = 60, 45, 7, 9
+    pool = _meta_pool(kv, nh, nc, ms, stride)
+    model = PoolModel(nh, nc, ms, stride)
+    rng = np.random.default_rng(seed)
+    refused = 0
+    for step in range(1500):
+        on_model, on_lib = _random_call(kv, pool, rng, nh, nc, ms, stride)
+        before = _snapshot(kv, pool, ms)
+        try:
+            expect = on_model(model)
+        except ModelError as e:
+            refused += 1
+            with pytest.raises(kv.KVError) as err:
+                on_lib()
+            assert err.value.status == e.code, (e, err.value)
+            assert _snapshot(kv, pool, ms) == before
+        else:
+            got = on_lib()
+            assert got == expect
+        _same(kv, pool, model, ms)
+    assert 100 < refused < 1400
+    kv.kv_pool_destroy(pool)
+
+
+def test_exhaustion_codes():
+    kv = _lib()
+    pool = _meta_pool(kv, 4, 2, 4, 4)
+    a = kv.kv_session_create(pool, 48)
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_session_create(pool, 33)
+    assert e.value.status == kv.KV_ERR_NO_HOT_PAGES
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_evict_session(pool, a)
+    assert e.value.status == kv.KV_ERR_NO_COLD_PAGES
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_resume_session(pool, a)
+    assert e.value.status == kv.KV_ERR_STATE
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_write_tokens(pool, a, 0, 0, 1, 0, 0)
+    assert e.value.status == kv.KV_ERR_INVALID
+    kv.kv_pool_destroy(pool)
