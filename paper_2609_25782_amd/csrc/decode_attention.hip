@@ -116,8 +116,8 @@ __device__ __forceinline__ f32x4 page_scores(const PageRegs<D, BF16>& r,
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                s = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, r.k[i][j]),
-                                                         __builtin_bit_cast(float, q[i][j]), s, 0,
+                s = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(r.k[i][j]),
+                                                         __uint_as_float(q[i][j]), s, 0,
                                                          0, 0);
         }
     }
@@ -206,7 +206,7 @@ __device__ __forceinline__ void compute_page(SegmentState<D, BF16>& st, PageRegs
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 st.o[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                    __builtin_bit_cast(float, pg.v[c][j]), p[j], st.o[c], 0, 0, 0);
+                    __uint_as_float(pg.v[c][j]), p[j], st.o[c], 0, 0, 0);
     }
 }
 
@@ -308,7 +308,7 @@ __global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs 
     int64_t u, u1;
     wave_units(total, wave, a.waves, u, u1);
     while (u < u1) {
-        const Piece pc = piece_at(s_pref, a.batch, a.num_kv_heads, wave, u, u1);
+        const Piece pc = piece_at<true>(s_pref, a.batch, a.num_kv_heads, wave, u, u1);
         if (pc.p1 <= pc.p0) break;  // cannot happen for a consistent prefix; never spin
         const int nb = lds_uniform(s_pref + pc.b + 1) - lds_uniform(s_pref + pc.b);
         const int32_t L = a.seq_lens[pc.b];

@@ -75,7 +75,16 @@ __device__ __forceinline__ void wave_units(int64_t total_units, int wave, int wa
     u1 = static_cast<int64_t>(wave + 1) * total_units / waves;
 }
 
+// LDS read used by piece_at: readfirstlane when every lane of the wave asks
+// for the same unit (decode), a plain per-lane read otherwise (partition table).
+template <bool kWaveUniform>
+__device__ __forceinline__ int32_t lds_read(const int32_t* p) {
+    if constexpr (kWaveUniform) return lds_uniform(p);
+    return *p;
+}
+
 // The piece that starts at unit u (< total), ending no later than u_end.
+template <bool kWaveUniform>
 __device__ __forceinline__ Piece piece_at(const int32_t* s_pref, int batch, int num_kv_heads,
                                           int wave, int64_t u, int64_t u_end) {
     // largest row b with Hkv * s_pref[b] <= u; it has at least one page
@@ -83,12 +92,12 @@ __device__ __forceinline__ Piece piece_at(const int32_t* s_pref, int batch, int 
     int lo = 0, hi = batch - 1;
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (lds_uniform(s_pref + mid) <= target) lo = mid; else hi = mid - 1;
+        if (lds_read<kWaveUniform>(s_pref + mid) <= target) lo = mid; else hi = mid - 1;
     }
     Piece pc;
     pc.b = lo;
-    const int32_t first = lds_uniform(s_pref + lo);
-    const int nb = lds_uniform(s_pref + lo + 1) - first;
+    const int32_t first = lds_read<kWaveUniform>(s_pref + lo);
+    const int nb = lds_read<kWaveUniform>(s_pref + lo + 1) - first;
     const int64_t rel = u - static_cast<int64_t>(first) * num_kv_heads;
     pc.g = static_cast<int>(rel / nb);
     pc.p0 = static_cast<int>(rel % nb);

@@ -179,7 +179,8 @@ __global__ __launch_bounds__(kBlockThreads) void partition_holes_kernel(int32_t*
     }
 }
 
-// One thread per wave: enumerate its pieces exactly as the decode kernel does.
+// One thread per wave: enumerate its pieces exactly as the decode kernel does
+// (here the lanes of a hardware wave work on different decode waves).
 __global__ __launch_bounds__(kBlockThreads) void partition_kernel(const int32_t* seq_lens, int batch,
                                                                   int num_kv_heads, int waves,
                                                                   int64_t stride, int32_t* slots) {
@@ -191,7 +192,7 @@ __global__ __launch_bounds__(kBlockThreads) void partition_kernel(const int32_t*
         int64_t u, u1;
         wave_units(total, k, waves, u, u1);
         while (u < u1) {
-            const Piece pc = piece_at(s_pref, batch, num_kv_heads, k, u, u1);
+            const Piece pc = piece_at<false>(s_pref, batch, num_kv_heads, k, u, u1);
             if (pc.p1 <= pc.p0) break;  // cannot happen for a consistent prefix; never spin
             reinterpret_cast<int4*>(slots)[pc.slot] = make_int4(pc.b, pc.g, pc.p0, pc.p1);
             u += pc.p1 - pc.p0;

@@ -91,7 +91,7 @@ def test_evict_resume_round_trip_decode_bitwise(dev):
     for sid in (0, 2):
         pool.evict(sid)
     # occupy the freed pages so the resume must land elsewhere
-    blocker = pool.create_session(16 * 200)
+    blocker = pool.create_session(16 * 40)
     pool.resume([2, 0])
     torch.cuda.synchronize()
     assert not torch.equal(pool.page_table[:4], rows_before)
