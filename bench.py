@@ -1,0 +1,270 @@
+#!/usr/bin/env python3
+"""Benchmark of the hot-cold KV hot path on one MI355X.
+
+One step is one pass of the whole hot path over one batch:
+  1. resume R paused sessions (batched cold -> hot gather + page-table rewrite),
+  2. paged GQA decode attention over the B active sessions (split + combine),
+  3. evict the R sessions again (write-on-evict: their cold copies are still
+     valid, so no page is rewritten; rows are cleared and pages freed).
+
+Default workload: one Qwen3-Coder-30B-A3B-shaped attention layer (32 query /
+4 KV heads, head_dim 128, bf16, 16-token pages), 32 active sessions with
+context lengths uniform in [8192, 32768], values N(0,1)/sqrt(128), pages
+randomly scattered over a hot pool 1.25x the pages needed; plus 8 paused
+sessions of the same length distribution in the cold pool.
+
+Prints one JSON line.  `value` is decode-attention throughput in GB/s:
+algorithmic bytes (K and V of every valid token, Q, out, page-table entries,
+lengths) per decode call divided by the measured device time of the decode
+kernels (HIP events on the launch stream).  Inputs are resident in HBM.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "decode-attention HBM GB/s (% of peak) + resume latency ms/session, 1 GPU"
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def decode_bytes(seq_lens, hq, hkv, d, elt):
+    """Algorithmic bytes of one decode call: K+V of each valid token for every KV
+    head, Q and out rows, one page-table entry per used page, one length per row."""
+    seq_lens = np.asarray(seq_lens, dtype=np.int64)
+    B = len(seq_lens)
+    kv = int(seq_lens.sum()) * hkv * d * 2 * elt
+    qo = B * hq * d * elt * 2
+    pt = 4 * int(((seq_lens + 15) // 16).sum()) + 4 * B
+    return kv, qo, pt
+
+
+def split_kernel_bytes(seq_lens, hq, hkv, d, elt):
+    kv, qo, pt = decode_bytes(seq_lens, hq, hkv, d, elt)
+    return kv + qo // 2 + pt  # K/V, Q, page table, lengths (the output is the combine's)
+
+
+def cpu_baseline(w, budget_s: float):
+    """Time the fp64 oracle on whole sessions of the same workload until about
+    `budget_s` seconds of oracle time have been spent (at least one session)."""
+    import oracle
+    import synth
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    d, hkv, hq = w.head_dim, w.num_kv_heads, w.num_q_heads
+    spent, nbytes, sessions = 0.0, 0, 0
+    q_all = synth.queries(w.seed + 1, w.batch, hq, d, w.value_scale, w.dtype)
+    for b in range(w.batch):
+        L = int(w.seq_lens[b])
+        k, v = synth.session_kv(w.seed, b, L, 0, hkv, d, w.value_scale, w.dtype)
+        n = synth.pages_for(L)
+        pb = oracle.page_bytes(1, hkv, d, oracle.BF16)
+        pool = np.zeros(n * pb, np.uint8)
+        pages = np.arange(n, dtype=np.int32)
+        oracle.pack_pool(pool, 1, hkv, d, oracle.BF16, 0, pages, k, v)
+        pt = pages[None, :].copy()
+        t0 = time.perf_counter()
+        oracle.paged_attention(pool, n, 1, hkv, d, oracle.BF16, 0, q_all[b:b + 1], pt,
+                               np.array([L], np.int32), 1.0 / math.sqrt(d), num_threads=threads)
+        spent += time.perf_counter() - t0
+        kvb, qo, ptb = decode_bytes([L], hq, hkv, d, 2)
+        nbytes += kvb + qo + ptb
+        sessions += 1
+        log("cpu baseline: session %d (L=%d) done, %.1f s of oracle time" % (b, L, spent))
+        if spent >= budget_s:
+            break
+    return {"value": round(nbytes / spent / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "fp64 C oracle (OpenMP over query heads) on %d whole sessions of the same "
+                      "workload (%d tokens, all 32 query heads), %.1f s" % (
+                          sessions, int(np.sum(w.seq_lens[:sessions])), spent)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--resume-per-step", type=int, default=8)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--waves", type=int, default=0, help="override the decode wave count")
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of oracle time for the CPU baseline (0 = skip)")
+    ap.add_argument("--no-check", action="store_true", help="skip the sampled oracle check")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(each GPU would own its own sessions; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda", 0)
+    w = synth.config_layer(args.seed)
+    R = args.resume_per_step
+    rng = np.random.Generator(np.random.PCG64([args.seed, 7]))
+    paused_lens = rng.integers(8192, 32768, size=R, endpoint=True).astype(np.int32)
+    paused_pages = int(sum(synth.pages_for(L) for L in paused_lens))
+    active_pages = int(sum(synth.pages_for(L) for L in w.seq_lens))
+    num_hot = w.hot_pages + paused_pages
+    stride = max(synth.pages_for(32768), 1)
+    log("workload %s: B=%d, %d tokens, %d active pages, %d resumed pages/step, hot pool %d pages"
+        % (w.name, w.batch, int(w.seq_lens.sum()), active_pages, paused_pages, num_hot))
+
+    pool = HotColdPool(1, w.num_kv_heads, w.head_dim, "bf16", num_hot, paused_pages,
+                       w.batch + R, stride)
+    mult = float(synth.value_multiplier(w.value_scale))
+    # active sessions 0..B-1 at the workload's scattered pages
+    for b in range(w.batch):
+        sid = pool.create_session(int(w.seq_lens[b]), [int(p) for p in w.placement[b]])
+        assert sid == b
+        pool.fill_synthetic(sid, b, w.seed, mult)
+    # paused sessions: written once, evicted (the one cold write each page gets)
+    paused = []
+    for j, L in enumerate(paused_lens):
+        sid = pool.create_session(int(L))
+        pool.fill_synthetic(sid, w.batch + j, w.seed, mult)
+        paused.append(sid)
+    for sid in paused:
+        pool.evict(sid)
+    torch.cuda.synchronize()
+    if args.waves:
+        pool.set_waves(args.waves)
+
+    q = torch.from_numpy(synth.queries(w.seed + 1, w.batch, w.num_q_heads, w.head_dim,
+                                       w.value_scale, "bf16").view(np.int16)).to(dev).view(torch.bfloat16)
+    seq = torch.from_numpy(w.seq_lens.copy()).to(dev)
+    pt = pool.page_table[:w.batch]
+    out = torch.empty_like(q)
+    scale = 1.0 / math.sqrt(w.head_dim)
+
+    def step():
+        pool.resume(paused)
+        pool.decode(0, q, seq, page_table=pt, scale=scale, out=out)
+        for sid in paused:
+            pool.evict(sid)
+
+    for i in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("warmup done (%d steps)" % args.warmup)
+
+    # sampled parity check of this exact launch configuration
+    check = None
+    if not args.no_check:
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from helpers import Case, tolerance_check
+        b = int(np.argmax(w.seq_lens))
+        case = Case(1, w.num_q_heads, w.num_kv_heads, w.head_dim, "bf16", [int(w.seq_lens[b])],
+                    seed=w.seed, value_scale=w.value_scale,
+                    placement=[np.arange(synth.pages_for(int(w.seq_lens[b])), dtype=np.int32)])
+        case.kv = [synth.session_kv(w.seed, b, int(w.seq_lens[b]), 0, w.num_kv_heads, w.head_dim,
+                                    w.value_scale, "bf16")]
+        case.q = synth.queries(w.seed + 1, w.batch, w.num_q_heads, w.head_dim, w.value_scale, "bf16")[b:b + 1]
+        ref = case.oracle_out()
+        got = out[b:b + 1].float().cpu().numpy().astype(np.float64)
+        err, norm = tolerance_check(got, ref)
+        check = {"session": b, "seq_len": int(w.seq_lens[b]), "max_abs_err": err, "normalised_err": norm}
+        log("sampled oracle check: session %d max abs %.3g normalised %.3g" % (b, err, norm))
+
+    kv.kv_pool_set_profiling(pool.handle, True)
+    for k in range(3):
+        kv.kv_pool_profile_read(pool.handle, k)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    n1, ms1 = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_DECODE_SPLIT)
+    n2, ms2 = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_DECODE_COMBINE)
+    n3, ms3 = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
+    kv.kv_pool_set_profiling(pool.handle, False)
+    assert n1 == args.steps and n2 == args.steps and n3 == args.steps, (n1, n2, n3)
+    log("timed %d steps: %.3f ms/step; split %.1f us, combine %.1f us, resume copy %.1f us"
+        % (args.steps, total_ms / args.steps, 1e3 * ms1 / n1, 1e3 * ms2 / n2, 1e3 * ms3 / n3))
+
+    kvb, qo, ptb = decode_bytes(w.seq_lens, w.num_q_heads, w.num_kv_heads, w.head_dim, 2)
+    dec_bytes = kvb + qo + ptb
+    dec_s = (ms1 + ms2) / 1e3 / args.steps
+    value = dec_bytes / dec_s / 1e9
+    k1_bytes = split_kernel_bytes(w.seq_lens, w.num_q_heads, w.num_kv_heads, w.head_dim, 2)
+    k1_s = ms1 / 1e3 / n1
+    k1_gbs = k1_bytes / k1_s / 1e9
+    payload = paused_pages * pool.page_bytes
+    res_s = ms3 / 1e3 / n3
+    res_gbs = 2 * payload / res_s / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "qwen3-coder-30b-a3b attention layer: 32 active sessions, context U[8192,32768], "
+                        "32q/4kv heads, d=128, bf16, 16-token pages scattered over the hot pool; "
+                        "%d paused sessions resumed and evicted per step" % R,
+            "batch": w.batch, "total_tokens": int(w.seq_lens.sum()), "num_q_heads": w.num_q_heads,
+            "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "layers": 1, "page_tokens": 16,
+            "hot_pages": num_hot, "decode_waves": pool.waves(), "seed": args.seed,
+        },
+        "pct_of_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+        "decode_us": round(1e6 * dec_s, 2),
+        "decode_bytes": dec_bytes,
+        "resume": {
+            "ms_per_session": round(1e3 * res_s / R, 5),
+            "ms_per_batch": round(1e3 * res_s, 5),
+            "sessions_per_batch": R,
+            "payload_bytes": payload,
+            "copy_GBps": round(res_gbs, 2),
+            "frac_of_copy_roofline": round(res_gbs / HBM_PEAK_GBS, 4),
+            "note": "copy roofline counts each payload byte read once and written once",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "decode_split_kernel",
+            "achieved": round(k1_gbs, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(k1_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "bytes_per_launch": k1_bytes,
+            "us_per_launch": round(1e6 * k1_s, 2),
+        },
+        "check": check,
+    }
+    pool.close()
+    if args.cpu_budget > 0:
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
