@@ -57,6 +57,31 @@ def split_kernel_bytes(seq_lens, hq, hkv, d, elt):
     return kv + qo // 2 + pt  # K/V, Q, page table, lengths (the output is the combine's)
 
 
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "decode_split_layer_b32_pmc.md")
+SPLIT_SOURCES = ("paper_2609_25782_amd/csrc/decode_attention.hip",
+                 "paper_2609_25782_amd/csrc/device_common.h")
+
+
+def measured_traffic():
+    """HBM bytes per split-kernel launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, calibrated against a copy of known size),
+    or None when the kernel sources changed since the counters were taken."""
+    import hashlib
+    try:
+        text = open(PMC_SUMMARY).read()
+    except OSError:
+        return None
+    fields = dict(l.split(": ", 1) for l in text.splitlines()
+                  if l.startswith(("traffic_bytes_per_launch: ", "kernel_source_sha256: ")))
+    h = hashlib.sha256()
+    for f in SPLIT_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if fields.get("kernel_source_sha256") != h.hexdigest():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(w, budget_s: float):
     """Time the fp64 oracle on whole sessions of the same workload until about
     `budget_s` seconds of oracle time have been spent (at least one session)."""
@@ -98,8 +123,11 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--resume-per-step", type=int, default=8)
+    ap.add_argument("--batch", type=int, default=32, help="active sessions (the workload has 32)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--waves", type=int, default=0, help="override the decode wave count")
+    ap.add_argument("--combine", choices=["fused", "separate"], default="separate",
+                    help="merge split partials in the split kernel's last wave or in a second kernel")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--no-check", action="store_true", help="skip the sampled oracle check")
@@ -117,7 +145,7 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda", 0)
-    w = synth.config_layer(args.seed)
+    w = synth.config_layer(args.seed, batch=args.batch)
     R = args.resume_per_step
     rng = np.random.Generator(np.random.PCG64([args.seed, 7]))
     paused_lens = rng.integers(8192, 32768, size=R, endpoint=True).astype(np.int32)
@@ -147,6 +175,7 @@ def main():
     torch.cuda.synchronize()
     if args.waves:
         pool.set_waves(args.waves)
+    pool.set_combine(args.combine == "fused")
 
     q = torch.from_numpy(synth.queries(w.seed + 1, w.batch, w.num_q_heads, w.head_dim,
                                        w.value_scale, "bf16").view(np.int16)).to(dev).view(torch.bfloat16)
@@ -199,15 +228,17 @@ def main():
     n2, ms2 = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_DECODE_COMBINE)
     n3, ms3 = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
     kv.kv_pool_set_profiling(pool.handle, False)
-    assert n1 == args.steps and n2 == args.steps and n3 == args.steps, (n1, n2, n3)
+    assert n1 == args.steps and n3 == args.steps and n2 == (0 if args.combine == "fused" else args.steps), (n1, n2, n3)
     log("timed %d steps: %.3f ms/step; split %.1f us, combine %.1f us, resume copy %.1f us"
-        % (args.steps, total_ms / args.steps, 1e3 * ms1 / n1, 1e3 * ms2 / n2, 1e3 * ms3 / n3))
+        % (args.steps, total_ms / args.steps, 1e3 * ms1 / n1, 1e3 * ms2 / max(n2, 1), 1e3 * ms3 / n3))
 
     kvb, qo, ptb = decode_bytes(w.seq_lens, w.num_q_heads, w.num_kv_heads, w.head_dim, 2)
     dec_bytes = kvb + qo + ptb
     dec_s = (ms1 + ms2) / 1e3 / args.steps
     value = dec_bytes / dec_s / 1e9
-    k1_bytes = split_kernel_bytes(w.seq_lens, w.num_q_heads, w.num_kv_heads, w.head_dim, 2)
+    # the split kernel's algorithmic bytes: with the fused merge it also writes the output
+    k1_bytes = dec_bytes if args.combine == "fused" else split_kernel_bytes(
+        w.seq_lens, w.num_q_heads, w.num_kv_heads, w.head_dim, 2)
     k1_s = ms1 / 1e3 / n1
     k1_gbs = k1_bytes / k1_s / 1e9
     payload = paused_pages * pool.page_bytes
@@ -233,7 +264,8 @@ def main():
                         "%d paused sessions resumed and evicted per step" % R,
             "batch": w.batch, "total_tokens": int(w.seq_lens.sum()), "num_q_heads": w.num_q_heads,
             "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "layers": 1, "page_tokens": 16,
-            "hot_pages": num_hot, "decode_waves": pool.waves(), "seed": args.seed,
+            "hot_pages": num_hot, "decode_waves": pool.waves(), "combine": args.combine,
+            "seed": args.seed,
         },
         "pct_of_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
         "decode_us": round(1e6 * dec_s, 2),
@@ -254,7 +286,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(k1_gbs / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic() if args.combine == "separate" else None,
             "bytes_per_launch": k1_bytes,
             "us_per_launch": round(1e6 * k1_s, 2),
         },

@@ -48,8 +48,8 @@
  *    exception crosses this boundary.  kv_last_error() gives a message for the
  *    calling thread's last failure.
  *  - All buffers are owned by the caller and must outlive the pool.  The
- *    library owns only host bookkeeping, a small pinned staging ring and a
- *    small device buffer for copy lists.
+ *    library owns only host bookkeeping, a small pinned staging ring, a small
+ *    device buffer for copy lists and a 512 KiB array of decode counters.
  *  - Device work is enqueued on the caller's stream (kv_stream_t is a
  *    hipStream_t; NULL is the default stream) and the call returns without
  *    waiting for it.  Asynchronous device faults surface at the caller's next
@@ -259,6 +259,17 @@ int32_t paged_decode_waves(const kv_pool* pool);
 /* Override the number of decode waves (>= 1); 0 restores the automatic choice. */
 int kv_pool_set_decode_waves(kv_pool* pool, int32_t waves);
 
+enum kv_combine_mode {
+    KV_COMBINE_SEPARATE = 0, /* partials merged by a second kernel (default) */
+    KV_COMBINE_FUSED = 1     /* the last wave of each (row, KV head) merges them; needs a
+                                device-scope release/acquire per partial, which on gfx950
+                                writes back and invalidates the L2 and is slower */
+};
+/* How paged_decode_attention merges its split partials.  The two modes merge
+ * in different orders, so their results agree to float32 rounding, not bit for
+ * bit; each mode on its own is deterministic. */
+int kv_pool_set_decode_combine(kv_pool* pool, int32_t mode);
+
 /* Device workspace bytes paged_decode_attention needs for this batch. */
 size_t paged_decode_workspace_bytes(const kv_pool* pool, int32_t batch, int32_t num_q_heads);
 
@@ -283,6 +294,8 @@ size_t paged_decode_workspace_bytes(const kv_pool* pool, int32_t batch, int32_t 
  *   workspace  device, >= paged_decode_workspace_bytes(), 256-byte aligned
  * Only tokens [0, L) are read: other slots of the tail page and pages past
  * ceil(L / 16) may hold anything, NaN included.
+ * Decode calls of one pool are ordered with each other across streams (they
+ * share the pool's small arrival-counter array).
  * Numerics: bf16 or float32 inputs, float32 accumulation, scores and weights in
  * float32 (bf16 pools round the softmax weights to bf16 for the weighted sum of
  * V and use the same rounded weights in the normaliser).  The result does not

@@ -40,6 +40,16 @@ namespace {
 
 constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9 family)
 
+// Cache-policy bits of the K/V page loads: 2 = nontemporal (streaming).  Every
+// K/V byte is read exactly once per call, so keeping it out of the caches'
+// normal replacement leaves them to page ids, queries and partials.
+#ifndef HCK_DECODE_LOAD_AUX
+#define HCK_DECODE_LOAD_AUX 2
+#endif
+#ifndef HCK_RING_BF16_D128
+#define HCK_RING_BF16_D128 3
+#endif
+
 template <int D, bool BF16>
 struct Shape {
     static constexpr int kElt = BF16 ? 2 : 4;
@@ -91,37 +101,38 @@ __device__ __forceinline__ void load_page(PageRegs<D, BF16>& r, const char* lh_b
                                           ok ? 2 * S::kTile : 0, kRsrcWord3);
 #pragma unroll
     for (int i = 0; i < S::kKLoads; ++i)
-        r.k[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, koff + 1024u * i, 0, 0);
+        r.k[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, koff + 1024u * i, 0, HCK_DECODE_LOAD_AUX);
 #pragma unroll
     for (int c = 0; c < S::kChunks; ++c) {
         if constexpr (BF16)
-            r.v[c] = __builtin_amdgcn_raw_buffer_load_b64(rs, voff + S::kTile + 512u * c, 0, 0);
+            r.v[c] = __builtin_amdgcn_raw_buffer_load_b64(rs, voff + S::kTile + 512u * c, 0, HCK_DECODE_LOAD_AUX);
         else
-            r.v[c] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + S::kTile + 1024u * c, 0, 0);
+            r.v[c] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + S::kTile + 1024u * c, 0, HCK_DECODE_LOAD_AUX);
     }
 }
 
 // S^T tile of one page: lane l gets scores of head l % 16 for tokens 4 (l / 16) + r.
+// Two accumulators halve the dependent MFMA chain; their sum is added once.
 template <int D, bool BF16>
 __device__ __forceinline__ f32x4 page_scores(const PageRegs<D, BF16>& r,
                                              const u32x4 (&q)[Shape<D, BF16>::kKLoads]) {
     using S = Shape<D, BF16>;
-    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < S::kKLoads; ++i) {
+        f32x4& acc = (i & 1) ? s1 : s0;
         if constexpr (BF16) {
-            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, r.k[i]),
-                                                        __builtin_bit_cast(bf16x8, q[i]), s, 0,
-                                                        0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, r.k[i]),
+                                                          __builtin_bit_cast(bf16x8, q[i]), acc, 0,
+                                                          0, 0);
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                s = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(r.k[i][j]),
-                                                         __uint_as_float(q[i][j]), s, 0,
-                                                         0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(r.k[i][j]),
+                                                           __uint_as_float(q[i][j]), acc, 0, 0, 0);
         }
     }
-    return s;
+    return s0 + s1;
 }
 
 // Zero the V slice entries of tokens >= valid (this lane holds tokens 4 qg + j).
@@ -171,11 +182,12 @@ __device__ __forceinline__ void compute_page(SegmentState<D, BF16>& st, PageRegs
         s[r] *= scale_log2;
         mx = fmaxf(mx, s[r]);
     }
-    mx = wave_max_4(mx);
-    const float m_new = fmaxf(st.m, mx);
-    // Rescale only when some head's running max grew; otherwise every factor
-    // would be exactly 1.
-    if (__builtin_amdgcn_ballot_w64(m_new > st.m)) {
+    // The running max m is the same on the four lanes of a head.  Only when some
+    // lane sees a score above it is the page max reduced across lanes and the
+    // accumulators rescaled; otherwise the reduced max would equal m and every
+    // factor would be exactly 1, so skipping is bitwise identical.
+    if (__builtin_amdgcn_ballot_w64(mx > st.m)) {
+        const float m_new = fmaxf(st.m, wave_max_4(mx));
         const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
         st.l *= alpha;
 #pragma unroll
@@ -210,6 +222,107 @@ __device__ __forceinline__ void compute_page(SegmentState<D, BF16>& st, PageRegs
     }
 }
 
+__device__ __forceinline__ void lse_merge(float& M, float& den, f32x4& acc, float m2, float l2,
+                                          const f32x4& o2) {
+    const float Mn = fmaxf(M, m2);
+    const float c1 = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
+    const float c2 = (m2 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m2 - Mn);
+    acc = acc * c1 + o2 * c2;
+    den = den * c1 + l2 * c2;
+    M = Mn;
+}
+
+// Range of waves whose partials belong to segment (b, g): units [u_a, u_a + nb).
+struct SegWaves {
+    int k_first, k_last, pieces;
+};
+
+__device__ __forceinline__ SegWaves seg_waves(int64_t u_a, int nb, int64_t T, int N) {
+    SegWaves w;
+    w.k_first = static_cast<int>(((u_a + 1) * N - 1) / T);
+    w.k_last = static_cast<int>(((u_a + nb) * N - 1) / T);
+    // with more waves than units every non-empty wave holds exactly one unit
+    w.pieces = (N <= T) ? (w.k_last - w.k_first + 1) : nb;
+    return w;
+}
+
+// One wave merges every query head of segment (b, g): lane l owns the items
+// (head, 4-dim quad) l, l + 64, ...; loads of all its items for one partial
+// are issued together.
+template <int D, bool BF16>
+__device__ __forceinline__ void store_quad(const DecodeArgs& a, int64_t orow, const f32x4& res) {
+    if constexpr (BF16) {
+        __bf16 v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = static_cast<__bf16>(res[j]);
+        *reinterpret_cast<u32x2*>(static_cast<__bf16*>(a.out) + orow) = __builtin_bit_cast(u32x2, v);
+    } else {
+        *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + orow) = res;
+    }
+}
+
+// Every query head of (b, g) set to one value (rows with no pages, bad rows).
+template <int D, bool BF16>
+__device__ void fill_segment(const DecodeArgs& a, int b, int g, float value, int lane) {
+    constexpr int kQuads = D / 4;
+    for (int idx = lane; idx < a.group * kQuads; idx += kWave) {
+        const int h = idx / kQuads, quad = idx % kQuads;
+        store_quad<D, BF16>(a, (static_cast<int64_t>(b) * a.num_q_heads + g * a.group + h) * D + 4 * quad,
+                            f32x4{value, value, value, value});
+    }
+}
+
+template <int D, bool BF16>
+__device__ void combine_segment(const DecodeArgs& a, int b, int g, const SegWaves& sw, int64_t T,
+                                int lane) {
+    constexpr int kQuads = D / 4;
+    constexpr int kMaxItems = (16 * kQuads + kWave - 1) / kWave;
+    const int items = a.group * kQuads;
+    const int seg = b * a.num_kv_heads + g;
+    const int N = a.waves;
+    float M[kMaxItems], den[kMaxItems];
+    f32x4 acc[kMaxItems];
+#pragma unroll
+    for (int it = 0; it < kMaxItems; ++it) {
+        M[it] = -INFINITY;
+        den[it] = 0.f;
+        acc[it] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int k = sw.k_first; k <= sw.k_last; ++k) {
+        if (static_cast<int64_t>(k) * T / N == static_cast<int64_t>(k + 1) * T / N) continue;
+        const int64_t slot = static_cast<int64_t>(k) + seg;
+        const float* pml = a.part_ml + slot * 2 * a.group;
+        float mk[kMaxItems], lk[kMaxItems];
+        f32x4 ok[kMaxItems];
+#pragma unroll
+        for (int it = 0; it < kMaxItems; ++it) {
+            const int idx = it * kWave + lane;
+            if (idx < items) {
+                const int h = idx / kQuads, quad = idx % kQuads;
+                mk[it] = pml[h];
+                lk[it] = pml[a.group + h];
+                ok[it] = *reinterpret_cast<const f32x4*>(a.part_o + (slot * a.group + h) * D + 4 * quad);
+            }
+        }
+#pragma unroll
+        for (int it = 0; it < kMaxItems; ++it)
+            if (it * kWave + lane < items) lse_merge(M[it], den[it], acc[it], mk[it], lk[it], ok[it]);
+    }
+    const int32_t L = a.seq_lens[b];
+    const bool invalid = static_cast<int64_t>(L) > kPageTokens * a.pt_stride;
+    const float nan = __builtin_nanf("");
+#pragma unroll
+    for (int it = 0; it < kMaxItems; ++it) {
+        const int idx = it * kWave + lane;
+        if (idx < items) {
+            const int h = idx / kQuads, quad = idx % kQuads;
+            const f32x4 res = invalid ? f32x4{nan, nan, nan, nan} : acc[it] / den[it];
+            store_quad<D, BF16>(a, (static_cast<int64_t>(b) * a.num_q_heads + g * a.group + h) * D + 4 * quad,
+                                res);
+        }
+    }
+}
+
 __device__ __forceinline__ int load_ids(const int32_t* __restrict__ row, int first, int end,
                                         int lane) {
     const int i = first + lane;
@@ -220,7 +333,8 @@ __device__ __forceinline__ int load_ids(const int32_t* __restrict__ row, int fir
 // R page buffers form a ring: while one page is computed, the next R - 1 are
 // in flight.
 template <int D, bool BF16, int R>
-__device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_len, int lane) {
+__device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_len, int lane,
+                          int64_t seg_first_unit, int64_t total_units) {
     using S = Shape<D, BF16>;
     const int h = lane & 15, qg = lane >> 4;
     const bool hvalid = h < a.group;
@@ -294,6 +408,20 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
             pml[a.group + h] = l;
         }
     }
+    if (a.fused) {
+        // The wave that delivers the last partial of (b, g) merges them all.
+        const SegWaves sw = seg_waves(seg_first_unit, nb, total_units, a.waves);
+        int32_t* cnt = a.counters + pc.b * a.num_kv_heads + pc.g;
+        __threadfence();  // release this wave's partial
+        int prev = 0;
+        if (lane == 0) prev = atomicAdd(cnt, 1);
+        prev = __builtin_amdgcn_readfirstlane(__shfl(prev, 0));
+        if (prev + 1 == sw.pieces) {
+            __threadfence();  // acquire the other waves' partials
+            combine_segment<D, BF16>(a, pc.b, pc.g, sw, total_units, lane);
+            if (lane == 0) atomicExch(cnt, 0);  // ready for the next call
+        }
+    }
 }
 
 template <int D, bool BF16, int R>
@@ -304,6 +432,14 @@ __global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs 
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kBlockWaves + threadIdx.x / kWave);
     if (wave >= a.waves) return;
+    if (a.fused) {
+        // rows with no pages get no partials: write them here (0 for L = 0, NaN for L < 0)
+        for (int seg = wave; seg < a.batch * a.num_kv_heads; seg += a.waves) {
+            const int b = seg / a.num_kv_heads;
+            const int32_t L = a.seq_lens[b];
+            if (L <= 0) fill_segment<D, BF16>(a, b, seg % a.num_kv_heads, L == 0 ? 0.f : __builtin_nanf(""), lane);
+        }
+    }
     const int64_t total = static_cast<int64_t>(lds_uniform(s_pref + a.batch)) * a.num_kv_heads;
     int64_t u, u1;
     wave_units(total, wave, a.waves, u, u1);
@@ -313,84 +449,98 @@ __global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs 
         const int nb = lds_uniform(s_pref + pc.b + 1) - lds_uniform(s_pref + pc.b);
         const int32_t L = a.seq_lens[pc.b];
         const int seq_len = L < kPageTokens * nb ? L : kPageTokens * nb;
-        run_piece<D, BF16, R>(a, pc, nb, seq_len, lane);
+        const int64_t seg_first = static_cast<int64_t>(lds_uniform(s_pref + pc.b)) * a.num_kv_heads +
+                                  static_cast<int64_t>(pc.g) * nb;
+        run_piece<D, BF16, R>(a, pc, nb, seq_len, lane, seg_first, total);
         u += pc.p1 - pc.p0;
     }
 }
 
-// Merge the partials of one (b, g) and write the group's output rows.
+// Merge the partials of one (b, g) for one query head and write its output row.
+// One wave per (b, g, h): the D/4 lanes of a lane group each own four output
+// dims, and the wave's lane groups take every kGroups-th partial; loads for
+// four partials are issued before any of them is merged, then the lane groups
+// are merged with cross-lane exchanges.
 template <int D, bool BF16>
 __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArgs a) {
-    __shared__ int64_t s_red[2][kBlockWaves];
+    constexpr int kQuads = D / 4;
+    constexpr int kGroups = kWave / kQuads;
+    constexpr int kUnroll = 4;
     const int seg = blockIdx.x;
+    const int h = blockIdx.y * kBlockWaves + threadIdx.x / kWave;
+    if (h >= a.group) return;
     const int b = seg / a.num_kv_heads, g = seg % a.num_kv_heads;
-    const int tid = threadIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int quad = lane % kQuads, grp = lane / kQuads;
+
     int64_t before = 0, total = 0;
-    for (int r = tid; r < a.batch; r += kBlockThreads) {
+    for (int r = lane; r < a.batch; r += kWave) {
         const int n = row_pages(a.seq_lens[r], a.pt_stride);
         total += n;
         if (r < b) before += n;
     }
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
+    for (int o = kWave / 2; o > 0; o >>= 1) {
         before += __shfl_xor(before, o);
         total += __shfl_xor(total, o);
     }
-    if ((tid & (kWave - 1)) == 0) {
-        s_red[0][tid / kWave] = before;
-        s_red[1][tid / kWave] = total;
-    }
-    __syncthreads();
-    before = s_red[0][0] + s_red[0][1] + s_red[0][2] + s_red[0][3];
-    total = s_red[1][0] + s_red[1][1] + s_red[1][2] + s_red[1][3];
-
     const int32_t L = a.seq_lens[b];
     const bool invalid = L < 0 || static_cast<int64_t>(L) > kPageTokens * a.pt_stride;
     const int nb = row_pages(L, a.pt_stride);
-    const int64_t T = total * a.num_kv_heads;
-    const int64_t u_a = before * a.num_kv_heads + static_cast<int64_t>(g) * nb;
-    const int64_t u_e = u_a + nb;
-    const int N = a.waves;
-    int k_first = 0, k_last = -1;
-    if (!invalid && nb > 0) {
-        k_first = static_cast<int>(((u_a + 1) * N - 1) / T);
-        k_last = static_cast<int>((u_e * N - 1) / T);
-    }
-    constexpr int kQuads = D / 4;
-    for (int idx = tid; idx < a.group * kQuads; idx += kBlockThreads) {
-        const int h = idx / kQuads, d4 = 4 * (idx % kQuads);
-        f32x4 res;
-        if (invalid) {
-            const float nan = __builtin_nanf("");
-            res = f32x4{nan, nan, nan, nan};
-        } else if (nb == 0) {
-            res = f32x4{0.f, 0.f, 0.f, 0.f};
-        } else {
-            float M = -INFINITY, den = 0.f;
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-            for (int k = k_first; k <= k_last; ++k) {
-                if (static_cast<int64_t>(k) * T / N == static_cast<int64_t>(k + 1) * T / N) continue;
-                const int64_t slot = static_cast<int64_t>(k) + seg;
+    f32x4 res;
+    if (invalid) {
+        const float nan = __builtin_nanf("");
+        res = f32x4{nan, nan, nan, nan};
+    } else if (nb == 0) {
+        res = f32x4{0.f, 0.f, 0.f, 0.f};
+    } else {
+        const int64_t T = total * a.num_kv_heads;
+        const int64_t u_a = before * a.num_kv_heads + static_cast<int64_t>(g) * nb;
+        const int64_t u_e = u_a + nb;
+        const int N = a.waves;
+        const int k_first = static_cast<int>(((u_a + 1) * N - 1) / T);
+        const int k_last = static_cast<int>((u_e * N - 1) / T);
+        float M = -INFINITY, den = 0.f;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int k0 = k_first + grp; k0 <= k_last; k0 += kUnroll * kGroups) {
+            float mk[kUnroll], lk[kUnroll];
+            f32x4 ok[kUnroll];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int k = k0 + u * kGroups;
+                // waves whose own unit range is empty wrote nothing to their slot
+                const bool use = k <= k_last &&
+                                 static_cast<int64_t>(k) * T / N != static_cast<int64_t>(k + 1) * T / N;
+                const int64_t slot = static_cast<int64_t>(use ? k : 0) + seg;
                 const float* pml = a.part_ml + slot * 2 * a.group;
-                const float mk = pml[h], lk = pml[a.group + h];
-                const f32x4 ok =
-                    *reinterpret_cast<const f32x4*>(a.part_o + (slot * a.group + h) * D + d4);
-                const float Mn = fmaxf(M, mk);
-                const float c_old = __builtin_amdgcn_exp2f(M - Mn);
-                const float c_new = __builtin_amdgcn_exp2f(mk - Mn);
-                acc = acc * c_old + ok * c_new;
-                den = den * c_old + lk * c_new;
-                M = Mn;
+                const float m_raw = pml[h], l_raw = pml[a.group + h];
+                const f32x4 o_raw =
+                    *reinterpret_cast<const f32x4*>(a.part_o + (slot * a.group + h) * D + 4 * quad);
+                mk[u] = use ? m_raw : -INFINITY;
+                lk[u] = use ? l_raw : 0.f;
+                ok[u] = use ? o_raw : f32x4{0.f, 0.f, 0.f, 0.f};
             }
-            res = acc / den;
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) lse_merge(M, den, acc, mk[u], lk[u], ok[u]);
         }
-        const int64_t orow = (static_cast<int64_t>(b) * a.num_q_heads + g * a.group + h) * D + d4;
+#pragma unroll
+        for (int off = kQuads; off < kWave; off <<= 1) {
+            const float M2 = __shfl_xor(M, off), den2 = __shfl_xor(den, off);
+            f32x4 acc2;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc2[j] = __shfl_xor(acc[j], off);
+            lse_merge(M, den, acc, M2, den2, acc2);
+        }
+        res = acc / den;
+    }
+    if (grp == 0) {
+        const int64_t orow =
+            (static_cast<int64_t>(b) * a.num_q_heads + g * a.group + h) * D + 4 * quad;
         if constexpr (BF16) {
-            __bf16* o = static_cast<__bf16*>(a.out) + orow;
             __bf16 v[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) v[j] = static_cast<__bf16>(res[j]);
-            *reinterpret_cast<u32x2*>(o) = __builtin_bit_cast(u32x2, v);
+            *reinterpret_cast<u32x2*>(static_cast<__bf16*>(a.out) + orow) = __builtin_bit_cast(u32x2, v);
         } else {
             *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + orow) = res;
         }
@@ -401,7 +551,7 @@ __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArg
 // waves per SIMD, i.e. at most 256 (168) VGPRs.
 template <int D, bool BF16>
 constexpr int ring_depth() {
-    return BF16 ? (D == 128 ? 3 : 5) : (D == 128 ? 2 : 3);
+    return BF16 ? (D == 128 ? HCK_RING_BF16_D128 : 5) : (D == 128 ? 2 : 3);
 }
 
 template <int D, bool BF16>
@@ -446,10 +596,11 @@ hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hip
 hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s) {
     const void* k = pick_combine(head_dim, dtype);
     if (!k) return hipErrorInvalidValue;
-    const int blocks = a.batch * a.num_kv_heads;
-    if (blocks == 0) return hipSuccess;
+    const int segs = a.batch * a.num_kv_heads;
+    if (segs == 0) return hipSuccess;
     void* args[] = {const_cast<DecodeArgs*>(&a)};
-    return hipLaunchKernel(k, dim3(blocks), dim3(kBlockThreads), args, 0, s);
+    return hipLaunchKernel(k, dim3(segs, (a.group + kBlockWaves - 1) / kBlockWaves),
+                           dim3(kBlockThreads), args, 0, s);
 }
 
 int decode_split_blocks_per_cu(int head_dim, int dtype, int batch) {

@@ -31,6 +31,8 @@ struct DecodeArgs {
     float* part_o;            // [slots][group][head_dim] unnormalised partial outputs
     float* part_ml;           // [slots][2][group] running max (log2 domain) and weight sum
     void* out;                // [batch][num_q_heads][head_dim]
+    int32_t* counters;        // [batch * num_kv_heads] arrival counters, zero between calls
+    int32_t fused;            // 1: the last wave of each (b, g) merges its partials
 };
 
 // Bytes of partial results for `slots` slots.
@@ -40,6 +42,8 @@ inline size_t decode_partials_bytes(int64_t slots, int group, int head_dim) {
 
 hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s);
 hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s);
+// Largest batch the decode kernels accept (bounds the counter array).
+constexpr int kMaxDecodeBatch = 8192;
 // Resident 256-thread blocks per CU of the split kernel (0 if unsupported shape).
 int decode_split_blocks_per_cu(int head_dim, int dtype, int batch);
 

@@ -90,7 +90,11 @@ struct Session {
 constexpr int kStagingSlots = 4;
 constexpr size_t kStagingBytes = size_t(1) << 20;
 constexpr int32_t kStagingEntries = static_cast<int32_t>(kStagingBytes / sizeof(hck::CopyEntry));
-constexpr int32_t kMaxDecodeBatch = 8192;
+constexpr int32_t kMaxDecodeBatch = hck::kMaxDecodeBatch;
+#ifndef HCK_DECODE_WAVES_PER_CU
+#define HCK_DECODE_WAVES_PER_CU 3
+#endif
+constexpr int32_t kDecodeWavesPerCu = HCK_DECODE_WAVES_PER_CU;
 
 struct StagingSlot {
     void* host = nullptr;  // pinned
@@ -162,6 +166,10 @@ struct kv_pool {
     hipEvent_t free_event = nullptr;
     bool free_pending = false;
     bool profiling = false;
+    int32_t combine_mode = KV_COMBINE_SEPARATE;
+    int32_t* counters = nullptr;  // decode arrival counters, zero between calls
+    hipEvent_t decode_event = nullptr;
+    bool decode_pending = false;
     std::vector<ProfRec> prof[KV_KERNEL_COUNT];
     std::vector<hipEvent_t> spare_events;
 
@@ -175,6 +183,11 @@ struct kv_pool {
             if (s.done) (void)hipEventDestroy(s.done);
         }
         if (free_event) (void)hipEventDestroy(free_event);
+        if (decode_event) {
+            (void)hipEventSynchronize(decode_event);
+            (void)hipEventDestroy(decode_event);
+        }
+        if (counters) (void)hipFree(counters);
         for (auto& v : prof)
             for (auto& r : v) {
                 (void)hipEventDestroy(r.start);
@@ -302,11 +315,9 @@ struct kv_pool {
         if (--cold_ref[c] == 0) cold_free.give(c);
     }
 
-    int32_t auto_waves() const {
-        const int per_cu = hck::decode_split_blocks_per_cu(d.head_dim, d.dtype, 0);
-        const int32_t w = cus * std::max(1, per_cu) * hck::kBlockWavesHost;
-        return std::max<int32_t>(w, 1);
-    }
+    // Three waves per CU: enough loads in flight to saturate HBM with the
+    // register ring, without the extra partials and DRAM contention of more.
+    int32_t auto_waves() const { return std::max<int32_t>(cus * kDecodeWavesPerCu, 1); }
     int32_t decode_waves() const { return waves_override > 0 ? waves_override : auto_waves(); }
 };
 
@@ -373,9 +384,20 @@ int kv_pool_create(const kv_pool_desc* desc, void* hot_base, size_t hot_bytes, v
                 return fail(KV_ERR_OOM, "staging allocation failed");
             }
         }
-        if (hipEventCreateWithFlags(&p->free_event, hipEventDisableTiming) != hipSuccess) {
+        if (hipEventCreateWithFlags(&p->free_event, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&p->decode_event, hipEventDisableTiming) != hipSuccess) {
             delete p;
             return fail(KV_ERR_OOM, "event creation failed");
+        }
+        const int64_t ncnt = static_cast<int64_t>(kMaxDecodeBatch) * 16;
+        if (hipMalloc(&p->counters, ncnt * sizeof(int32_t)) != hipSuccess) {
+            delete p;
+            return fail(KV_ERR_OOM, "counter allocation failed");
+        }
+        e = hck::launch_fill_i32(p->counters, ncnt, 0, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) {
+            delete p;
+            return hip_fail(e, "counter fill");
         }
         e = hck::launch_fill_i32(page_table,
                                  static_cast<int64_t>(desc->max_sessions) * desc->max_pages_per_session,
@@ -679,6 +701,13 @@ int32_t paged_decode_waves(const kv_pool* pool) {
     return pool->decode_waves();
 }
 
+int kv_pool_set_decode_combine(kv_pool* pool, int32_t mode) {
+    if (!pool || (mode != KV_COMBINE_SEPARATE && mode != KV_COMBINE_FUSED))
+        return fail(KV_ERR_INVALID, "bad arguments");
+    pool->combine_mode = mode;
+    return KV_OK;
+}
+
 int kv_pool_set_decode_waves(kv_pool* pool, int32_t waves) {
     if (!pool || waves < 0) return fail(KV_ERR_INVALID, "bad arguments");
     pool->waves_override = waves;
@@ -741,15 +770,27 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
     a.part_o = static_cast<float*>(workspace);
     a.part_ml = a.part_o + slots * group * pool->d.head_dim;
     a.out = out;
+    a.counters = pool->counters;
+    a.fused = pool->combine_mode == KV_COMBINE_FUSED ? 1 : 0;
     hipStream_t st = pool->strm(stream);
+    // decode calls of one pool share its counters: order them across streams
+    if (pool->decode_pending) {
+        hipError_t w = hipStreamWaitEvent(st, pool->decode_event, 0);
+        if (w != hipSuccess) return hip_fail(w, "hipStreamWaitEvent(decode)");
+    }
     hipEvent_t p = pool->prof_begin(st);
     hipError_t e = hck::launch_decode_split(a, pool->d.head_dim, pool->d.dtype, st);
     pool->prof_end(KV_KERNEL_DECODE_SPLIT, p, st);
     if (e != hipSuccess) return hip_fail(e, "decode split launch");
-    p = pool->prof_begin(st);
-    e = hck::launch_decode_combine(a, pool->d.head_dim, pool->d.dtype, st);
-    pool->prof_end(KV_KERNEL_DECODE_COMBINE, p, st);
-    if (e != hipSuccess) return hip_fail(e, "decode combine launch");
+    if (!a.fused) {
+        p = pool->prof_begin(st);
+        e = hck::launch_decode_combine(a, pool->d.head_dim, pool->d.dtype, st);
+        pool->prof_end(KV_KERNEL_DECODE_COMBINE, p, st);
+        if (e != hipSuccess) return hip_fail(e, "decode combine launch");
+    }
+    e = hipEventRecord(pool->decode_event, st);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord(decode)");
+    pool->decode_pending = true;
     return KV_OK;
 }
 

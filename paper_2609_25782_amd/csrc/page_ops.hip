@@ -16,32 +16,38 @@
 namespace hck {
 namespace {
 
-constexpr int kCopyUnroll = 8;  // 16-byte loads in flight per thread
-constexpr int64_t kCopyChunk = static_cast<int64_t>(kBlockThreads) * kCopyUnroll * 16;
+#ifndef HCK_COPY_NONTEMPORAL
+#define HCK_COPY_NONTEMPORAL 1
+#endif
 
+// A block copies `U` x 4 KiB of one page: every thread moves U 16-byte words,
+// all loads issued before the first store.  The host picks U so that the
+// chunk divides the page, so the body has no bounds checks (pages are always a
+// multiple of 4 KiB: two tiles of at least 2 KiB per layer and KV head).
+template <int U>
 __global__ __launch_bounds__(kBlockThreads) void page_copy_kernel(
     const char* __restrict__ src_base, char* __restrict__ dst_base, int64_t page_bytes,
     const CopyEntry* __restrict__ entries, int32_t n, int chunks_per_page,
     int32_t* __restrict__ page_table) {
-    const int64_t flat = blockIdx.x;
-    const int ent = static_cast<int>(flat / chunks_per_page);
-    const int chunk = static_cast<int>(flat % chunks_per_page);
+    const int ent = static_cast<int>(blockIdx.x / chunks_per_page);
+    const int chunk = static_cast<int>(blockIdx.x % chunks_per_page);
     if (ent >= n) return;
     const CopyEntry e = entries[ent];
-    const int64_t base = static_cast<int64_t>(chunk) * kCopyChunk;
-    const u32x4* s = reinterpret_cast<const u32x4*>(src_base + e.src * page_bytes + base);
-    u32x4* d = reinterpret_cast<u32x4*>(dst_base + e.dst * page_bytes + base);
-    const int64_t left = (page_bytes - base) / 16;  // 16-byte words left in this page
-    u32x4 buf[kCopyUnroll];
+    const int64_t base = static_cast<int64_t>(chunk) * U * kBlockThreads * 16;
+    const u32x4* s =
+        reinterpret_cast<const u32x4*>(src_base + e.src * page_bytes + base) + threadIdx.x;
+    u32x4* d = reinterpret_cast<u32x4*>(dst_base + e.dst * page_bytes + base) + threadIdx.x;
+    u32x4 buf[U];
 #pragma unroll
-    for (int i = 0; i < kCopyUnroll; ++i) {
-        const int64_t w = static_cast<int64_t>(i) * kBlockThreads + threadIdx.x;
-        if (w < left) buf[i] = __builtin_nontemporal_load(s + w);
-    }
+    for (int i = 0; i < U; ++i)
+        buf[i] = HCK_COPY_NONTEMPORAL ? __builtin_nontemporal_load(s + i * kBlockThreads)
+                                      : s[i * kBlockThreads];
 #pragma unroll
-    for (int i = 0; i < kCopyUnroll; ++i) {
-        const int64_t w = static_cast<int64_t>(i) * kBlockThreads + threadIdx.x;
-        if (w < left) __builtin_nontemporal_store(buf[i], d + w);
+    for (int i = 0; i < U; ++i) {
+        if (HCK_COPY_NONTEMPORAL)
+            __builtin_nontemporal_store(buf[i], d + i * kBlockThreads);
+        else
+            d[i * kBlockThreads] = buf[i];
     }
     if (chunk == 0 && threadIdx.x == 0 && e.pt_index >= 0) page_table[e.pt_index] = e.dst;
 }
@@ -211,11 +217,21 @@ hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_b
                             const CopyEntry* entries, int32_t n, int32_t* page_table,
                             hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    const int chunks = static_cast<int>((page_bytes + kCopyChunk - 1) / kCopyChunk);
-    const int64_t blocks = static_cast<int64_t>(chunks) * n;
+    constexpr int64_t kRow = static_cast<int64_t>(kBlockThreads) * 16;  // 4 KiB
+    if (page_bytes % kRow) return hipErrorInvalidValue;
+    const int64_t rows = page_bytes / kRow;
+    const int u = rows % 8 == 0 ? 8 : rows % 4 == 0 ? 4 : rows % 2 == 0 ? 2 : 1;
+    const int64_t chunks = rows / u;
+    const int64_t blocks = chunks * n;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(page_copy_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kBlockThreads), 0,
-                       s, src_base, dst_base, page_bytes, entries, n, chunks, page_table);
+    const dim3 grid(static_cast<unsigned>(blocks)), block(kBlockThreads);
+    const int cpp = static_cast<int>(chunks);
+    switch (u) {
+        case 8: hipLaunchKernelGGL(page_copy_kernel<8>, grid, block, 0, s, src_base, dst_base, page_bytes, entries, n, cpp, page_table); break;
+        case 4: hipLaunchKernelGGL(page_copy_kernel<4>, grid, block, 0, s, src_base, dst_base, page_bytes, entries, n, cpp, page_table); break;
+        case 2: hipLaunchKernelGGL(page_copy_kernel<2>, grid, block, 0, s, src_base, dst_base, page_bytes, entries, n, cpp, page_table); break;
+        default: hipLaunchKernelGGL(page_copy_kernel<1>, grid, block, 0, s, src_base, dst_base, page_bytes, entries, n, cpp, page_table); break;
+    }
     return hipGetLastError();
 }
 

@@ -25,6 +25,7 @@ KV_COLD_DEVICE, KV_COLD_PINNED_HOST = 0, 1
 KV_SESSION_FREE, KV_SESSION_ACTIVE, KV_SESSION_PAUSED = 0, 1, 2
 KV_POOL_METADATA_ONLY = 1
 KV_KERNEL_DECODE_SPLIT, KV_KERNEL_DECODE_COMBINE, KV_KERNEL_PAGE_COPY = 0, 1, 2
+KV_COMBINE_SEPARATE, KV_COMBINE_FUSED = 0, 1
 
 
 class KVError(RuntimeError):
@@ -77,6 +78,7 @@ _SIGS = {
     "kv_resume_sessions": (ctypes.c_int, [_P, _PI32, _I32, _P]),
     "paged_decode_waves": (_I32, [_P]),
     "kv_pool_set_decode_waves": (ctypes.c_int, [_P, _I32]),
+    "kv_pool_set_decode_combine": (ctypes.c_int, [_P, _I32]),
     "paged_decode_workspace_bytes": (_SZ, [_P, _I32, _I32]),
     "paged_decode_attention": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _I32, _I32,
                                               ctypes.c_float, _P, _P, _SZ, _P]),
@@ -204,6 +206,10 @@ def paged_decode_waves(pool: int) -> int:
 
 def kv_pool_set_decode_waves(pool: int, waves: int) -> None:
     _check(_lib.kv_pool_set_decode_waves(pool, waves), "kv_pool_set_decode_waves")
+
+
+def kv_pool_set_decode_combine(pool: int, mode: int) -> None:
+    _check(_lib.kv_pool_set_decode_combine(pool, mode), "kv_pool_set_decode_combine")
 
 
 def paged_decode_workspace_bytes(pool: int, batch: int, num_q_heads: int) -> int:

@@ -135,3 +135,6 @@ class HotColdPool:
 
     def set_waves(self, waves: int) -> None:
         kv.kv_pool_set_decode_waves(self.handle, waves)
+
+    def set_combine(self, fused: bool) -> None:
+        kv.kv_pool_set_decode_combine(self.handle, kv.KV_COMBINE_FUSED if fused else kv.KV_COMBINE_SEPARATE)

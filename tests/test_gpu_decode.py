@@ -31,15 +31,16 @@ def _say(*a):
     sys.stdout.flush()
 
 
-def _run(case: Case, dev, poison=False, waves=None, scale=None, pool=None):
-    _say("decode case: dtype=%s D=%d Hq=%d Hkv=%d NL=%d layer=%d lens=%s waves=%s" % (
+def _run(case: Case, dev, poison=False, waves=None, scale=None, pool=None, fused=True):
+    _say("decode case: dtype=%s D=%d Hq=%d Hkv=%d NL=%d layer=%d lens=%s waves=%s fused=%s" % (
         case.dtype, case.head_dim, case.num_q_heads, case.num_kv_heads, case.num_layers, case.layer,
-        case.seq_lens[:8], waves))
+        case.seq_lens[:8], waves, fused))
     own = pool is None
     if own:
         pool = build_gpu(case, dev, poison=poison)
     if waves:
         pool.set_waves(waves)
+    pool.set_combine(fused)
     q = to_device(case.q, case.dtype, dev)
     sl = torch.tensor(case.seq_lens, dtype=torch.int32, device=dev)
     out = pool.decode(case.layer, q, sl, scale=scale)
@@ -78,12 +79,21 @@ def test_group_of_16_and_multilayer(dev):
     tolerance_check(got, case.oracle_out())
 
 
+@pytest.mark.parametrize("fused", [True, False])
 @pytest.mark.parametrize("waves", [1, 3, 7, 64, 1000, 5000])
-def test_split_invariance(dev, waves):
-    """Any number of waves gives the oracle's answer within tolerance (P10)."""
+def test_split_invariance(dev, waves, fused):
+    """Any number of waves, either merge of the partials: the oracle's answer
+    within tolerance (P10)."""
     case = Case(1, 32, 4, 128, "bf16", [5000, 16, 1, 777, 3000, 48], seed=5)
-    got = _run(case, dev, waves=waves)
+    got = _run(case, dev, waves=waves, fused=fused)
     tolerance_check(got, case.oracle_out())
+
+
+@pytest.mark.parametrize("dtype,D,hq,hkv", [("bf16", 128, 32, 4), ("f32", 64, 16, 1), ("bf16", 64, 16, 1)])
+def test_separate_combine(dev, dtype, D, hq, hkv):
+    case = Case(1, hq, hkv, D, dtype, [1, 15, 16, 17, 100, 3000, 250], seed=16)
+    got = _run(case, dev, fused=False)
+    tolerance_check(got, case.oracle_out(), 1e-2, 1e-2 if dtype == "bf16" else 1e-5)
 
 
 def test_layer_shape_scaled_values(dev):
@@ -96,9 +106,11 @@ def test_layer_shape_scaled_values(dev):
     _say("layer shape scaled: abs %.3g norm %.3g" % (err, norm))
 
 
-def test_zero_and_invalid_lengths(dev):
+@pytest.mark.parametrize("fused", [True, False])
+def test_zero_and_invalid_lengths(dev, fused):
     case = Case(1, 8, 2, 64, "bf16", [40, 0, 70], seed=7)
     pool = build_gpu(case, dev)
+    pool.set_combine(fused)
     q = to_device(case.q, "bf16", dev)
     sl = torch.tensor([40, 0, 70], dtype=torch.int32, device=dev)
     out = to_host(pool.decode(0, q, sl))
@@ -111,12 +123,18 @@ def test_zero_and_invalid_lengths(dev):
     torch.cuda.synchronize()
     assert np.all(np.isnan(out2[1])) and np.all(np.isnan(out2[2]))
     assert np.array_equal(out2[0], out[0])
+    # the next call is clean again (the fused merge's counters reset themselves)
+    out3 = to_host(pool.decode(0, q, sl))
+    torch.cuda.synchronize()
+    assert np.array_equal(out3, out)
     pool.close()
 
 
-def test_out_of_range_page_id_gives_nan(dev):
+@pytest.mark.parametrize("fused", [True, False])
+def test_out_of_range_page_id_gives_nan(dev, fused):
     case = Case(1, 8, 2, 64, "bf16", [40, 70], seed=8)
     pool = build_gpu(case, dev)
+    pool.set_combine(fused)
     q = to_device(case.q, "bf16", dev)
     sl = torch.tensor(case.seq_lens, dtype=torch.int32, device=dev)
     pt = pool.page_table[:2].clone()
@@ -224,4 +242,24 @@ def test_partition_table_matches_reference(dev):
         got = pool.partition(sl, waves).cpu().numpy()
         want = np.array(partition.slot_table(lens, 4, waves), dtype=np.int32)
         assert np.array_equal(got, want)
+    pool.close()
+
+
+def test_repeated_calls_and_batch_changes_are_consistent(dev):
+    """Back-to-back calls with different batches on one pool: every call matches
+    its own first result (the merge counters return to zero after each call)."""
+    case = Case(1, 32, 4, 128, "bf16", [3000, 17, 900, 4096, 1, 64], seed=17)
+    pool = build_gpu(case, dev)
+    q = to_device(case.q, "bf16", dev)
+    sl = torch.tensor(case.seq_lens, dtype=torch.int32, device=dev)
+    first = to_host(pool.decode(0, q, sl))
+    sub = to_host(pool.decode(0, q[2:5].contiguous(), sl[2:5].contiguous(),
+                              page_table=pool.page_table[2:5].contiguous()))
+    for _ in range(5):
+        again = to_host(pool.decode(0, q, sl))
+        assert np.array_equal(again, first)
+    assert np.array_equal(to_host(pool.decode(0, q[2:5].contiguous(), sl[2:5].contiguous(),
+                                              page_table=pool.page_table[2:5].contiguous())), sub)
+    torch.cuda.synchronize()
+    tolerance_check(first, case.oracle_out())
     pool.close()
