@@ -117,6 +117,116 @@ def cpu_baseline(w, budget_s: float):
                           sessions, int(np.sum(w.seq_lens[:sessions])), spent)}
 
 
+def measure_resume_mix(seed: int, steps: int, warmup: int):
+    """Resume-heavy mix at 48 layers: 32 active sessions (8K-32K tokens), 1,024 paused
+    sessions of 32K-128K tokens over a physical cold pool of 49,152 pages, 8 resumes
+    per step.  Times the batched resume alone, the 48-layer decode of the active
+    sessions alone, and both together on two streams (TBT impact)."""
+    import torch
+    import synth
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+
+    w = synth.config_resume_mix(seed)
+    dev = torch.device("cuda", 0)
+    stride = synth.pages_for(131072)
+    n_paused = len(w.paused_lens)
+    pool = HotColdPool(48, 4, 128, "bf16", w.hot_pages, w.cold_pages, w.batch + n_paused, stride)
+    mult = float(synth.value_multiplier(w.value_scale))
+    for b in range(w.batch):
+        pool.create_session(int(w.seq_lens[b]), [int(p) for p in w.placement[b]])
+        pool.fill_synthetic(b, b, w.seed, mult)
+    paused = [pool.import_cold(int(L), synth.cold_page_draw(w.seed, j, synth.pages_for(int(L)), w.cold_pages))
+              for j, L in enumerate(w.paused_lens)]
+    log("resume mix: %d hot pages, %d cold pages, %d paused sessions imported" % (
+        w.hot_pages, w.cold_pages, n_paused))
+    q = torch.from_numpy(synth.queries(w.seed + 1, w.batch, 32, 128, w.value_scale, "bf16")
+                         .view(np.int16)).to(dev).view(torch.bfloat16)
+    sl = torch.from_numpy(w.seq_lens.copy()).to(dev)
+    pt = pool.page_table[:w.batch]
+    out = torch.empty_like(q)
+    rng = np.random.Generator(np.random.PCG64([seed, 11]))
+    picks = [[paused[i] for i in rng.choice(n_paused, size=8, replace=False)]
+             for _ in range(warmup + 3 * steps)]
+    side = torch.cuda.Stream()
+    main_s = torch.cuda.current_stream()
+
+    def decode48(stream):
+        for layer in range(48):
+            pool.decode(layer, q, sl, page_table=pt, out=out, stream=stream)
+
+    def resume_batch(sids, stream):
+        pool.resume(sids, stream=stream)
+        for sid in sids:
+            pool.evict(sid, stream=stream)
+
+    def timed(fn, stream, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(n):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    k = 0
+    for _ in range(warmup):
+        resume_batch(picks[k], main_s)
+        k += 1
+        decode48(main_s)
+    torch.cuda.synchronize()
+    decode_ms = timed(lambda i: decode48(main_s), main_s, steps)
+    # resume alone: kernel time from the profiling hook, host time of the call
+    kv.kv_pool_set_profiling(pool.handle, True)
+    kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
+    payload, host_s = 0, 0.0
+    for i in range(steps):
+        sids = picks[k]
+        k += 1
+        for sid in sids:
+            payload += synth.pages_for(pool.info(sid)[1]) * pool.page_bytes
+        torch.cuda.synchronize()  # the call's own host cost, not a wait for a staging slot
+        t0 = time.perf_counter()
+        pool.resume(sids, stream=main_s)
+        host_s += time.perf_counter() - t0
+        for sid in sids:
+            pool.evict(sid, stream=main_s)
+    torch.cuda.synchronize()
+    n_copy, copy_ms = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
+    kv.kv_pool_set_profiling(pool.handle, False)
+    # both at once: resumes on a second stream while the 48 layers decode
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(2 * steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        side.wait_stream(main_s)
+        resume_batch(picks[k], side)
+        k += 1
+        e[2 * i].record(main_s)
+        decode48(main_s)
+        e[2 * i + 1].record(main_s)
+        main_s.wait_stream(side)
+    torch.cuda.synchronize()
+    both_ms = sum(e[2 * i].elapsed_time(e[2 * i + 1]) for i in range(steps)) / steps
+    pool.close()
+    del pool
+    torch.cuda.empty_cache()
+    per_session_ms = copy_ms / (8 * steps)
+    gbs = 2 * payload / (copy_ms / 1e3) / 1e9
+    return {
+        "workload": "48 layers, 32q/4kv heads, d=128, bf16, 1.5 MiB pages; 1024 paused sessions "
+                    "U[32768,131072] over %d physical cold pages; 8 resumed per step" % w.cold_pages,
+        "ms_per_session": round(per_session_ms, 4),
+        "mean_session_bytes": int(payload / (8 * steps)),
+        "copy_GBps": round(gbs, 1),
+        "frac_of_copy_roofline": round(gbs / HBM_PEAK_GBS, 4),
+        "host_ms_per_call": round(1e3 * host_s / steps, 3),
+        "decode48_ms": round(decode_ms, 3),
+        "decode48_ms_with_concurrent_resume": round(both_ms, 3),
+        "tbt_impact": round(both_ms / decode_ms, 3),
+        "decode48_GBps": round(48 * sum(decode_bytes(w.seq_lens, 32, 4, 128, 2)) / (decode_ms / 1e3) / 1e9, 1),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -131,6 +241,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--no-check", action="store_true", help="skip the sampled oracle check")
+    ap.add_argument("--no-resume-mix", action="store_true",
+                    help="skip the 48-layer resume-heavy measurement (needs ~235 GB of HBM)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -293,6 +405,11 @@ def main():
         "check": check,
     }
     pool.close()
+    del pool
+    torch.cuda.empty_cache()
+    if not args.no_resume_mix:
+        result["resume48"] = measure_resume_mix(args.seed, max(3, args.steps // 4), 1)
+        log("resume mix: %s" % json.dumps(result["resume48"]))
     if args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
     print(json.dumps(result), flush=True)

@@ -19,37 +19,47 @@ namespace {
 #ifndef HCK_COPY_NONTEMPORAL
 #define HCK_COPY_NONTEMPORAL 1
 #endif
+// Persistent copy grid: at most this many blocks (64 per CU on 256 CUs;
+// measured best for multi-GB resumes of 1.5 MiB pages).
+#ifndef HCK_COPY_MAX_BLOCKS
+#define HCK_COPY_MAX_BLOCKS 16384
+#endif
 
-// A block copies `U` x 4 KiB of one page: every thread moves U 16-byte words,
-// all loads issued before the first store.  The host picks U so that the
-// chunk divides the page, so the body has no bounds checks (pages are always a
-// multiple of 4 KiB: two tiles of at least 2 KiB per layer and KV head).
+// A block copies chunks of `U` x 4 KiB: every thread moves U 16-byte words, all
+// loads issued before the first store.  The host picks U so that a chunk
+// divides the page, so the body has no bounds checks (pages are always a
+// multiple of 4 KiB: two tiles of at least 2 KiB per layer and KV head).  The
+// grid is persistent: block i takes chunks i, i + grid, ... of the whole copy
+// list, so a multi-GB resume is a few thousand long-lived blocks rather than
+// millions of short ones.
 template <int U>
 __global__ __launch_bounds__(kBlockThreads) void page_copy_kernel(
     const char* __restrict__ src_base, char* __restrict__ dst_base, int64_t page_bytes,
     const CopyEntry* __restrict__ entries, int32_t n, int chunks_per_page,
     int32_t* __restrict__ page_table) {
-    const int ent = static_cast<int>(blockIdx.x / chunks_per_page);
-    const int chunk = static_cast<int>(blockIdx.x % chunks_per_page);
-    if (ent >= n) return;
-    const CopyEntry e = entries[ent];
-    const int64_t base = static_cast<int64_t>(chunk) * U * kBlockThreads * 16;
-    const u32x4* s =
-        reinterpret_cast<const u32x4*>(src_base + e.src * page_bytes + base) + threadIdx.x;
-    u32x4* d = reinterpret_cast<u32x4*>(dst_base + e.dst * page_bytes + base) + threadIdx.x;
-    u32x4 buf[U];
+    const int64_t total = static_cast<int64_t>(n) * chunks_per_page;
+    for (int64_t flat = blockIdx.x; flat < total; flat += gridDim.x) {
+        const int ent = static_cast<int>(flat / chunks_per_page);
+        const int chunk = static_cast<int>(flat % chunks_per_page);
+        const CopyEntry e = entries[ent];
+        const int64_t base = static_cast<int64_t>(chunk) * U * kBlockThreads * 16;
+        const u32x4* s =
+            reinterpret_cast<const u32x4*>(src_base + e.src * page_bytes + base) + threadIdx.x;
+        u32x4* d = reinterpret_cast<u32x4*>(dst_base + e.dst * page_bytes + base) + threadIdx.x;
+        u32x4 buf[U];
 #pragma unroll
-    for (int i = 0; i < U; ++i)
-        buf[i] = HCK_COPY_NONTEMPORAL ? __builtin_nontemporal_load(s + i * kBlockThreads)
-                                      : s[i * kBlockThreads];
+        for (int i = 0; i < U; ++i)
+            buf[i] = HCK_COPY_NONTEMPORAL ? __builtin_nontemporal_load(s + i * kBlockThreads)
+                                          : s[i * kBlockThreads];
 #pragma unroll
-    for (int i = 0; i < U; ++i) {
-        if (HCK_COPY_NONTEMPORAL)
-            __builtin_nontemporal_store(buf[i], d + i * kBlockThreads);
-        else
-            d[i * kBlockThreads] = buf[i];
+        for (int i = 0; i < U; ++i) {
+            if (HCK_COPY_NONTEMPORAL)
+                __builtin_nontemporal_store(buf[i], d + i * kBlockThreads);
+            else
+                d[i * kBlockThreads] = buf[i];
+        }
+        if (chunk == 0 && threadIdx.x == 0 && e.pt_index >= 0) page_table[e.pt_index] = e.dst;
     }
-    if (chunk == 0 && threadIdx.x == 0 && e.pt_index >= 0) page_table[e.pt_index] = e.dst;
 }
 
 __global__ __launch_bounds__(kBlockThreads) void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
@@ -222,8 +232,8 @@ hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_b
     const int64_t rows = page_bytes / kRow;
     const int u = rows % 8 == 0 ? 8 : rows % 4 == 0 ? 4 : rows % 2 == 0 ? 2 : 1;
     const int64_t chunks = rows / u;
-    const int64_t blocks = chunks * n;
-    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const int64_t work = chunks * n;
+    const int64_t blocks = work < HCK_COPY_MAX_BLOCKS ? work : HCK_COPY_MAX_BLOCKS;
     const dim3 grid(static_cast<unsigned>(blocks)), block(kBlockThreads);
     const int cpp = static_cast<int>(chunks);
     switch (u) {
