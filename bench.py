@@ -4,8 +4,9 @@
 One step is one pass of the whole hot path over one batch:
   1. resume R paused sessions (batched cold -> hot gather + page-table rewrite),
   2. paged GQA decode attention over the B active sessions (split + combine),
-  3. evict the R sessions again (write-on-evict: their cold copies are still
-     valid, so no page is rewritten; rows are cleared and pages freed).
+  3. evict the R sessions again in one batched call (write-on-evict: their
+     cold copies are still valid, so no page is rewritten; rows are cleared and
+     pages freed).
 
 Default workload: one Qwen3-Coder-30B-A3B-shaped attention layer (32 query /
 4 KV heads, head_dim 128, bf16, 16-token pages), 32 active sessions with
@@ -157,8 +158,7 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
 
     def resume_batch(sids, stream):
         pool.resume(sids, stream=stream)
-        for sid in sids:
-            pool.evict(sid, stream=stream)
+        pool.evict(sids, stream=stream)
 
     def timed(fn, stream, n):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -189,8 +189,7 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
         t0 = time.perf_counter()
         pool.resume(sids, stream=main_s)
         host_s += time.perf_counter() - t0
-        for sid in sids:
-            pool.evict(sid, stream=main_s)
+        pool.evict(sids, stream=main_s)
     torch.cuda.synchronize()
     n_copy, copy_ms = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
     kv.kv_pool_set_profiling(pool.handle, False)
@@ -282,8 +281,7 @@ def main():
         sid = pool.create_session(int(L))
         pool.fill_synthetic(sid, w.batch + j, w.seed, mult)
         paused.append(sid)
-    for sid in paused:
-        pool.evict(sid)
+    pool.evict(paused)
     torch.cuda.synchronize()
     if args.waves:
         pool.set_waves(args.waves)
@@ -299,8 +297,7 @@ def main():
     def step():
         pool.resume(paused)
         pool.decode(0, q, seq, page_table=pt, scale=scale, out=out)
-        for sid in paused:
-            pool.evict(sid)
+        pool.evict(paused)
 
     for i in range(args.warmup):
         step()

@@ -233,6 +233,10 @@ int kv_fill_synthetic(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed
  */
 int kv_evict_session(kv_pool* pool, int32_t sid, kv_stream_t stream);
 
+/* Batched eviction: sessions in argument order, atomic as a whole, one launch
+ * for all copies and row clears.  Errors as kv_evict_session. */
+int kv_evict_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t stream);
+
 /*
  * Resume a PAUSED session (data path 2; Sec. III, "Eviction, resume and
  * decode": the KV is brought back into the fast tier before the session runs).

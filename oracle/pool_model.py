@@ -150,6 +150,25 @@ class PoolModel:
         self.evicts += 1
         return copies
 
+    def evict_many(self, sids: Sequence[int]):
+        """Batched eviction, atomic as a whole: sessions in argument order.
+        Returns the (hot_src, cold_dst) copies of all of them."""
+        sids = [int(x) for x in sids]
+        if len(set(sids)) != len(sids):
+            raise ModelError(ERR_INVALID, "duplicate session")
+        dirty = 0
+        for sid in sids:
+            s = self._session(sid)
+            if s.state != ACTIVE:
+                raise ModelError(ERR_STATE, "not active")
+            dirty += sum(1 for c in s.cold if c < 0)
+        if dirty > len(self.cold_free):
+            raise ModelError(ERR_NO_COLD, "cold pool exhausted")
+        out = []
+        for sid in sids:
+            out += self.evict(sid)
+        return out
+
     def resume(self, sids: Sequence[int]):
         """Batched resume, atomic as a whole.  Returns, per session, the list of
         (cold_src, hot_dst) copies in logical page order."""

@@ -52,14 +52,15 @@ hipError_t launch_partition(const int32_t* seq_lens, int batch, int num_kv_heads
                             int64_t pt_stride, int32_t* slots, hipStream_t s);
 
 struct CopyEntry {
-    int32_t src;       // source page id
+    int32_t src;       // source page id, or -1: no copy
     int32_t dst;       // destination page id
-    int32_t pt_index;  // page-table element to set to dst, or -1
-    int32_t pad;
+    int32_t pt_index;  // page-table element to write, or -1
+    int32_t pt_value;  // value written there
 };
 
-// Copies whole pages src_base[e.src] -> dst_base[e.dst] for n entries (device
-// array) and writes page_table[e.pt_index] = e.dst where pt_index >= 0.
+// For n entries (device array): copies the whole page src_base[e.src] to
+// dst_base[e.dst] where e.src >= 0, and writes page_table[e.pt_index] =
+// e.pt_value where e.pt_index >= 0.
 hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_bytes,
                             const CopyEntry* entries, int32_t n, int32_t* page_table,
                             hipStream_t s);

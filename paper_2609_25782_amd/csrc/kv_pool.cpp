@@ -601,42 +601,72 @@ int kv_fill_synthetic(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed
     return KV_OK;
 }
 
-int kv_evict_session(kv_pool* pool, int32_t sid, kv_stream_t stream) {
-    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
-    Session* s = pool->session(sid);
-    if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
-    if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sid);
-    std::vector<int32_t> dirty;
-    for (size_t i = 0; i < s->cold.size(); ++i)
-        if (s->cold[i] < 0) dirty.push_back(static_cast<int32_t>(i));
-    if (static_cast<int32_t>(dirty.size()) > pool->cold_free.free_count())
-        return fail(KV_ERR_NO_COLD_PAGES, "need %zu cold pages, %d free", dirty.size(),
+int kv_evict_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t stream) {
+    if (!pool || (n > 0 && !sids) || n < 0) return fail(KV_ERR_INVALID, "bad arguments");
+    if (n == 0) return KV_OK;
+    std::vector<int32_t> ids(sids, sids + n);
+    {
+        std::vector<int32_t> sorted = ids;
+        std::sort(sorted.begin(), sorted.end());
+        if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end())
+            return fail(KV_ERR_INVALID, "duplicate session in batch");
+    }
+    int64_t dirty = 0;
+    for (int32_t sid : ids) {
+        Session* s = pool->session(sid);
+        if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+        if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sid);
+        for (int32_t c : s->cold) dirty += c < 0;
+    }
+    if (dirty > pool->cold_free.free_count())
+        return fail(KV_ERR_NO_COLD_PAGES, "need %lld cold pages, %d free", static_cast<long long>(dirty),
                     pool->cold_free.free_count());
+    // cold pages for the dirty pages, lowest first, in argument and logical-page order
     std::vector<int32_t> dst;
-    pool->cold_free.lowest(static_cast<int32_t>(dirty.size()), dst);
+    pool->cold_free.lowest(static_cast<int32_t>(dirty), dst);
     if (!pool->meta) {
         DeviceGuard g(pool->d.device);
         hipStream_t st = pool->strm(stream);
-        std::vector<hck::CopyEntry> entries(dirty.size());
-        for (size_t j = 0; j < dirty.size(); ++j)
-            entries[j] = hck::CopyEntry{s->hot[dirty[j]], dst[j], -1, 0};
+        std::vector<hck::CopyEntry> entries;
+        size_t k = 0;
+        for (int32_t sid : ids) {
+            const Session& s = pool->sessions[sid];
+            const int32_t row = sid * pool->d.max_pages_per_session;
+            for (size_t i = 0; i < s.hot.size(); ++i) {
+                const bool copy = s.cold[i] < 0;
+                entries.push_back(hck::CopyEntry{copy ? s.hot[i] : -1, copy ? dst[k] : -1,
+                                                 row + static_cast<int32_t>(i), -1});
+                k += copy;
+            }
+        }
         int rc = pool->submit_copies(pool->hot, pool->cold, entries, st);
-        if (!rc) rc = pool->clear_row(sid, static_cast<int32_t>(s->hot.size()), st);
         if (!rc) rc = pool->note_frees(st);
         if (rc) return rc;
     }
-    for (size_t j = 0; j < dirty.size(); ++j) {
-        pool->cold_free.take(dst[j]);
-        pool->cold_ref[dst[j]] = 1;
-        s->cold[dirty[j]] = dst[j];
+    size_t k = 0;
+    for (int32_t sid : ids) {
+        Session& s = pool->sessions[sid];
+        int64_t written = 0;
+        for (size_t i = 0; i < s.cold.size(); ++i) {
+            if (s.cold[i] < 0) {
+                pool->cold_free.take(dst[k]);
+                pool->cold_ref[dst[k]] = 1;
+                s.cold[i] = dst[k++];
+                ++written;
+            }
+        }
+        for (int32_t p : s.hot) pool->hot_free.give(p);
+        s.hot.clear();
+        s.state = KV_SESSION_PAUSED;
+        pool->st.pages_to_cold += written;
+        pool->st.bytes_to_cold += written * pool->page_bytes;
+        pool->st.evicts += 1;
     }
-    for (int32_t p : s->hot) pool->hot_free.give(p);
-    s->hot.clear();
-    s->state = KV_SESSION_PAUSED;
-    pool->st.pages_to_cold += static_cast<int64_t>(dirty.size());
-    pool->st.bytes_to_cold += static_cast<int64_t>(dirty.size()) * pool->page_bytes;
-    pool->st.evicts += 1;
     return KV_OK;
+}
+
+int kv_evict_session(kv_pool* pool, int32_t sid, kv_stream_t stream) {
+    return kv_evict_sessions(pool, &sid, 1, stream);
 }
 
 int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t stream) {
@@ -671,7 +701,7 @@ int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_
             const Session& s = pool->sessions[sid];
             const int32_t row = sid * pool->d.max_pages_per_session;
             for (size_t i = 0; i < s.cold.size(); ++i, ++k)
-                entries.push_back(hck::CopyEntry{s.cold[i], dst[k], row + static_cast<int32_t>(i), 0});
+                entries.push_back(hck::CopyEntry{s.cold[i], dst[k], row + static_cast<int32_t>(i), dst[k]});
         }
         int rc = pool->order_after_frees(st);
         if (!rc) rc = pool->submit_copies(pool->cold, pool->hot, entries, st);

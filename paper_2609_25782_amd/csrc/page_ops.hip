@@ -1,9 +1,10 @@
 // Page movement and page-content kernels for gfx950.
 //
 //  - page_copy_kernel: whole-page copies between pools with an optional
-//    page-table write per page.  Resume (data path 2) gathers cold pages into
-//    free hot pages and rewrites the session's row in the same launch; eviction
-//    (data path 4) scatters the pages that have no valid cold copy.  The copy
+//    page-table write per entry.  Resume (data path 2) gathers cold pages into
+//    free hot pages and rewrites the sessions' rows in the same launch; eviction
+//    (data path 4) scatters the pages that have no valid cold copy and clears
+//    the rows, also in one launch.  The copy
 //    is byte for byte, 16-byte vector loads and stores, several loads in
 //    flight per thread before the first store.
 //  - fill kernels for page tables and for synthetic page contents.
@@ -42,6 +43,8 @@ __global__ __launch_bounds__(kBlockThreads) void page_copy_kernel(
         const int ent = static_cast<int>(flat / chunks_per_page);
         const int chunk = static_cast<int>(flat % chunks_per_page);
         const CopyEntry e = entries[ent];
+        if (chunk == 0 && threadIdx.x == 0 && e.pt_index >= 0) page_table[e.pt_index] = e.pt_value;
+        if (e.src < 0) continue;
         const int64_t base = static_cast<int64_t>(chunk) * U * kBlockThreads * 16;
         const u32x4* s =
             reinterpret_cast<const u32x4*>(src_base + e.src * page_bytes + base) + threadIdx.x;
@@ -58,7 +61,6 @@ __global__ __launch_bounds__(kBlockThreads) void page_copy_kernel(
             else
                 d[i * kBlockThreads] = buf[i];
         }
-        if (chunk == 0 && threadIdx.x == 0 && e.pt_index >= 0) page_table[e.pt_index] = e.dst;
     }
 }
 

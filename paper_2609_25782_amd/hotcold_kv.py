@@ -74,6 +74,7 @@ _SIGS = {
     "kv_write_tokens": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P]),
     "kv_fill_synthetic": (ctypes.c_int, [_P, _I32, _I32, _U64, ctypes.c_float, _P]),
     "kv_evict_session": (ctypes.c_int, [_P, _I32, _P]),
+    "kv_evict_sessions": (ctypes.c_int, [_P, _PI32, _I32, _P]),
     "kv_resume_session": (ctypes.c_int, [_P, _I32, _P]),
     "kv_resume_sessions": (ctypes.c_int, [_P, _PI32, _I32, _P]),
     "paged_decode_waves": (_I32, [_P]),
@@ -187,6 +188,11 @@ def kv_fill_synthetic(pool: int, sid: int, gen_sid: int, seed: int, value_mult: 
 
 def kv_evict_session(pool: int, sid: int, stream: int = 0) -> None:
     _check(_lib.kv_evict_session(pool, sid, stream or None), "kv_evict_session")
+
+
+def kv_evict_sessions(pool: int, sids: Sequence[int], stream: int = 0) -> None:
+    _check(_lib.kv_evict_sessions(pool, _i32_array(sids), len(sids), stream or None),
+           "kv_evict_sessions")
 
 
 def kv_resume_session(pool: int, sid: int, stream: int = 0) -> None:

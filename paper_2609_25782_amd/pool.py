@@ -89,8 +89,11 @@ class HotColdPool:
     def fill_synthetic(self, sid: int, gen_sid: int, seed: int, value_mult: float, stream=None) -> None:
         kv.kv_fill_synthetic(self.handle, sid, gen_sid, seed, float(value_mult), _stream(stream))
 
-    def evict(self, sid: int, stream=None) -> None:
-        kv.kv_evict_session(self.handle, sid, _stream(stream))
+    def evict(self, sids, stream=None) -> None:
+        if isinstance(sids, int):
+            kv.kv_evict_session(self.handle, sids, _stream(stream))
+        else:
+            kv.kv_evict_sessions(self.handle, list(sids), _stream(stream))
 
     def resume(self, sids, stream=None) -> None:
         if isinstance(sids, int):

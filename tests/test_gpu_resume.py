@@ -199,13 +199,14 @@ def test_random_sequences_match_model(dev):
                     raise e
                 assert pool.create_session(L) == model_sid
             elif op == 1:
+                sids = [int(x) for x in rng.choice(ms, size=int(rng.integers(1, 3)), replace=False)]
                 try:
-                    copies = model.evict(sid)
+                    copies = model.evict_many(sids)
                 except Exception as e:
                     with pytest.raises(kv.KVError):
-                        pool.evict(sid)
+                        pool.evict(sids)
                     raise e
-                pool.evict(sid)
+                pool.evict(sids)
                 for h, c in copies:
                     cold_img[c] = hot_img[h]
             elif op == 2:

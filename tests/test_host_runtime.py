@@ -41,7 +41,7 @@ def _same(kv, pool, model, ms):
 
 def _random_call(kv, pool, rng, nh, nc, ms, stride):
     """One random call as a (model call, library call) pair."""
-    op = int(rng.integers(0, 5))
+    op = int(rng.integers(0, 6))
     sid = int(rng.integers(-1, ms + 1))
     if op == 0:
         L = int(rng.integers(-2, 16 * stride + 20))
@@ -56,6 +56,9 @@ def _random_call(kv, pool, rng, nh, nc, ms, stride):
         return (lambda m: (m.resume(sids), None)[1]), (lambda: kv.kv_resume_sessions(pool, sids))
     if op == 3:
         return (lambda m: m.destroy(sid)), (lambda: kv.kv_session_destroy(pool, sid))
+    if op == 5:
+        sids = [int(x) for x in rng.integers(-1, ms + 1, size=int(rng.integers(1, 4)))]
+        return (lambda m: (m.evict_many(sids), None)[1]), (lambda: kv.kv_evict_sessions(pool, sids))
     n = int(rng.integers(0, stride + 1))
     cold = [int(p) for p in rng.choice(nc, size=n, replace=False)]
     L = 16 * n - (int(rng.integers(0, 16)) if n else 0)

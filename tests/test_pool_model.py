@@ -123,3 +123,13 @@ def test_random_sequences_conserve_pages():
                 assert all(c >= 0 for c in s.cold)
             if s.state == ACTIVE:
                 assert len(s.hot) == (s.seq_len + 15) // 16 == len(s.cold)
+
+
+def test_batched_evict_is_atomic():
+    m = PoolModel(num_hot=10, num_cold=5, max_sessions=4, max_pages_per_session=4)
+    a, b = m.create(48), m.create(48)      # 3 + 3 dirty pages, only 5 cold pages
+    before = copy.deepcopy(m.__dict__)
+    with pytest.raises(ModelError) as e:
+        m.evict_many([a, b])
+    assert e.value.code == ERR_NO_COLD and m.__dict__ == before
+    assert m.evict_many([b]) == [(3, 0), (4, 1), (5, 2)]
