@@ -206,6 +206,31 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
         main_s.wait_stream(side)
     torch.cuda.synchronize()
     both_ms = sum(e[2 * i].elapsed_time(e[2 * i + 1]) for i in range(steps)) / steps
+    # partial residency: sessions paused with all pages resident, a fraction of
+    # their pages evicted page by page (LRU; clean, so no cold writes), resumed
+    partial = []
+    for j, frac in enumerate((0.25, 0.5, 0.75)):
+        sids = picks[k % len(picks)]
+        k += 1
+        pool.resume(sids, stream=main_s)
+        for sid in sids:
+            pool.pause(sid)
+        n_pages = sum(synth.pages_for(pool.info(sid)[1]) for sid in sids)
+        pool.evict_pages(int(frac * n_pages), stream=main_s)
+        torch.cuda.synchronize()
+        st0 = pool.stats()
+        kv.kv_pool_set_profiling(pool.handle, True)
+        kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
+        pool.resume(sids, stream=main_s)
+        n_k, ms_k = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
+        kv.kv_pool_set_profiling(pool.handle, False)
+        st1 = pool.stats()
+        hit = (st1["resume_pages_resident"] - st0["resume_pages_resident"]) / \
+            (st1["resume_pages_total"] - st0["resume_pages_total"])
+        partial.append({"evicted_fraction": frac, "hit_rate": round(hit, 4),
+                        "ms_per_session": round(ms_k / len(sids), 4)})
+        pool.evict(sids, stream=main_s)
+    torch.cuda.synchronize()
     pool.close()
     del pool
     torch.cuda.empty_cache()
@@ -223,6 +248,7 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
         "decode48_ms_with_concurrent_resume": round(both_ms, 3),
         "tbt_impact": round(both_ms / decode_ms, 3),
         "decode48_GBps": round(48 * sum(decode_bytes(w.seq_lens, 32, 4, 128, 2)) / (decode_ms / 1e3) / 1e9, 1),
+        "partial_residency": partial,
     }
 
 
@@ -323,7 +349,7 @@ def main():
         log("sampled oracle check: session %d max abs %.3g normalised %.3g" % (b, err, norm))
 
     kv.kv_pool_set_profiling(pool.handle, True)
-    for k in range(3):
+    for k in range(4):
         kv.kv_pool_profile_read(pool.handle, k)
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()

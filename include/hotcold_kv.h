@@ -99,8 +99,9 @@ enum kv_session_state { KV_SESSION_FREE = 0, KV_SESSION_ACTIVE = 1, KV_SESSION_P
 enum kv_kernel_id {
     KV_KERNEL_DECODE_SPLIT = 0,   /* split-K paged decode attention */
     KV_KERNEL_DECODE_COMBINE = 1, /* combine of split partials */
-    KV_KERNEL_PAGE_COPY = 2,      /* resume gather / evict scatter */
-    KV_KERNEL_COUNT = 3
+    KV_KERNEL_PAGE_COPY = 2,      /* resume gather (cold -> hot) */
+    KV_KERNEL_EVICT_COPY = 3,     /* eviction scatter and row clears (hot -> cold) */
+    KV_KERNEL_COUNT = 4
 };
 
 typedef void* kv_stream_t;
@@ -132,6 +133,9 @@ typedef struct kv_pool_stats {
     int64_t bytes_to_hot;
     int64_t resumes;         /* sessions resumed */
     int64_t evicts;          /* sessions evicted */
+    int64_t resume_pages_resident; /* pages already in the hot tier when their session resumed */
+    int64_t resume_pages_total;    /* pages of resumed sessions (hit rate = resident / total) */
+    int64_t lru_evicted_pages;     /* pages of paused sessions evicted page by page (LRU) */
 } kv_pool_stats;
 
 /* ----------------------------------------------------------------------- */
@@ -169,13 +173,44 @@ int kv_pool_stats_get(const kv_pool* pool, kv_pool_stats* out);
  * Create an ACTIVE session of seq_len tokens (a stand-in for prefill, which is
  * outside this library): allocates ceil(seq_len / 16) hot pages and writes the
  * session's page-table row.  hot_pages (host array, nullable) picks the exact
- * pages, which must be free and distinct; NULL takes the lowest free ones.
- * The page contents are left as they are: fill them with kv_write_tokens or
- * kv_fill_synthetic.  The new session id (lowest free row) goes to *sid_out.
- * Errors: KV_ERR_INVALID, KV_ERR_NO_HOT_PAGES.
+ * pages, which must be free and distinct.  NULL takes the lowest free ones; if
+ * too few are free, least-recently-used pages of paused sessions are evicted
+ * first (see kv_session_pause).  The page contents are left as they are: fill
+ * them with kv_write_tokens or kv_fill_synthetic.  The new session id (lowest
+ * free row) goes to *sid_out.
+ * Errors: KV_ERR_INVALID, KV_ERR_NO_HOT_PAGES, KV_ERR_NO_COLD_PAGES (no room
+ * for the cold copies of the pages that would have to be evicted).
  */
 int kv_session_create(kv_pool* pool, int32_t seq_len, const int32_t* hot_pages,
                       kv_stream_t stream, int32_t* sid_out);
+
+/*
+ * Grow an ACTIVE session to new_seq_len tokens: decoding appends each new
+ * token's KV (Sec. II; fresh KV goes to the fast tier, data path 3).  Pages for
+ * the new tokens are allocated like kv_session_create's and appended to the
+ * row; write the tokens' K and V with kv_write_tokens.
+ * Errors: KV_ERR_INVALID (shrinking, row stride), KV_ERR_STATE, KV_ERR_NO_HOT_PAGES,
+ * KV_ERR_NO_COLD_PAGES.
+ */
+int kv_session_extend(kv_pool* pool, int32_t sid, int32_t new_seq_len, kv_stream_t stream);
+
+/*
+ * Pause an ACTIVE session (the agent waits for a tool or a user, Sec. II): no
+ * data moves.  Its pages stay in the hot tier but become evictable, least
+ * recently used first: the paper evicts LRU blocks, and since active blocks are
+ * read every step, the oldest paused sessions' blocks go first (Sec. III,
+ * "Eviction, resume and decode").  Pages of one session go in logical order.
+ * Errors: KV_ERR_STATE (not ACTIVE).
+ */
+int kv_session_pause(kv_pool* pool, int32_t sid);
+
+/*
+ * Evict up to n least-recently-used resident pages of paused sessions to the
+ * cold tier (write-on-evict: pages with a valid cold copy cost no write) and
+ * free them; *evicted (nullable) gets the number evicted.
+ * Errors: KV_ERR_NO_COLD_PAGES (nothing changes).
+ */
+int kv_evict_pages(kv_pool* pool, int32_t n, kv_stream_t stream, int32_t* evicted);
 
 /*
  * Register a PAUSED session of seq_len tokens whose KV already sits in the given
@@ -193,8 +228,8 @@ int kv_session_destroy(kv_pool* pool, int32_t sid, kv_stream_t stream);
 
 /*
  * Describe a session.  Host outputs (any may be NULL): state, seq_len, and up to
- * `cap` entries each of its hot page ids (logical page order; empty unless
- * ACTIVE) and cold page ids (-1 where the page has no valid cold copy).
+ * `cap` entries each of its hot page ids (logical page order, -1 where the page
+ * is not resident) and cold page ids (-1 where the page has no valid cold copy).
  */
 int kv_session_info(const kv_pool* pool, int32_t sid, int32_t* state, int32_t* seq_len,
                     int32_t* hot_pages, int32_t* cold_pages, int32_t cap);
@@ -240,10 +275,13 @@ int kv_evict_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t
 /*
  * Resume a PAUSED session (data path 2; Sec. III, "Eviction, resume and
  * decode": the KV is brought back into the fast tier before the session runs).
- * Takes ceil(seq_len / 16) free hot pages, lowest ids first in logical page
- * order, copies every page cold -> hot (whole pages, byte for byte) and writes
- * the page-table row.  The cold copies stay valid.  One kernel launch.
- * Errors: KV_ERR_STATE (not PAUSED), KV_ERR_NO_HOT_PAGES (nothing changes).
+ * Only pages that are not resident are fetched: they get free hot pages (lowest
+ * ids first, in logical page order; least-recently-used pages of other paused
+ * sessions are evicted first if too few are free) and are copied cold -> hot
+ * byte for byte.  The whole page-table row is written.  The cold copies stay
+ * valid.  The statistics count resident and total pages (the resume hit rate).
+ * Errors: KV_ERR_STATE (not PAUSED), KV_ERR_NO_HOT_PAGES, KV_ERR_NO_COLD_PAGES
+ * (nothing changes).
  */
 int kv_resume_session(kv_pool* pool, int32_t sid, kv_stream_t stream);
 

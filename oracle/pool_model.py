@@ -2,26 +2,32 @@
 
 It replays the documented policy on plain Python sets and lists and predicts,
 for every call, the resulting page-table rows, the pages copied in each
-direction and the number of cold-tier writes.  Nothing here touches a GPU or
-the library.
+direction and the counters.  Nothing here touches a GPU or the library.
 
 Policy being modelled (paper Sec. III):
 
-* Active sessions keep their KV in the hot tier; paused sessions keep it in the
-  cold tier (Sec. III, first paragraph; data paths 2 and 4).
+* Active sessions keep their KV in the hot tier; paused sessions' KV drains to
+  the cold tier (Sec. III, first paragraph; data paths 2 and 4).
 * Write-on-evict: a page is written to the cold tier only when it is evicted,
   and a cold copy stays valid after the session is resumed, because written KV
   never changes; an unmodified page is therefore written to the cold tier at
   most once (Sec. III, "Memory hierarchy and write policy").
-* A resumed session's KV is brought back into the hot tier before it runs
-  (Sec. III, "Eviction, resume and decode").
+* Eviction is least-recently-used at page granularity; active pages are read
+  every step, so the pages of the longest-paused sessions go first (Sec. III,
+  "Eviction, resume and decode").
+* A resumed session's missing KV is brought back before it runs; pages still
+  resident are not fetched, and the share found resident is the resume hit
+  rate (Sec. III, "Eviction, resume and decode"; Sec. IV, Methodology).
 
 Readings where the paper is silent (each is stated in the design notes):
 
-* Hot and cold pages are handed out lowest id first; a session's logical pages
-  0..n-1 get the n lowest free ids in ascending order; batched calls process
-  sessions in argument order; session ids are also handed out lowest first.
-* Resume restores every page of the session (no partial residency).
+* Hot and cold pages are handed out lowest id first; pages needed by one call
+  go to its sessions in argument order and logical page order; session ids are
+  handed out lowest first.
+* LRU order: paused sessions by pause time, oldest first; within a session,
+  logical page order.  Only paused sessions' pages are evicted page by page
+  (no spilling of active pages); a call that would have to evict pages of the
+  sessions it resumes fails instead.
 * Writing tokens into a page that has a cold copy invalidates that copy, so the
   next eviction writes the page again.
 * Cold pages may be shared by several paused sessions (a virtualised cold
@@ -32,7 +38,7 @@ Readings where the paper is silent (each is stated in the design notes):
 from __future__ import annotations
 
 from dataclasses import dataclass, field
-from typing import Dict, List, Optional, Sequence
+from typing import List, Optional, Sequence, Tuple
 
 PAGE_TOKENS = 16
 
@@ -51,7 +57,8 @@ class ModelError(Exception):
 class _Session:
     state: int = FREE
     seq_len: int = 0
-    hot: List[int] = field(default_factory=list)
+    stamp: int = 0
+    hot: List[int] = field(default_factory=list)   # -1 = not resident
     cold: List[int] = field(default_factory=list)  # -1 = no valid cold copy
 
 
@@ -67,17 +74,19 @@ class PoolModel:
         self.cold_free = set(range(num_cold))
         self.cold_ref = [0] * num_cold
         self.sessions = [_Session() for _ in range(max_sessions)]
+        self.clock = 0
         self.cold_writes = 0          # pages written to the cold tier
         self.pages_to_hot = 0         # pages copied cold -> hot
         self.resumes = 0
         self.evicts = 0
+        self.resume_resident = 0      # pages found resident by resumes
+        self.resume_total = 0         # pages of resumed sessions
+        self.lru_evicted = 0          # pages evicted page by page
 
     # -- helpers -----------------------------------------------------------
-    def _take(self, free: set, n: int) -> List[int]:
-        got = sorted(free)[:n]
-        for p in got:
-            free.remove(p)
-        return got
+    @staticmethod
+    def _lowest(free: set, n: int) -> List[int]:
+        return sorted(free)[:n]
 
     def _new_sid(self) -> int:
         for sid, s in enumerate(self.sessions):
@@ -96,25 +105,108 @@ class PoolModel:
         if self.cold_ref[page] == 0:
             self.cold_free.add(page)
 
+    def _tick(self) -> int:
+        self.clock += 1
+        return self.clock
+
+    def _lru(self, need: int, exclude=()) -> List[Tuple[int, int]]:
+        """Up to `need` (sid, page) resident pages of paused sessions, LRU first."""
+        order = sorted((s.stamp, sid) for sid, s in enumerate(self.sessions)
+                       if s.state == PAUSED and sid not in exclude and any(p >= 0 for p in s.hot))
+        out = []
+        for _stamp, sid in order:
+            for i, p in enumerate(self.sessions[sid].hot):
+                if len(out) == need:
+                    return out
+                if p >= 0:
+                    out.append((sid, i))
+        return out
+
+    def _plan(self, k: int, exclude=()):
+        """k hot pages, with the LRU victims to evict first.  Changes nothing.
+        Returns (victims, cold pages for the dirty victims, the k hot pages)."""
+        victims = []
+        if k > len(self.hot_free):
+            victims = self._lru(k - len(self.hot_free), exclude)
+            if len(victims) < k - len(self.hot_free):
+                raise ModelError(ERR_NO_HOT, "hot pool exhausted")
+        dirty = sum(1 for sid, i in victims if self.sessions[sid].cold[i] < 0)
+        if dirty > len(self.cold_free):
+            raise ModelError(ERR_NO_COLD, "cold pool exhausted")
+        cold = self._lowest(self.cold_free, dirty)
+        after = set(self.hot_free) | {self.sessions[sid].hot[i] for sid, i in victims}
+        return victims, cold, self._lowest(after, k)
+
+    def _evict_victims(self, victims, cold):
+        """Apply the victims; returns their (hot_src, cold_dst) copies."""
+        copies, it = [], iter(cold)
+        for sid, i in victims:
+            s = self.sessions[sid]
+            if s.cold[i] < 0:
+                c = next(it)
+                self.cold_free.remove(c)
+                self.cold_ref[c] = 1
+                s.cold[i] = c
+                copies.append((s.hot[i], c))
+                self.cold_writes += 1
+            self.hot_free.add(s.hot[i])
+            s.hot[i] = -1
+            self.lru_evicted += 1
+        return copies
+
+    def _take_hot(self, pages):
+        for p in pages:
+            self.hot_free.remove(p)
+
     # -- calls ---------------------------------------------------------------
     def create(self, seq_len: int, pages: Optional[Sequence[int]] = None) -> int:
         if seq_len < 0 or _pages(seq_len) > self.stride:
             raise ModelError(ERR_INVALID, "bad length")
         n = _pages(seq_len)
+        sid = self._new_sid()
+        victims, cold = [], []
         if pages is not None:
             pages = [int(p) for p in pages]
             if len(pages) != n or len(set(pages)) != n or any(p not in self.hot_free for p in pages):
                 raise ModelError(ERR_INVALID, "pages not free/distinct")
-        elif n > len(self.hot_free):
-            raise ModelError(ERR_NO_HOT, "hot pool exhausted")
-        sid = self._new_sid()
-        if pages is None:
-            pages = self._take(self.hot_free, n)
         else:
-            for p in pages:
-                self.hot_free.remove(p)
-        self.sessions[sid] = _Session(ACTIVE, seq_len, list(pages), [-1] * n)
+            victims, cold, pages = self._plan(n)
+        self.last_victim_copies = self._evict_victims(victims, cold)
+        self._take_hot(pages)
+        self.sessions[sid] = _Session(ACTIVE, seq_len, 0, list(pages), [-1] * n)
         return sid
+
+    def extend(self, sid: int, new_len: int) -> None:
+        s = self._session(sid)
+        if s.state != ACTIVE:
+            raise ModelError(ERR_STATE, "not active")
+        if new_len < s.seq_len or _pages(new_len) > self.stride:
+            raise ModelError(ERR_INVALID, "bad length")
+        add = _pages(new_len) - len(s.hot)
+        victims, cold, pages = self._plan(add)
+        self.last_victim_copies = self._evict_victims(victims, cold)
+        self._take_hot(pages)
+        s.hot += pages
+        s.cold += [-1] * add
+        s.seq_len = new_len
+
+    def pause(self, sid: int) -> None:
+        s = self._session(sid)
+        if s.state != ACTIVE:
+            raise ModelError(ERR_STATE, "not active")
+        s.state = PAUSED
+        s.stamp = self._tick()
+
+    def evict_pages(self, n: int):
+        """Returns (number evicted, their copies)."""
+        if n < 0:
+            raise ModelError(ERR_INVALID, "negative count")
+        victims = self._lru(n)
+        dirty = sum(1 for sid, i in victims if self.sessions[sid].cold[i] < 0)
+        if dirty > len(self.cold_free):
+            raise ModelError(ERR_NO_COLD, "cold pool exhausted")
+        copies = self._evict_victims(victims, self._lowest(self.cold_free, dirty))
+        return len(victims), copies
 
     def import_cold(self, seq_len: int, cold_pages: Sequence[int]) -> int:
         n = _pages(seq_len)
@@ -126,32 +218,14 @@ class PoolModel:
         for p in cold_pages:
             self.cold_free.discard(p)
             self.cold_ref[p] += 1
-        self.sessions[sid] = _Session(PAUSED, seq_len, [], list(cold_pages))
+        self.sessions[sid] = _Session(PAUSED, seq_len, self._tick(), [-1] * n, list(cold_pages))
         return sid
 
     def evict(self, sid: int):
-        """Returns the list of (hot_src, cold_dst) copies the eviction performs."""
-        s = self._session(sid)
-        if s.state != ACTIVE:
-            raise ModelError(ERR_STATE, "not active")
-        dirty = [i for i, c in enumerate(s.cold) if c < 0]
-        if len(dirty) > len(self.cold_free):
-            raise ModelError(ERR_NO_COLD, "cold pool exhausted")
-        dst = self._take(self.cold_free, len(dirty))
-        copies = []
-        for i, c in zip(dirty, dst):
-            s.cold[i] = c
-            self.cold_ref[c] += 1
-            copies.append((s.hot[i], c))
-        self.cold_writes += len(dirty)
-        self.hot_free.update(s.hot)
-        s.hot = []
-        s.state = PAUSED
-        self.evicts += 1
-        return copies
+        return self.evict_many([sid])
 
     def evict_many(self, sids: Sequence[int]):
-        """Batched eviction, atomic as a whole: sessions in argument order.
+        """Whole-session eviction, atomic as a whole, sessions in argument order.
         Returns the (hot_src, cold_dst) copies of all of them."""
         sids = [int(x) for x in sids]
         if len(set(sids)) != len(sids):
@@ -164,14 +238,28 @@ class PoolModel:
             dirty += sum(1 for c in s.cold if c < 0)
         if dirty > len(self.cold_free):
             raise ModelError(ERR_NO_COLD, "cold pool exhausted")
-        out = []
+        copies = []
         for sid in sids:
-            out += self.evict(sid)
-        return out
+            s = self.sessions[sid]
+            for i in range(len(s.hot)):
+                if s.cold[i] < 0:
+                    c = self._lowest(self.cold_free, 1)[0]
+                    self.cold_free.remove(c)
+                    self.cold_ref[c] = 1
+                    s.cold[i] = c
+                    copies.append((s.hot[i], c))
+                    self.cold_writes += 1
+                self.hot_free.add(s.hot[i])
+                s.hot[i] = -1
+            s.state = PAUSED
+            s.stamp = self._tick()
+            self.evicts += 1
+        return copies
 
     def resume(self, sids: Sequence[int]):
-        """Batched resume, atomic as a whole.  Returns, per session, the list of
-        (cold_src, hot_dst) copies in logical page order."""
+        """Batched resume, atomic as a whole.  Fetches only non-resident pages.
+        Returns, per session, the (cold_src, hot_dst) copies in logical page order;
+        the LRU victims' copies of the call are in `last_victim_copies`."""
         sids = [int(x) for x in sids]
         if len(set(sids)) != len(sids):
             raise ModelError(ERR_INVALID, "duplicate session")
@@ -180,18 +268,24 @@ class PoolModel:
             s = self._session(sid)
             if s.state != PAUSED:
                 raise ModelError(ERR_STATE, "not paused")
-            need += len(s.cold)
-        if need > len(self.hot_free):
-            raise ModelError(ERR_NO_HOT, "hot pool exhausted")
-        out = []
+            need += sum(1 for p in s.hot if p < 0)
+        victims, cold, pages = self._plan(need, exclude=set(sids))
+        self.last_victim_copies = self._evict_victims(victims, cold)
+        self._take_hot(pages)
+        out, it = [], iter(pages)
         for sid in sids:
             s = self.sessions[sid]
-            dst = self._take(self.hot_free, len(s.cold))
-            s.hot = dst
+            per = []
+            for i, p in enumerate(s.hot):
+                if p < 0:
+                    s.hot[i] = next(it)
+                    per.append((s.cold[i], s.hot[i]))
+            self.pages_to_hot += len(per)
+            self.resume_resident += len(s.hot) - len(per)
+            self.resume_total += len(s.hot)
             s.state = ACTIVE
-            out.append(list(zip(s.cold, dst)))
-            self.pages_to_hot += len(dst)
             self.resumes += 1
+            out.append(per)
         return out
 
     def write_tokens(self, sid: int, tok_begin: int, n_tok: int) -> None:
@@ -209,7 +303,7 @@ class PoolModel:
         s = self._session(sid)
         if s.state == FREE:
             raise ModelError(ERR_STATE, "not in use")
-        self.hot_free.update(s.hot)
+        self.hot_free.update(p for p in s.hot if p >= 0)
         for c in s.cold:
             if c >= 0:
                 self._release_cold(c)
@@ -219,7 +313,7 @@ class PoolModel:
     def row(self, sid: int) -> List[int]:
         """Expected page-table row (length = row stride)."""
         s = self.sessions[sid]
-        r = list(s.hot) if s.state == ACTIVE else []
+        r = list(s.hot) if s.state != FREE else []
         return r + [-1] * (self.stride - len(r))
 
     def table(self) -> List[List[int]]:

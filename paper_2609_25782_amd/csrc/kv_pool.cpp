@@ -15,6 +15,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <new>
 #include <string>
 #include <vector>
@@ -83,8 +84,21 @@ class PageSet {
 struct Session {
     int32_t state = KV_SESSION_FREE;
     int32_t seq_len = 0;
-    std::vector<int32_t> hot;   // hot page per logical page (ACTIVE only)
+    int64_t stamp = 0;          // pause time (LRU order) while PAUSED
+    std::vector<int32_t> hot;   // hot page per logical page, -1 = not resident
     std::vector<int32_t> cold;  // cold page per logical page, -1 = no valid copy
+};
+
+// One resident page of a paused session chosen for eviction.
+struct Victim {
+    int32_t sid, page;
+};
+
+// Hot pages for one call, and what must be evicted to free them.
+struct Alloc {
+    std::vector<Victim> victims;       // LRU pages evicted first
+    std::vector<int32_t> victim_cold;  // cold page for each victim without a valid copy
+    std::vector<int32_t> pages;        // hot pages handed out, ascending
 };
 
 constexpr int kStagingSlots = 4;
@@ -158,6 +172,8 @@ struct kv_pool {
     PageSet hot_free, cold_free;
     std::vector<int32_t> cold_ref;
     std::vector<Session> sessions;
+    int64_t clock = 0;                // pause stamps
+    std::map<int64_t, int32_t> lru;  // stamp -> sid of paused sessions with resident pages
     kv_pool_stats st{};
     int cus = 0;
     int32_t waves_override = 0;
@@ -253,7 +269,7 @@ struct kv_pool {
 
     // Enqueue page copies (in chunks that fit a staging slot).
     int submit_copies(const char* src, char* dst, const std::vector<hck::CopyEntry>& entries,
-                      hipStream_t s) {
+                      hipStream_t s, int kernel_id) {
         for (size_t off = 0; off < entries.size(); off += kStagingEntries) {
             const int32_t n = static_cast<int32_t>(
                 std::min<size_t>(kStagingEntries, entries.size() - off));
@@ -267,7 +283,7 @@ struct kv_pool {
             hipEvent_t p = prof_begin(s);
             e = hck::launch_page_copy(src, dst, page_bytes,
                                       static_cast<const hck::CopyEntry*>(slot->dev), n, pt, s);
-            prof_end(KV_KERNEL_PAGE_COPY, p, s);
+            prof_end(kernel_id, p, s);
             if (e != hipSuccess) return hip_fail(e, "page copy launch");
             e = hipEventRecord(slot->done, s);
             if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
@@ -298,6 +314,115 @@ struct kv_pool {
             hck::launch_fill_i32(pt + static_cast<int64_t>(sid) * d.max_pages_per_session, n, -1, s);
         if (e != hipSuccess) return hip_fail(e, "page-table clear");
         return KV_OK;
+    }
+
+    // Write `n` page ids into page-table row `sid` starting at entry `first`.
+    int submit_row_at(int32_t sid, int32_t first, const int32_t* vals, int32_t n, hipStream_t s) {
+        if (n <= 0) return KV_OK;
+        StagingSlot* slot;
+        int rc = acquire_slot(&slot);
+        if (rc) return rc;
+        std::memcpy(slot->host, vals, n * sizeof(int32_t));
+        hipError_t e = hipMemcpyAsync(
+            pt + static_cast<int64_t>(sid) * d.max_pages_per_session + first, slot->host,
+            n * sizeof(int32_t), hipMemcpyHostToDevice, s);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(page-table row)");
+        e = hipEventRecord(slot->done, s);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
+        slot->pending = true;
+        return KV_OK;
+    }
+
+    static bool has_resident(const Session& s) {
+        for (int32_t p : s.hot)
+            if (p >= 0) return true;
+        return false;
+    }
+
+    // Least-recently-used resident pages of paused sessions: oldest pause first,
+    // lowest logical page first, skipping `exclude`; at most `need` of them.
+    void plan_lru(int64_t need, const std::vector<int32_t>& exclude, std::vector<Victim>& out) const {
+        out.clear();
+        for (auto it = lru.begin(); it != lru.end() && static_cast<int64_t>(out.size()) < need; ++it) {
+            const int32_t sid = it->second;
+            if (std::find(exclude.begin(), exclude.end(), sid) != exclude.end()) continue;
+            const Session& s = sessions[sid];
+            for (size_t i = 0; i < s.hot.size() && static_cast<int64_t>(out.size()) < need; ++i)
+                if (s.hot[i] >= 0) out.push_back(Victim{sid, static_cast<int32_t>(i)});
+        }
+    }
+
+    // Cold pages for the victims that have no valid cold copy (write-on-evict).
+    int plan_victim_cold(Alloc& a) {
+        int64_t dirty = 0;
+        for (const Victim& v : a.victims) dirty += sessions[v.sid].cold[v.page] < 0;
+        if (dirty > cold_free.free_count())
+            return fail(KV_ERR_NO_COLD_PAGES, "evicting %zu pages needs %lld cold pages, %d free",
+                        a.victims.size(), static_cast<long long>(dirty), cold_free.free_count());
+        cold_free.lowest(static_cast<int32_t>(dirty), a.victim_cold);
+        return KV_OK;
+    }
+
+    // Plan k hot pages, evicting LRU pages of paused sessions (never those of
+    // `exclude`) when too few are free.  Changes nothing.
+    int plan_alloc(int64_t k, const std::vector<int32_t>& exclude, Alloc& a) {
+        a = Alloc();
+        const int64_t have = hot_free.free_count();
+        if (k > have) {
+            plan_lru(k - have, exclude, a.victims);
+            if (static_cast<int64_t>(a.victims.size()) < k - have)
+                return fail(KV_ERR_NO_HOT_PAGES, "need %lld hot pages: %lld free, %zu evictable",
+                            static_cast<long long>(k), static_cast<long long>(have), a.victims.size());
+            int rc = plan_victim_cold(a);
+            if (rc) return rc;
+            PageSet after = hot_free;
+            for (const Victim& v : a.victims) after.give(sessions[v.sid].hot[v.page]);
+            after.lowest(static_cast<int32_t>(k), a.pages);
+        } else {
+            hot_free.lowest(static_cast<int32_t>(k), a.pages);
+        }
+        return KV_OK;
+    }
+
+    // Enqueue the victims' cold writes and row clears (one launch), before any
+    // launch that reuses their hot pages on the same stream.
+    int submit_victims(const Alloc& a, hipStream_t s) {
+        if (a.victims.empty()) return KV_OK;
+        std::vector<hck::CopyEntry> entries;
+        entries.reserve(a.victims.size());
+        size_t k = 0;
+        for (const Victim& v : a.victims) {
+            const Session& ss = sessions[v.sid];
+            const bool copy = ss.cold[v.page] < 0;
+            entries.push_back(hck::CopyEntry{copy ? ss.hot[v.page] : -1, copy ? a.victim_cold[k] : -1,
+                                             v.sid * d.max_pages_per_session + v.page, -1});
+            k += copy;
+        }
+        int rc = submit_copies(hot, cold, entries, s, KV_KERNEL_EVICT_COPY);
+        if (!rc) rc = note_frees(s);
+        return rc;
+    }
+
+    void commit_victims(const Alloc& a) {
+        size_t k = 0;
+        for (const Victim& v : a.victims) {
+            Session& ss = sessions[v.sid];
+            if (ss.cold[v.page] < 0) {
+                const int32_t c = a.victim_cold[k++];
+                cold_free.take(c);
+                cold_ref[c] = 1;
+                ss.cold[v.page] = c;
+                st.pages_to_cold += 1;
+                st.bytes_to_cold += page_bytes;
+            }
+            hot_free.give(ss.hot[v.page]);
+            ss.hot[v.page] = -1;
+            st.lru_evicted_pages += 1;
+        }
+        for (const Victim& v : a.victims) {
+            Session& ss = sessions[v.sid];
+            if (!has_resident(ss)) lru.erase(ss.stamp);
+        }
     }
 
     int32_t new_sid() const {
@@ -438,38 +563,96 @@ int kv_session_create(kv_pool* pool, int32_t seq_len, const int32_t* hot_pages, 
     if (n > pool->d.max_pages_per_session)
         return fail(KV_ERR_INVALID, "%d pages exceed the row stride %d", n,
                     pool->d.max_pages_per_session);
-    std::vector<int32_t> pages;
+    const int32_t sid = pool->new_sid();
+    if (sid < 0) return fail(KV_ERR_INVALID, "no free session slot");
+    Alloc a;
     if (hot_pages) {
-        pages.assign(hot_pages, hot_pages + n);
-        std::vector<int32_t> sorted = pages;
+        a.pages.assign(hot_pages, hot_pages + n);
+        std::vector<int32_t> sorted = a.pages;
         std::sort(sorted.begin(), sorted.end());
         if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end())
             return fail(KV_ERR_INVALID, "duplicate hot page");
-        for (int32_t p : pages)
+        for (int32_t p : a.pages)
             if (p < 0 || p >= pool->d.num_hot_pages || !pool->hot_free.is_free(p))
                 return fail(KV_ERR_INVALID, "hot page %d is not free", p);
     } else {
-        if (n > pool->hot_free.free_count())
-            return fail(KV_ERR_NO_HOT_PAGES, "need %d hot pages, %d free", n,
-                        pool->hot_free.free_count());
-        pool->hot_free.lowest(n, pages);
+        int rc = pool->plan_alloc(n, {}, a);
+        if (rc) return rc;
     }
-    const int32_t sid = pool->new_sid();
-    if (sid < 0) return fail(KV_ERR_INVALID, "no free session slot");
     if (!pool->meta && n > 0) {
         DeviceGuard g(pool->d.device);
         hipStream_t s = pool->strm(stream);
         int rc = pool->order_after_frees(s);
-        if (!rc) rc = pool->submit_row(sid, pages.data(), n, s);
+        if (!rc) rc = pool->submit_victims(a, s);
+        if (!rc) rc = pool->submit_row_at(sid, 0, a.pages.data(), n, s);
         if (rc) return rc;
     }
-    for (int32_t p : pages) pool->hot_free.take(p);
+    pool->commit_victims(a);
+    for (int32_t p : a.pages) pool->hot_free.take(p);
     Session& ss = pool->sessions[sid];
+    ss = Session();
     ss.state = KV_SESSION_ACTIVE;
     ss.seq_len = seq_len;
-    ss.hot = pages;
+    ss.hot = a.pages;
     ss.cold.assign(n, -1);
     *sid_out = sid;
+    return KV_OK;
+}
+
+int kv_session_extend(kv_pool* pool, int32_t sid, int32_t new_seq_len, kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    Session* s = pool->session(sid);
+    if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+    if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sid);
+    if (new_seq_len < s->seq_len) return fail(KV_ERR_INVALID, "a session only grows");
+    const int32_t n_old = static_cast<int32_t>(s->hot.size());
+    const int32_t n_new = pages_of(new_seq_len);
+    if (n_new > pool->d.max_pages_per_session)
+        return fail(KV_ERR_INVALID, "%d pages exceed the row stride %d", n_new,
+                    pool->d.max_pages_per_session);
+    Alloc a;
+    int rc = pool->plan_alloc(n_new - n_old, {}, a);
+    if (rc) return rc;
+    if (!pool->meta && n_new > n_old) {
+        DeviceGuard g(pool->d.device);
+        hipStream_t st = pool->strm(stream);
+        rc = pool->order_after_frees(st);
+        if (!rc) rc = pool->submit_victims(a, st);
+        if (!rc) rc = pool->submit_row_at(sid, n_old, a.pages.data(), n_new - n_old, st);
+        if (rc) return rc;
+    }
+    pool->commit_victims(a);
+    for (int32_t p : a.pages) pool->hot_free.take(p);
+    s->hot.insert(s->hot.end(), a.pages.begin(), a.pages.end());
+    s->cold.resize(n_new, -1);
+    s->seq_len = new_seq_len;
+    return KV_OK;
+}
+
+int kv_session_pause(kv_pool* pool, int32_t sid) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    Session* s = pool->session(sid);
+    if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+    if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sid);
+    s->state = KV_SESSION_PAUSED;
+    s->stamp = ++pool->clock;
+    if (kv_pool::has_resident(*s)) pool->lru[s->stamp] = sid;
+    return KV_OK;
+}
+
+int kv_evict_pages(kv_pool* pool, int32_t n, kv_stream_t stream, int32_t* evicted) {
+    if (!pool || n < 0) return fail(KV_ERR_INVALID, "bad arguments");
+    Alloc a;
+    pool->plan_lru(n, {}, a.victims);
+    int rc = pool->plan_victim_cold(a);
+    if (rc) return rc;
+    if (!pool->meta && !a.victims.empty()) {
+        DeviceGuard g(pool->d.device);
+        rc = pool->submit_victims(a, pool->strm(stream));
+        if (rc) return rc;
+    }
+    pool->commit_victims(a);
+    if (evicted) *evicted = static_cast<int32_t>(a.victims.size());
     return KV_OK;
 }
 
@@ -492,9 +675,11 @@ int kv_session_import_cold(kv_pool* pool, int32_t seq_len, const int32_t* cold_p
         if (pool->cold_ref[p]++ == 0) pool->cold_free.take(p);
     }
     Session& ss = pool->sessions[sid];
+    ss = Session();
     ss.state = KV_SESSION_PAUSED;
     ss.seq_len = seq_len;
-    ss.hot.clear();
+    ss.stamp = ++pool->clock;
+    ss.hot.assign(n, -1);
     ss.cold = pages;
     *sid_out = sid;
     return KV_OK;
@@ -505,16 +690,19 @@ int kv_session_destroy(kv_pool* pool, int32_t sid, kv_stream_t stream) {
     Session* s = pool->session(sid);
     if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
     if (s->state == KV_SESSION_FREE) return fail(KV_ERR_STATE, "session %d is not in use", sid);
-    if (!pool->meta && s->state == KV_SESSION_ACTIVE && !s->hot.empty()) {
+    const bool resident = kv_pool::has_resident(*s);
+    if (!pool->meta && resident) {
         DeviceGuard g(pool->d.device);
         hipStream_t st = pool->strm(stream);
         int rc = pool->clear_row(sid, static_cast<int32_t>(s->hot.size()), st);
         if (!rc) rc = pool->note_frees(st);
         if (rc) return rc;
     }
-    for (int32_t p : s->hot) pool->hot_free.give(p);
+    for (int32_t p : s->hot)
+        if (p >= 0) pool->hot_free.give(p);
     for (int32_t c : s->cold)
         if (c >= 0) pool->release_cold(c);
+    if (s->state == KV_SESSION_PAUSED) pool->lru.erase(s->stamp);
     *s = Session();
     return KV_OK;
 }
@@ -639,7 +827,7 @@ int kv_evict_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t
                 k += copy;
             }
         }
-        int rc = pool->submit_copies(pool->hot, pool->cold, entries, st);
+        int rc = pool->submit_copies(pool->hot, pool->cold, entries, st, KV_KERNEL_EVICT_COPY);
         if (!rc) rc = pool->note_frees(st);
         if (rc) return rc;
     }
@@ -654,10 +842,11 @@ int kv_evict_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t
                 s.cold[i] = dst[k++];
                 ++written;
             }
+            pool->hot_free.give(s.hot[i]);
+            s.hot[i] = -1;
         }
-        for (int32_t p : s.hot) pool->hot_free.give(p);
-        s.hot.clear();
         s.state = KV_SESSION_PAUSED;
+        s.stamp = ++pool->clock;
         pool->st.pages_to_cold += written;
         pool->st.bytes_to_cold += written * pool->page_bytes;
         pool->st.evicts += 1;
@@ -684,38 +873,53 @@ int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_
         Session* s = pool->session(sid);
         if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
         if (s->state != KV_SESSION_PAUSED) return fail(KV_ERR_STATE, "session %d is not paused", sid);
-        need += static_cast<int64_t>(s->cold.size());
+        for (int32_t p : s->hot) need += p < 0;
     }
-    if (need > pool->hot_free.free_count())
-        return fail(KV_ERR_NO_HOT_PAGES, "need %lld hot pages, %d free", static_cast<long long>(need),
-                    pool->hot_free.free_count());
-    std::vector<int32_t> dst;
-    pool->hot_free.lowest(static_cast<int32_t>(need), dst);
+    // the sessions being resumed keep their resident pages: never evict those
+    Alloc a;
+    int rc = pool->plan_alloc(need, ids, a);
+    if (rc) return rc;
     if (!pool->meta) {
         DeviceGuard g(pool->d.device);
         hipStream_t st = pool->strm(stream);
         std::vector<hck::CopyEntry> entries;
-        entries.reserve(need);
         size_t k = 0;
         for (int32_t sid : ids) {
             const Session& s = pool->sessions[sid];
             const int32_t row = sid * pool->d.max_pages_per_session;
-            for (size_t i = 0; i < s.cold.size(); ++i, ++k)
-                entries.push_back(hck::CopyEntry{s.cold[i], dst[k], row + static_cast<int32_t>(i), dst[k]});
+            for (size_t i = 0; i < s.hot.size(); ++i) {
+                if (s.hot[i] < 0) {
+                    entries.push_back(hck::CopyEntry{s.cold[i], a.pages[k], row + static_cast<int32_t>(i),
+                                                     a.pages[k]});
+                    ++k;
+                } else {
+                    entries.push_back(hck::CopyEntry{-1, -1, row + static_cast<int32_t>(i), s.hot[i]});
+                }
+            }
         }
-        int rc = pool->order_after_frees(st);
-        if (!rc) rc = pool->submit_copies(pool->cold, pool->hot, entries, st);
+        rc = pool->order_after_frees(st);
+        if (!rc) rc = pool->submit_victims(a, st);
+        if (!rc) rc = pool->submit_copies(pool->cold, pool->hot, entries, st, KV_KERNEL_PAGE_COPY);
         if (rc) return rc;
     }
+    pool->commit_victims(a);
     size_t k = 0;
     for (int32_t sid : ids) {
         Session& s = pool->sessions[sid];
-        s.hot.assign(dst.begin() + k, dst.begin() + k + s.cold.size());
-        for (int32_t p : s.hot) pool->hot_free.take(p);
-        k += s.cold.size();
+        int64_t fetched = 0;
+        for (size_t i = 0; i < s.hot.size(); ++i) {
+            if (s.hot[i] < 0) {
+                s.hot[i] = a.pages[k++];
+                pool->hot_free.take(s.hot[i]);
+                ++fetched;
+            }
+        }
+        pool->lru.erase(s.stamp);
         s.state = KV_SESSION_ACTIVE;
-        pool->st.pages_to_hot += static_cast<int64_t>(s.hot.size());
-        pool->st.bytes_to_hot += static_cast<int64_t>(s.hot.size()) * pool->page_bytes;
+        pool->st.pages_to_hot += fetched;
+        pool->st.bytes_to_hot += fetched * pool->page_bytes;
+        pool->st.resume_pages_resident += static_cast<int64_t>(s.hot.size()) - fetched;
+        pool->st.resume_pages_total += static_cast<int64_t>(s.hot.size());
         pool->st.resumes += 1;
     }
     return KV_OK;

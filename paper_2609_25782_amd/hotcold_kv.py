@@ -24,7 +24,7 @@ KV_DTYPE_BF16, KV_DTYPE_F32 = 0, 1
 KV_COLD_DEVICE, KV_COLD_PINNED_HOST = 0, 1
 KV_SESSION_FREE, KV_SESSION_ACTIVE, KV_SESSION_PAUSED = 0, 1, 2
 KV_POOL_METADATA_ONLY = 1
-KV_KERNEL_DECODE_SPLIT, KV_KERNEL_DECODE_COMBINE, KV_KERNEL_PAGE_COPY = 0, 1, 2
+KV_KERNEL_DECODE_SPLIT, KV_KERNEL_DECODE_COMBINE, KV_KERNEL_PAGE_COPY, KV_KERNEL_EVICT_COPY = 0, 1, 2, 3
 KV_COMBINE_SEPARATE, KV_COMBINE_FUSED = 0, 1
 
 
@@ -46,7 +46,9 @@ class kv_pool_stats(ctypes.Structure):
                 ("active_sessions", ctypes.c_int32), ("paused_sessions", ctypes.c_int32),
                 ("pages_to_cold", ctypes.c_int64), ("pages_to_hot", ctypes.c_int64),
                 ("bytes_to_cold", ctypes.c_int64), ("bytes_to_hot", ctypes.c_int64),
-                ("resumes", ctypes.c_int64), ("evicts", ctypes.c_int64)]
+                ("resumes", ctypes.c_int64), ("evicts", ctypes.c_int64),
+                ("resume_pages_resident", ctypes.c_int64), ("resume_pages_total", ctypes.c_int64),
+                ("lru_evicted_pages", ctypes.c_int64)]
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}
@@ -69,6 +71,9 @@ _SIGS = {
     "kv_pool_stats_get": (ctypes.c_int, [_P, ctypes.POINTER(kv_pool_stats)]),
     "kv_session_create": (ctypes.c_int, [_P, _I32, _PI32, _P, _PI32]),
     "kv_session_import_cold": (ctypes.c_int, [_P, _I32, _PI32, _PI32]),
+    "kv_session_extend": (ctypes.c_int, [_P, _I32, _I32, _P]),
+    "kv_session_pause": (ctypes.c_int, [_P, _I32]),
+    "kv_evict_pages": (ctypes.c_int, [_P, _I32, _P, _PI32]),
     "kv_session_destroy": (ctypes.c_int, [_P, _I32, _P]),
     "kv_session_info": (ctypes.c_int, [_P, _I32, _PI32, _PI32, _PI32, _PI32, _I32]),
     "kv_write_tokens": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P]),
@@ -157,6 +162,20 @@ def kv_session_import_cold(pool: int, seq_len: int, cold_pages: Sequence[int]) -
     return sid.value
 
 
+def kv_session_extend(pool: int, sid: int, new_seq_len: int, stream: int = 0) -> None:
+    _check(_lib.kv_session_extend(pool, sid, new_seq_len, stream or None), "kv_session_extend")
+
+
+def kv_session_pause(pool: int, sid: int) -> None:
+    _check(_lib.kv_session_pause(pool, sid), "kv_session_pause")
+
+
+def kv_evict_pages(pool: int, n: int, stream: int = 0) -> int:
+    got = ctypes.c_int32()
+    _check(_lib.kv_evict_pages(pool, n, stream or None, ctypes.byref(got)), "kv_evict_pages")
+    return got.value
+
+
 def kv_session_destroy(pool: int, sid: int, stream: int = 0) -> None:
     _check(_lib.kv_session_destroy(pool, sid, stream or None), "kv_session_destroy")
 
@@ -170,8 +189,8 @@ def kv_session_info(pool: int, sid: int, cap: int = 0):
     n = cap or (seq_len.value + KV_PAGE_TOKENS - 1) // KV_PAGE_TOKENS
     hot, cold = (ctypes.c_int32 * max(n, 1))(), (ctypes.c_int32 * max(n, 1))()
     _check(_lib.kv_session_info(pool, sid, None, None, hot, cold, n), "kv_session_info")
-    nh = n if state.value == KV_SESSION_ACTIVE else 0
-    return state.value, seq_len.value, list(hot[:nh]), list(cold[:n])
+    n = n if state.value != KV_SESSION_FREE else 0
+    return state.value, seq_len.value, list(hot[:n]), list(cold[:n])
 
 
 def kv_write_tokens(pool: int, sid: int, layer: int, tok_begin: int, n_tok: int, k_ptr: int,

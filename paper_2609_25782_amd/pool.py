@@ -73,6 +73,15 @@ class HotColdPool:
     def import_cold(self, seq_len: int, cold_pages: Sequence[int]) -> int:
         return kv.kv_session_import_cold(self.handle, int(seq_len), cold_pages)
 
+    def extend(self, sid: int, new_seq_len: int, stream=None) -> None:
+        kv.kv_session_extend(self.handle, sid, int(new_seq_len), _stream(stream))
+
+    def pause(self, sid: int) -> None:
+        kv.kv_session_pause(self.handle, sid)
+
+    def evict_pages(self, n: int, stream=None) -> int:
+        return kv.kv_evict_pages(self.handle, int(n), _stream(stream))
+
     def destroy_session(self, sid: int, stream=None) -> None:
         kv.kv_session_destroy(self.handle, sid, _stream(stream))
 

@@ -172,8 +172,9 @@ def test_aliased_cold_pages_resume(dev):
 
 
 def test_random_sequences_match_model(dev):
-    """Random create / write / evict / resume / destroy sequences: page tables,
-    statistics and every active page's bytes follow the model exactly."""
+    """Random create / write / evict / pause / LRU-evict / extend / resume /
+    destroy sequences: page tables, statistics and the bytes of every resident
+    page and every valid cold copy follow the model exactly."""
     from paper_2609_25782_amd import hotcold_kv as kv
     from paper_2609_25782_amd.pool import HotColdPool
     nh, nc, ms, stride = 48, 40, 6, 8
@@ -185,8 +186,13 @@ def test_random_sequences_match_model(dev):
     hot_img = pool.hot.view(nh, -1).cpu().numpy().copy()
     cold_img = pool.cold.view(nc, -1).cpu().numpy().copy()
     rng = np.random.default_rng(4)
-    for step in range(300):
-        op = int(rng.integers(0, 5))
+
+    def apply(copies, src_img, dst_img):
+        for a_, b_ in copies:
+            dst_img[b_] = src_img[a_]
+
+    for step in range(400):
+        op = int(rng.integers(0, 8))
         sid = int(rng.integers(0, ms))
         try:
             if op == 0:
@@ -198,6 +204,35 @@ def test_random_sequences_match_model(dev):
                         pool.create_session(L)
                     raise e
                 assert pool.create_session(L) == model_sid
+                apply(model.last_victim_copies, hot_img, cold_img)
+            elif op == 5:
+                try:
+                    model.pause(sid)
+                except Exception as e:
+                    with pytest.raises(kv.KVError):
+                        pool.pause(sid)
+                    raise e
+                pool.pause(sid)
+            elif op == 6:
+                n = int(rng.integers(0, 10))
+                try:
+                    got, copies = model.evict_pages(n)
+                except Exception as e:
+                    with pytest.raises(kv.KVError):
+                        pool.evict_pages(n)
+                    raise e
+                assert pool.evict_pages(n) == got
+                apply(copies, hot_img, cold_img)
+            elif op == 7:
+                new_len = int(rng.integers(0, 16 * stride + 1))
+                try:
+                    model.extend(sid, new_len)
+                except Exception as e:
+                    with pytest.raises(kv.KVError):
+                        pool.extend(sid, new_len)
+                    raise e
+                pool.extend(sid, new_len)
+                apply(model.last_victim_copies, hot_img, cold_img)
             elif op == 1:
                 sids = [int(x) for x in rng.choice(ms, size=int(rng.integers(1, 3)), replace=False)]
                 try:
@@ -218,6 +253,7 @@ def test_random_sequences_match_model(dev):
                         pool.resume(sids)
                     raise e
                 pool.resume(sids)
+                apply(model.last_victim_copies, hot_img, cold_img)  # victims first
                 for per in res:
                     for c, h in per:
                         hot_img[h] = cold_img[c]
@@ -266,11 +302,18 @@ def test_random_sequences_match_model(dev):
             st = pool.stats()
             assert st["free_hot_pages"] == model.free_hot() and st["free_cold_pages"] == model.free_cold()
             assert st["pages_to_cold"] == model.cold_writes
+            assert st["lru_evicted_pages"] == model.lru_evicted
+            assert (st["resume_pages_resident"], st["resume_pages_total"]) == (model.resume_resident,
+                                                                               model.resume_total)
             gpu_hot = pool.hot.view(nh, -1).cpu().numpy()
+            gpu_cold = pool.cold.view(nc, -1).cpu().numpy()
             for s in model.sessions:
-                if s.state == 1:
-                    for p in s.hot:
+                for p in s.hot:
+                    if p >= 0:
                         assert np.array_equal(gpu_hot[p], hot_img[p])
+                for c in s.cold:
+                    if c >= 0:
+                        assert np.array_equal(gpu_cold[c], cold_img[c])
     pool.close()
 
 
@@ -307,4 +350,33 @@ def test_resume_48_layer_pages(dev):
     from helpers import tolerance_check
     tolerance_check(got, case.oracle_out())
     pool.destroy_session(blocker)
+    pool.close()
+
+
+def test_partial_residency_round_trip(dev):
+    """Pause, evict part of a session page by page (LRU), resume: only the missing
+    pages are fetched (the statistics show the hit rate) and decode is bitwise
+    the same as before the pause."""
+    case = Case(1, 32, 4, 128, "bf16", [4000, 1500, 3000], seed=41, slack=1.5)
+    n_pages = sum(synth.pages_for(L) for L in case.seq_lens)
+    pool = build_gpu(case, dev, num_cold_pages=n_pages, pool_kwargs={"max_sessions": 6})
+    q = to_device(case.q, "bf16", dev)
+    sl = torch.tensor(case.seq_lens, dtype=torch.int32, device=dev)
+    before = to_host(pool.decode(0, q, sl))
+    pool.pause(0)
+    pool.pause(2)
+    assert pool.evict_pages(100) == 100          # 100 of session 0's 250 pages (oldest pause)
+    st0 = pool.stats()
+    filler = pool.create_session(16 * 60)        # takes free pages, may evict more LRU pages
+    pool.resume([2, 0])
+    torch.cuda.synchronize()
+    st = pool.stats()
+    fetched = st["pages_to_hot"] - st0["pages_to_hot"]
+    resident = st["resume_pages_resident"] - st0["resume_pages_resident"]
+    assert fetched + resident == synth.pages_for(4000) + synth.pages_for(3000)
+    assert fetched >= 100 and resident > 0
+    after = to_host(pool.decode(0, q, sl, page_table=pool.page_table[:3].contiguous()))
+    torch.cuda.synchronize()
+    assert np.array_equal(before, after)
+    pool.destroy_session(filler)
     pool.close()

@@ -29,19 +29,21 @@ def _same(kv, pool, model, ms):
         s = model.sessions[sid]
         assert state == s.state
         if state:
-            assert L == s.seq_len and cold == s.cold
-            assert hot == (s.hot if state == ACTIVE else [])
+            assert L == s.seq_len and cold == s.cold and hot == s.hot
     st = kv.kv_pool_stats_get(pool)
     assert st["free_hot_pages"] == model.free_hot()
     assert st["free_cold_pages"] == model.free_cold()
     assert st["pages_to_cold"] == model.cold_writes
     assert st["pages_to_hot"] == model.pages_to_hot
     assert st["resumes"] == model.resumes and st["evicts"] == model.evicts
+    assert st["resume_pages_resident"] == model.resume_resident
+    assert st["resume_pages_total"] == model.resume_total
+    assert st["lru_evicted_pages"] == model.lru_evicted
 
 
 def _random_call(kv, pool, rng, nh, nc, ms, stride):
     """One random call as a (model call, library call) pair."""
-    op = int(rng.integers(0, 6))
+    op = int(rng.integers(0, 9))
     sid = int(rng.integers(-1, ms + 1))
     if op == 0:
         L = int(rng.integers(-2, 16 * stride + 20))
@@ -59,6 +61,14 @@ def _random_call(kv, pool, rng, nh, nc, ms, stride):
     if op == 5:
         sids = [int(x) for x in rng.integers(-1, ms + 1, size=int(rng.integers(1, 4)))]
         return (lambda m: (m.evict_many(sids), None)[1]), (lambda: kv.kv_evict_sessions(pool, sids))
+    if op == 6:
+        return (lambda m: m.pause(sid)), (lambda: kv.kv_session_pause(pool, sid))
+    if op == 7:
+        n = int(rng.integers(0, 12))
+        return (lambda m: m.evict_pages(n)[0]), (lambda: kv.kv_evict_pages(pool, n))
+    if op == 8:
+        new_len = int(rng.integers(0, 16 * stride + 20))
+        return (lambda m: m.extend(sid, new_len)), (lambda: kv.kv_session_extend(pool, sid, new_len))
     n = int(rng.integers(0, stride + 1))
     cold = [int(p) for p in rng.choice(nc, size=n, replace=False)]
     L = 16 * n - (int(rng.integers(0, 16)) if n else 0)

@@ -133,3 +133,79 @@ def test_batched_evict_is_atomic():
         m.evict_many([a, b])
     assert e.value.code == ERR_NO_COLD and m.__dict__ == before
     assert m.evict_many([b]) == [(3, 0), (4, 1), (5, 2)]
+
+
+def test_lru_hand_worked_trace():
+    """Page-granular LRU (Sec. III): the longest-paused session's pages go first,
+    in logical order; pages that still have a cold copy cost no write."""
+    m = PoolModel(num_hot=8, num_cold=16, max_sessions=4, max_pages_per_session=8)
+    a = m.create(16 * 3)          # hot 0,1,2
+    b = m.create(16 * 3)          # hot 3,4,5
+    m.pause(a)                    # paused first: least recently used
+    m.pause(b)
+    c = m.create(16 * 4)          # 2 free (6,7) -> evict a's pages 0,1 (hot 0,1)
+    assert m.sessions[c].hot == [0, 1, 6, 7]
+    assert m.sessions[a].hot == [-1, -1, 2] and m.sessions[a].cold == [0, 1, -1]
+    assert m.cold_writes == 2 and m.lru_evicted == 2
+    # resume a: fetches its 2 missing pages; a's resident page stays (hit 1 of 3)
+    m.destroy(c)
+    per = m.resume([a])
+    assert per == [[(0, 0), (1, 1)]] and m.sessions[a].hot == [0, 1, 2]
+    assert (m.resume_resident, m.resume_total) == (1, 3)
+    # pause a again: now b is older; pages 0,1 of a are clean (cold copies valid)
+    m.pause(a)
+    n, copies = m.evict_pages(5)
+    # b's three pages (dirty: written), then a's pages 0 and 1 (clean: no write)
+    assert n == 5 and copies == [(3, 2), (4, 3), (5, 4)]
+    assert m.sessions[a].hot == [-1, -1, 2] and m.sessions[a].cold == [0, 1, -1]
+    assert m.cold_writes == 2 + 3 and m.lru_evicted == 2 + 5
+
+
+def test_resume_hit_rate_and_no_self_eviction():
+    m = PoolModel(num_hot=6, num_cold=16, max_sessions=3, max_pages_per_session=8)
+    a = m.create(16 * 4)
+    m.pause(a)
+    assert m.resume([a]) == [[]] and (m.resume_resident, m.resume_total) == (4, 4)
+    m.pause(a)
+    assert m.evict_pages(3)[0] == 3           # a keeps page 3 resident
+    b = m.create(16 * 5)                      # fills the pool: 5 of 5 free
+    before = copy.deepcopy(m.__dict__)
+    with pytest.raises(ModelError) as e:      # needs 3 pages; only a's own page is evictable
+        m.resume([a])
+    assert e.value.code == ERR_NO_HOT and m.__dict__ == before
+    m.pause(b)                                # now b's pages are evictable
+    per = m.resume([a])
+    assert [len(x) for x in per] == [3] and m.resume_resident == 4 + 1
+
+
+def test_residency_invariant_on_random_sequences():
+    rng = np.random.default_rng(7)
+    nh, nc, ms, stride = 30, 60, 6, 8
+    m = PoolModel(nh, nc, ms, stride)
+    for step in range(4000):
+        op, sid = int(rng.integers(0, 7)), int(rng.integers(0, ms))
+        before = copy.deepcopy(m.__dict__)
+        try:
+            if op == 0:
+                m.create(int(rng.integers(0, 16 * stride + 1)))
+            elif op == 1:
+                m.pause(sid)
+            elif op == 2:
+                m.resume([sid])
+            elif op == 3:
+                m.extend(sid, int(rng.integers(0, 16 * stride + 1)))
+            elif op == 4:
+                m.evict_pages(int(rng.integers(0, 6)))
+            elif op == 5:
+                m.evict(sid)
+            else:
+                m.destroy(sid)
+        except ModelError:
+            assert m.__dict__ == before
+        used = [p for s in m.sessions for p in s.hot if p >= 0]
+        assert len(used) == len(set(used)) and len(used) + m.free_hot() == nh
+        for s in m.sessions:
+            if s.state == ACTIVE:
+                assert all(p >= 0 for p in s.hot) and len(s.hot) == (s.seq_len + 15) // 16
+            if s.state == PAUSED:
+                assert all(p >= 0 or c >= 0 for p, c in zip(s.hot, s.cold))
