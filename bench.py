@@ -206,6 +206,27 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
         main_s.wait_stream(side)
     torch.cuda.synchronize()
     both_ms = sum(e[2 * i].elapsed_time(e[2 * i + 1]) for i in range(steps)) / steps
+    # resume bandwidth budget: a capped copy grid leaves decode more of the GPU
+    budget = []
+    for blocks in (1024, 256, 64):
+        pool.set_copy_blocks(blocks)
+        kv.kv_pool_set_profiling(pool.handle, True)
+        kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        sids = picks[k % len(picks)]
+        k += 1
+        side.wait_stream(main_s)
+        resume_batch(sids, side)
+        ev[0].record(main_s)
+        decode48(main_s)
+        ev[1].record(main_s)
+        main_s.wait_stream(side)
+        torch.cuda.synchronize()
+        n_b, ms_b = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
+        kv.kv_pool_set_profiling(pool.handle, False)
+        budget.append({"copy_blocks": blocks, "resume_ms_per_session": round(ms_b / len(sids), 3),
+                       "decode48_ms_with_concurrent_resume": round(ev[0].elapsed_time(ev[1]), 3)})
+    pool.set_copy_blocks(0)
     # partial residency: sessions paused with all pages resident, a fraction of
     # their pages evicted page by page (LRU; clean, so no cold writes), resumed
     partial = []
@@ -249,7 +270,47 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
         "tbt_impact": round(both_ms / decode_ms, 3),
         "decode48_GBps": round(48 * sum(decode_bytes(w.seq_lens, 32, 4, 128, 2)) / (decode_ms / 1e3) / 1e9, 1),
         "partial_residency": partial,
+        "copy_budget": budget,
     }
+
+
+def measure_host_tier(seed: int):
+    """Resume from a cold tier in pinned host memory (read over PCIe by the copy
+    kernel): 8 one-layer sessions of the benchmark's shape, and one 48-layer
+    session of 32K tokens."""
+    import torch
+    import synth
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+    out = {}
+    rng = np.random.Generator(np.random.PCG64([seed, 13]))
+    for name, layers, lens in (("layer_8_sessions", 1, rng.integers(8192, 32768, size=8, endpoint=True)),
+                               ("step48_1_session", 48, np.array([32768]))):
+        n_pages = int(sum(synth.pages_for(int(L)) for L in lens))
+        pool = HotColdPool(layers, 4, 128, "bf16", n_pages, n_pages, len(lens), synth.pages_for(32768),
+                           cold_location="host")
+        sids = [pool.create_session(int(L)) for L in lens]
+        pool.evict(sids)                       # first write of every page to the host tier
+        torch.cuda.synchronize()
+        times = []
+        for rep in range(3):
+            kv.kv_pool_set_profiling(pool.handle, True)
+            kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
+            pool.resume(sids)
+            n, ms = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
+            times.append(ms)
+            pool.evict(sids)                   # clean: frees the hot pages, writes nothing
+            torch.cuda.synchronize()
+        kv.kv_pool_set_profiling(pool.handle, False)
+        ms = min(times)
+        payload = n_pages * pool.page_bytes
+        out[name] = {"payload_bytes": payload, "resume_ms": round(ms, 3),
+                     "ms_per_session": round(ms / len(lens), 3),
+                     "pcie_GBps": round(payload / (ms / 1e3) / 1e9, 2)}
+        pool.close()
+        del pool
+        torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -433,6 +494,8 @@ def main():
     if not args.no_resume_mix:
         result["resume48"] = measure_resume_mix(args.seed, max(3, args.steps // 4), 1)
         log("resume mix: %s" % json.dumps(result["resume48"]))
+        result["resume_host_tier"] = measure_host_tier(args.seed)
+        log("host tier: %s" % json.dumps(result["resume_host_tier"]))
     if args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
     print(json.dumps(result), flush=True)

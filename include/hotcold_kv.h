@@ -288,6 +288,16 @@ int kv_resume_session(kv_pool* pool, int32_t sid, kv_stream_t stream);
 /* Batched resume: sessions in argument order, atomic as a whole, one launch. */
 int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t stream);
 
+/*
+ * Bandwidth budget of the page copies (resume, eviction): at most `blocks`
+ * 256-thread blocks copy at once (0: the default, enough to fill the GPU).
+ * The paper overlaps eviction and resume with decode (Sec. III, "Architecture
+ * and data paths"); with a device-memory cold tier both share HBM, so a smaller
+ * budget leaves decode more bandwidth and CU slots at the cost of a slower
+ * resume.
+ */
+int kv_pool_set_copy_blocks(kv_pool* pool, int32_t blocks);
+
 /* ----------------------------------------------------------------------- */
 /* Decode attention (data path 1)                                           */
 /* ----------------------------------------------------------------------- */

@@ -61,9 +61,10 @@ struct CopyEntry {
 // For n entries (device array): copies the whole page src_base[e.src] to
 // dst_base[e.dst] where e.src >= 0, and writes page_table[e.pt_index] =
 // e.pt_value where e.pt_index >= 0.
+// max_blocks caps the persistent grid (0: the default cap).
 hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_bytes,
                             const CopyEntry* entries, int32_t n, int32_t* page_table,
-                            hipStream_t s);
+                            int32_t max_blocks, hipStream_t s);
 
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t s);
 

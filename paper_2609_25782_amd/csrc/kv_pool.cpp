@@ -177,6 +177,7 @@ struct kv_pool {
     kv_pool_stats st{};
     int cus = 0;
     int32_t waves_override = 0;
+    int32_t copy_blocks = 0;  // cap of the page-copy grid (0: default)
     StagingSlot ring[kStagingSlots];
     int ring_next = 0;
     hipEvent_t free_event = nullptr;
@@ -282,7 +283,8 @@ struct kv_pool {
             if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(copy list)");
             hipEvent_t p = prof_begin(s);
             e = hck::launch_page_copy(src, dst, page_bytes,
-                                      static_cast<const hck::CopyEntry*>(slot->dev), n, pt, s);
+                                      static_cast<const hck::CopyEntry*>(slot->dev), n, pt,
+                                      copy_blocks, s);
             prof_end(kernel_id, p, s);
             if (e != hipSuccess) return hip_fail(e, "page copy launch");
             e = hipEventRecord(slot->done, s);
@@ -933,6 +935,12 @@ int32_t paged_decode_waves(const kv_pool* pool) {
     if (!pool || pool->meta) return 0;
     DeviceGuard g(pool->d.device);
     return pool->decode_waves();
+}
+
+int kv_pool_set_copy_blocks(kv_pool* pool, int32_t blocks) {
+    if (!pool || blocks < 0) return fail(KV_ERR_INVALID, "bad arguments");
+    pool->copy_blocks = blocks;
+    return KV_OK;
 }
 
 int kv_pool_set_decode_combine(kv_pool* pool, int32_t mode) {

@@ -227,7 +227,7 @@ int grid_for(int64_t work, int cap) {
 
 hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_bytes,
                             const CopyEntry* entries, int32_t n, int32_t* page_table,
-                            hipStream_t s) {
+                            int32_t max_blocks, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     constexpr int64_t kRow = static_cast<int64_t>(kBlockThreads) * 16;  // 4 KiB
     if (page_bytes % kRow) return hipErrorInvalidValue;
@@ -235,7 +235,8 @@ hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_b
     const int u = rows % 8 == 0 ? 8 : rows % 4 == 0 ? 4 : rows % 2 == 0 ? 2 : 1;
     const int64_t chunks = rows / u;
     const int64_t work = chunks * n;
-    const int64_t blocks = work < HCK_COPY_MAX_BLOCKS ? work : HCK_COPY_MAX_BLOCKS;
+    const int64_t cap = max_blocks > 0 ? max_blocks : HCK_COPY_MAX_BLOCKS;
+    const int64_t blocks = work < cap ? work : cap;
     const dim3 grid(static_cast<unsigned>(blocks)), block(kBlockThreads);
     const int cpp = static_cast<int>(chunks);
     switch (u) {

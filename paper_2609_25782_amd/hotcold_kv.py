@@ -82,6 +82,7 @@ _SIGS = {
     "kv_evict_sessions": (ctypes.c_int, [_P, _PI32, _I32, _P]),
     "kv_resume_session": (ctypes.c_int, [_P, _I32, _P]),
     "kv_resume_sessions": (ctypes.c_int, [_P, _PI32, _I32, _P]),
+    "kv_pool_set_copy_blocks": (ctypes.c_int, [_P, _I32]),
     "paged_decode_waves": (_I32, [_P]),
     "kv_pool_set_decode_waves": (ctypes.c_int, [_P, _I32]),
     "kv_pool_set_decode_combine": (ctypes.c_int, [_P, _I32]),
@@ -221,6 +222,10 @@ def kv_resume_session(pool: int, sid: int, stream: int = 0) -> None:
 def kv_resume_sessions(pool: int, sids: Sequence[int], stream: int = 0) -> None:
     _check(_lib.kv_resume_sessions(pool, _i32_array(sids), len(sids), stream or None),
            "kv_resume_sessions")
+
+
+def kv_pool_set_copy_blocks(pool: int, blocks: int) -> None:
+    _check(_lib.kv_pool_set_copy_blocks(pool, blocks), "kv_pool_set_copy_blocks")
 
 
 # -- decode -------------------------------------------------------------------

@@ -110,6 +110,9 @@ class HotColdPool:
         else:
             kv.kv_resume_sessions(self.handle, list(sids), _stream(stream))
 
+    def set_copy_blocks(self, blocks: int) -> None:
+        kv.kv_pool_set_copy_blocks(self.handle, int(blocks))
+
     def stats(self) -> dict:
         return kv.kv_pool_stats_get(self.handle)
 

@@ -37,7 +37,11 @@ def _random_fill(pool, seed):
     g = torch.Generator(device=pool.device)
     g.manual_seed(seed)
     pool.hot.copy_(torch.randint(0, 256, pool.hot.shape, dtype=torch.uint8, device=pool.device, generator=g))
+    # the cold pool may be pinned host memory: generate on the device, then copy
     pool.cold.copy_(torch.randint(0, 256, pool.cold.shape, dtype=torch.uint8, device=pool.device, generator=g))
+
+
+COLD_TIERS = ["device", "host"]
 
 
 def _check_table(pool, model: PoolModel):
@@ -46,12 +50,14 @@ def _check_table(pool, model: PoolModel):
     assert np.array_equal(got, want)
 
 
-def test_tiny_resume_config(dev):
+@pytest.mark.parametrize("cold", COLD_TIERS)
+def test_tiny_resume_config(dev, cold):
     """Two paused sessions of 256 tokens resumed from a 64-page cold pool (fp32,
-    d=64, one layer): exact page table and bytes."""
+    d=64, one layer): exact page table and bytes, cold pool in device memory or
+    in pinned host memory read over PCIe."""
     from paper_2609_25782_amd.pool import HotColdPool
-    _say("tiny resume config")
-    pool = HotColdPool(1, 1, 64, "f32", 80, 64, 8, 32)
+    _say("tiny resume config, cold tier in %s memory" % cold)
+    pool = HotColdPool(1, 1, 64, "f32", 80, 64, 8, 32, cold_location=cold)
     model = PoolModel(80, 64, 8, 32)
     _random_fill(pool, 1)
     torch.cuda.synchronize()
@@ -79,11 +85,12 @@ def test_tiny_resume_config(dev):
     pool.close()
 
 
-def test_evict_resume_round_trip_decode_bitwise(dev):
+@pytest.mark.parametrize("cold", COLD_TIERS)
+def test_evict_resume_round_trip_decode_bitwise(dev, cold):
     """Decode before eviction equals decode after resume into other pages (P8)."""
     case = Case(1, 32, 4, 128, "bf16", [3000, 700, 16, 4099], seed=21, slack=1.3)
     pool = build_gpu(case, dev, num_cold_pages=sum(synth.pages_for(L) for L in case.seq_lens),
-                     pool_kwargs={"max_sessions": 8})
+                     pool_kwargs={"max_sessions": 8, "cold_location": cold})
     q = to_device(case.q, "bf16", dev)
     sl = torch.tensor(case.seq_lens, dtype=torch.int32, device=dev)
     before = to_host(pool.decode(0, q, sl))
@@ -171,14 +178,15 @@ def test_aliased_cold_pages_resume(dev):
     pool.close()
 
 
-def test_random_sequences_match_model(dev):
+@pytest.mark.parametrize("cold", COLD_TIERS)
+def test_random_sequences_match_model(dev, cold):
     """Random create / write / evict / pause / LRU-evict / extend / resume /
     destroy sequences: page tables, statistics and the bytes of every resident
     page and every valid cold copy follow the model exactly."""
     from paper_2609_25782_amd import hotcold_kv as kv
     from paper_2609_25782_amd.pool import HotColdPool
     nh, nc, ms, stride = 48, 40, 6, 8
-    pool = HotColdPool(2, 2, 64, "bf16", nh, nc, ms, stride)
+    pool = HotColdPool(2, 2, 64, "bf16", nh, nc, ms, stride, cold_location=cold)
     model = PoolModel(nh, nc, ms, stride)
     _random_fill(pool, 3)
     torch.cuda.synchronize()
@@ -353,13 +361,15 @@ def test_resume_48_layer_pages(dev):
     pool.close()
 
 
-def test_partial_residency_round_trip(dev):
+@pytest.mark.parametrize("cold", COLD_TIERS)
+def test_partial_residency_round_trip(dev, cold):
     """Pause, evict part of a session page by page (LRU), resume: only the missing
     pages are fetched (the statistics show the hit rate) and decode is bitwise
     the same as before the pause."""
     case = Case(1, 32, 4, 128, "bf16", [4000, 1500, 3000], seed=41, slack=1.5)
     n_pages = sum(synth.pages_for(L) for L in case.seq_lens)
-    pool = build_gpu(case, dev, num_cold_pages=n_pages, pool_kwargs={"max_sessions": 6})
+    pool = build_gpu(case, dev, num_cold_pages=n_pages,
+                     pool_kwargs={"max_sessions": 6, "cold_location": cold})
     q = to_device(case.q, "bf16", dev)
     sl = torch.tensor(case.seq_lens, dtype=torch.int32, device=dev)
     before = to_host(pool.decode(0, q, sl))
