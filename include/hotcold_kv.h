@@ -239,6 +239,8 @@ int kv_session_info(const kv_pool* pool, int32_t sid, int32_t* state, int32_t* s
  * [tok_begin, tok_begin + n_tok) of an ACTIVE session for one layer.  k and v
  * are device arrays [n_tok][num_kv_heads][head_dim] of the pool's dtype.  Pages
  * written to lose their cold copy, so the next eviction writes them again.
+ * On a KV_POOL_METADATA_ONLY pool only that bookkeeping happens (k and v are
+ * ignored and may be NULL): a replay records appended tokens this way.
  * Errors: KV_ERR_INVALID (range beyond seq_len, bad layer), KV_ERR_STATE.
  */
 int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin, int32_t n_tok,

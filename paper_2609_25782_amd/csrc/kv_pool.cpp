@@ -726,7 +726,6 @@ int kv_session_info(const kv_pool* pool, int32_t sid, int32_t* state, int32_t* s
 int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin, int32_t n_tok,
                     const void* k, const void* v, kv_stream_t stream) {
     if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
-    if (pool->meta) return fail(KV_ERR_INVALID, "metadata-only pool has no pages");
     Session* s = pool->session(sid);
     if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
     if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sid);
@@ -734,22 +733,24 @@ int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin
     if (tok_begin < 0 || n_tok < 0 || static_cast<int64_t>(tok_begin) + n_tok > s->seq_len)
         return fail(KV_ERR_INVALID, "token range outside the session");
     if (n_tok == 0) return KV_OK;
-    if (!k || !v) return fail(KV_ERR_INVALID, "NULL k or v");
-    DeviceGuard g(pool->d.device);
-    hck::WriteArgs a;
-    a.hot = pool->hot;
-    a.page_bytes = pool->page_bytes;
-    a.row = pool->pt + static_cast<int64_t>(sid) * pool->d.max_pages_per_session;
-    a.num_kv_heads = pool->d.num_kv_heads;
-    a.head_dim = pool->d.head_dim;
-    a.dtype = pool->d.dtype;
-    a.layer = layer;
-    a.tok_begin = tok_begin;
-    a.n_tok = n_tok;
-    a.k = k;
-    a.v = v;
-    hipError_t e = hck::launch_write_tokens(a, pool->strm(stream));
-    if (e != hipSuccess) return hip_fail(e, "write_tokens launch");
+    if (!pool->meta) {
+        if (!k || !v) return fail(KV_ERR_INVALID, "NULL k or v");
+        DeviceGuard g(pool->d.device);
+        hck::WriteArgs a;
+        a.hot = pool->hot;
+        a.page_bytes = pool->page_bytes;
+        a.row = pool->pt + static_cast<int64_t>(sid) * pool->d.max_pages_per_session;
+        a.num_kv_heads = pool->d.num_kv_heads;
+        a.head_dim = pool->d.head_dim;
+        a.dtype = pool->d.dtype;
+        a.layer = layer;
+        a.tok_begin = tok_begin;
+        a.n_tok = n_tok;
+        a.k = k;
+        a.v = v;
+        hipError_t e = hck::launch_write_tokens(a, pool->strm(stream));
+        if (e != hipSuccess) return hip_fail(e, "write_tokens launch");
+    }
     for (int32_t i = tok_begin / KV_PAGE_TOKENS; i <= (tok_begin + n_tok - 1) / KV_PAGE_TOKENS; ++i) {
         if (s->cold[i] >= 0) {
             pool->release_cold(s->cold[i]);

@@ -43,7 +43,7 @@ def _same(kv, pool, model, ms):
 
 def _random_call(kv, pool, rng, nh, nc, ms, stride):
     """One random call as a (model call, library call) pair."""
-    op = int(rng.integers(0, 9))
+    op = int(rng.integers(0, 10))
     sid = int(rng.integers(-1, ms + 1))
     if op == 0:
         L = int(rng.integers(-2, 16 * stride + 20))
@@ -69,6 +69,10 @@ def _random_call(kv, pool, rng, nh, nc, ms, stride):
     if op == 8:
         new_len = int(rng.integers(0, 16 * stride + 20))
         return (lambda m: m.extend(sid, new_len)), (lambda: kv.kv_session_extend(pool, sid, new_len))
+    if op == 9:
+        t0, n_tok = int(rng.integers(-2, 16 * stride)), int(rng.integers(0, 40))
+        return (lambda m: m.write_tokens(sid, t0, n_tok)), \
+            (lambda: kv.kv_write_tokens(pool, sid, 0, t0, n_tok, 0, 0))
     n = int(rng.integers(0, stride + 1))
     cold = [int(p) for p in rng.choice(nc, size=n, replace=False)]
     L = 16 * n - (int(rng.integers(0, 16)) if n else 0)
@@ -116,6 +120,22 @@ def test_exhaustion_codes():
         kv.kv_resume_session(pool, a)
     assert e.value.status == kv.KV_ERR_STATE
     with pytest.raises(kv.KVError) as e:
-        kv.kv_write_tokens(pool, a, 0, 0, 1, 0, 0)
+        kv.kv_write_tokens(pool, a, 1, 0, 1, 0, 0)          # one layer only
     assert e.value.status == kv.KV_ERR_INVALID
+    kv.kv_pool_destroy(pool)
+
+
+def test_metadata_write_drops_cold_copies():
+    """On a metadata-only pool a write is bookkeeping: the written pages lose
+    their cold copies, so the next eviction writes them again."""
+    kv = _lib()
+    pool = _meta_pool(kv, 8, 8, 2, 4)
+    a = kv.kv_session_create(pool, 40)
+    kv.kv_evict_session(pool, a)
+    kv.kv_resume_session(pool, a)
+    kv.kv_write_tokens(pool, a, 0, 17, 16, 0, 0)           # pages 1 and 2
+    assert kv.kv_session_info(pool, a)[3] == [0, -1, -1]
+    kv.kv_evict_session(pool, a)
+    st = kv.kv_pool_stats_get(pool)
+    assert st["pages_to_cold"] == 5 and kv.kv_session_info(pool, a)[3] == [0, 1, 2]
     kv.kv_pool_destroy(pool)

@@ -1,0 +1,189 @@
+"""The agentic replay driver (CPU only: a metadata-only pool).
+
+Pins: a hand-worked timeline whose counters follow from the scheduling rule,
+write-back LRU and the resume hit rate; the library pool and the oracle's pool
+model driven by the same replay reach identical summaries and session states;
+preemption keeps an over-full active set from stalling; the idle-gap draws have
+the median and mean the paper gives (Sec. IV, Methodology).
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+from oracle.pool_model import ERR_NO_COLD, ERR_NO_HOT, ModelError, PoolModel
+from paper_2609_25782_amd import replay as rp
+
+
+class ModelPool:
+    """The oracle's pool model behind the replay's pool interface."""
+
+    def __init__(self, cfg):
+        self.m = PoolModel(cfg.num_hot_pages, cfg.num_cold_pages, cfg.max_sessions, cfg.stride)
+
+    def refused(self, e):
+        return isinstance(e, ModelError) and e.code in (ERR_NO_HOT, ERR_NO_COLD)
+
+    def create(self, n):
+        return self.m.create(n)
+
+    def extend(self, sid, n):
+        self.m.extend(sid, n)
+
+    def write(self, sid, t0, n):
+        self.m.write_tokens(sid, t0, n)
+
+    def pause(self, sid):
+        self.m.pause(sid)
+
+    def resume(self, sid):
+        self.m.resume([sid])
+
+    def destroy(self, sid):
+        self.m.destroy(sid)
+
+    def stats(self):
+        m = self.m
+        return {"free_hot_pages": m.free_hot(), "free_cold_pages": m.free_cold(),
+                "pages_to_cold": m.cold_writes, "pages_to_hot": m.pages_to_hot,
+                "resumes": m.resumes, "resume_pages_resident": m.resume_resident,
+                "resume_pages_total": m.resume_total, "lru_evicted_pages": m.lru_evicted}
+
+    def close(self):
+        pass
+
+
+def _tiny(**kw):
+    """Page-sized everything: 1 layer, 1 head, D 64, f32 -> 8 KiB pages."""
+    base = dict(num_layers=1, num_kv_heads=1, head_dim=64, elt_bytes=4, weight_bytes=0.0,
+                max_sessions=64, sample_s=1.0, tbt_s=1.0)
+    base.update(kw)
+    cfg = rp.ReplayConfig(**base)
+    return cfg
+
+
+def _pages_bytes(cfg, n):
+    return n * cfg.page_bytes
+
+
+def test_hand_worked_cycle():
+    """N_a = 1, every draw fixed: prompt 16, later prompts 16, 16 decoded tokens
+    per turn, peak 64, idle gap one step, HBM of 4 pages.  Sessions A and B
+    alternate in a 64-step cycle:
+      0  A created (1 page), its first decoded token opens page 2;  15 A pauses
+      16 B created likewise (HBM now full);                          31 B pauses
+      32 A resumes (both pages resident), grows to 4 pages: LRU evicts B's two
+         dirty pages (2 cold writes);                                47 A ends
+      48 B resumes with nothing resident (2 pages fetched), grows to 4; 63 B ends
+    so per cycle: 2 resumes, 2 of 4 resumed pages resident (hit rate 1/2),
+    2 pages written, 2 fetched, 2 evicted by LRU, 128 tokens produced."""
+    cfg = _tiny(n_active=1, prompt0=(16, 16), turn_prompt=(16, 16), turn_decode=(16, 16),
+                peak=(64, 64), gap_median_s=1.0, gap_mean_s=1.0, warmup_s=64, plateau_s=128)
+    cfg.hbm_bytes = _pages_bytes(cfg, 4)
+    cfg.cold_bytes = _pages_bytes(cfg, 4)
+    for pool in (None, ModelPool(cfg)):
+        r = rp.Replay(cfg, pool)
+        s = r.run()
+        assert s["plateau_counts"] == {                          # plateau: two cycles
+            "resumes": 4, "resume_pages_resident": 4, "resume_pages_total": 8,
+            "pages_to_cold": 4, "pages_to_hot": 4, "lru_evicted_pages": 4, "produced_tokens": 256}
+        assert s["resume_hit_rate"] == 0.5
+        st = r.pool.stats()                                       # three cycles in all
+        assert (st["resumes"], st["pages_to_cold"], st["pages_to_hot"]) == (6, 6, 6)
+        assert (st["resume_pages_resident"], st["resume_pages_total"]) == (6, 12)
+        assert st["lru_evicted_pages"] == 6
+        assert (r.sessions_started, r.sessions_finished) == (6, 6)
+        assert s["preemptions"] == 0 and s["refused_admissions"] == 0
+        assert st["free_hot_pages"] == 4 and st["free_cold_pages"] == 4
+        r.close()
+
+
+def _final_state(r):
+    return sorted((a.sid, a.length, a.target, a.turn, a.preempted) for a in r.agents.values())
+
+
+@pytest.mark.parametrize("hot_pages,n_active,seed", [(40, 4, 0), (26, 4, 1), (100, 12, 2)])
+def test_library_pool_matches_oracle_model(hot_pages, n_active, seed):
+    """The same replay over the library and over the oracle's model: every
+    decision depends on the pool, so equal summaries and states mean the
+    library's allocation, LRU, write-back and resume followed the model."""
+    cfg = _tiny(n_active=n_active, prompt0=(10, 40), turn_prompt=(5, 30), turn_decode=(5, 40),
+                peak=(60, 160), gap_median_s=6.0, gap_mean_s=15.0, warmup_s=150, plateau_s=600,
+                seed=seed)
+    cfg.hbm_bytes = _pages_bytes(cfg, hot_pages)
+    cfg.cold_bytes = _pages_bytes(cfg, 400)
+    lib = rp.Replay(cfg)
+    a = lib.run()
+    model = rp.Replay(cfg, ModelPool(cfg))
+    b = model.run()
+    assert a == b
+    assert _final_state(lib) == _final_state(model)
+    c = a["plateau_counts"]        # each case has LRU pressure and partial residency
+    assert 0 < c["resume_pages_resident"] < c["resume_pages_total"] and c["lru_evicted_pages"] > 0
+    # the pool holds exactly the pages of the live sessions' hot and cold copies
+    for sid_state in range(cfg.max_sessions):
+        st, L, hot, cold = rp.kv.kv_session_info(lib.pool.h, sid_state)
+        if st:
+            ms = model.pool.m.sessions[sid_state]
+            assert (L, hot, cold) == (ms.seq_len, ms.hot, ms.cold)
+    live = sum(rp._pages(x.length) for x in lib.agents.values())
+    assert live == lib.live_pages
+    lib.close()
+
+
+def test_preemption_keeps_an_overfull_active_set_moving():
+    """HBM smaller than the active set's growth: sessions are paused mid-turn
+    instead of stalling, and every turn still finishes."""
+    cfg = _tiny(n_active=4, prompt0=(30, 40), turn_prompt=(10, 20), turn_decode=(60, 80),
+                peak=(150, 200), gap_median_s=2.0, gap_mean_s=4.0, warmup_s=50, plateau_s=800)
+    cfg.hbm_bytes = _pages_bytes(cfg, 18)
+    cfg.cold_bytes = _pages_bytes(cfg, 400)
+    lib = rp.Replay(cfg)
+    a = lib.run()
+    b = rp.Replay(cfg, ModelPool(cfg)).run()
+    assert a == b
+    assert a["preemptions"] > 0 and a["sessions_finished"] > 5
+    lib.close()
+
+
+def test_replay_is_deterministic():
+    cfg = _tiny(n_active=6, prompt0=(10, 40), turn_prompt=(5, 30), turn_decode=(5, 40),
+                peak=(60, 160), gap_median_s=6.0, gap_mean_s=15.0, warmup_s=100, plateau_s=300)
+    cfg.hbm_bytes = _pages_bytes(cfg, 80)
+    cfg.cold_bytes = _pages_bytes(cfg, 400)
+    assert rp.run(cfg) == rp.run(cfg)
+    cfg.seed = 1
+    assert rp.run(cfg) != rp.run(rp.ReplayConfig(**{**cfg.__dict__, "seed": 2}))
+
+
+def test_gap_draws_have_the_papers_median_and_mean():
+    cfg = rp.ReplayConfig(tbt_s=0.001)
+    r = rp.Replay(cfg)
+    g = np.array([r._gap_steps() for _ in range(200000)]) * cfg.step_s
+    assert np.median(g) == pytest.approx(8.0, rel=0.02)
+    assert g.mean() == pytest.approx(23.0, rel=0.04)
+    assert r.sigma == pytest.approx(math.sqrt(2 * math.log(23 / 8)))
+    r.close()
+
+
+def test_tbt_line_through_the_printed_points():
+    assert rp.tbt_for(48) == pytest.approx(0.014)
+    assert rp.tbt_for(128) == pytest.approx(0.027)
+
+
+def test_paper_scale_footprint_and_eviction_onset():
+    """At the paper's shape (96 KiB of KV per token, 1.5 MiB pages, 192 GiB HBM
+    minus 56.8 GiB of weights, 3 TiB flash) a resident agent holds about
+    0.82 GiB (Sec. IV) and low concurrency evicts nothing (Sec. IV, Endurance).
+    The per-turn prompt and decode lengths are a reading: the paper does not
+    print them; they are set so that writing every produced block gives its
+    all-KV-to-flash lifetime of about 11 years at N_a = 48."""
+    low = rp.run(rp.ReplayConfig(n_active=16, warmup_s=600, plateau_s=300))
+    assert low["cold_write_GBps"] == 0 and low["resume_hit_rate"] == 1.0
+    assert low["kv_per_resident_session_gib"] == pytest.approx(0.82, rel=0.08)
+    mid = rp.run(rp.ReplayConfig(n_active=48, warmup_s=600, plateau_s=300))
+    assert 0.5 < mid["resume_hit_rate"] < 1.0 and mid["cold_write_GBps"] > 0
+    assert 9.5 < mid["lifetime_years"]["all_kv_to_flash"] < 13.5
+    assert mid["lifetime_years"]["write_on_evict"] > mid["lifetime_years"]["all_kv_to_flash"]
+    assert mid["sessions_per_device"]["hbm_only"] == pytest.approx(165, rel=0.08)
