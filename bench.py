@@ -313,6 +313,86 @@ def measure_host_tier(seed: int):
     return out
 
 
+def measure_agentic_replay(seed: int, plateau_s: float = 20.0):
+    """The replay driver over a device pool of the paper's shape (48 layers, 4 KV
+    heads, 128, bf16, 1.5 MiB pages; 32 query heads), N_a = 32 sessions decoding:
+    40 GiB of hot pages and 160 GiB of device-memory cold pages, so LRU eviction,
+    write-back and partial resumes run on real pages.  The warm-up only moves
+    pages; the plateau also decodes all 48 layers of the running sessions every
+    step.  Times, per step on the GPU: the decode, and the whole step (its
+    admissions, resumes, evictions and page fills plus the decode)."""
+    import torch
+    import synth
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd import replay as rp
+    from paper_2609_25782_amd.pool import HotColdPool
+
+    cfg = rp.ReplayConfig(n_active=32, weight_bytes=0.0, warmup_s=420.0, plateau_s=plateau_s,
+                          sample_s=0.5, max_sessions=320, seed=seed)
+    page = cfg.page_bytes
+    cfg.hbm_bytes = float(40 * 2 ** 30 // page * page)
+    cfg.cold_bytes = float(160 * 2 ** 30 // page * page)
+    hp = HotColdPool(48, 4, 128, "bf16", cfg.num_hot_pages, cfg.num_cold_pages, cfg.max_sessions,
+                     cfg.stride)
+    dp = rp.DevicePool(cfg, hp, seed, float(synth.value_multiplier(1.0)))
+    q = torch.randn(cfg.n_active, 32, 128, generator=torch.Generator().manual_seed(seed))
+    dec = rp.DeviceDecode(hp, q.to(torch.bfloat16).to(hp.device))
+    r = rp.Replay(cfg, dp)
+    prof = [kv.KV_KERNEL_DECODE_SPLIT, kv.KV_KERNEL_DECODE_COMBINE, kv.KV_KERNEL_PAGE_COPY,
+            kv.KV_KERNEL_EVICT_COPY]
+
+    profiled = 300              # the library's per-kernel profiling runs over these steps only
+    kernels = {}
+
+    class Decode:
+        """The decode hook; the library's profiling brackets every launch with
+        events, so it is on for the first plateau steps and off for the rest."""
+        def step_begin(self):
+            if len(dec.marks) in (0, profiled):
+                torch.cuda.synchronize()
+                kv.kv_pool_set_profiling(hp.handle, not dec.marks)
+                for k, name in zip(prof, ("decode_split", "decode_combine", "resume_copy", "evict_copy")):
+                    n, ms = kv.kv_pool_profile_read(hp.handle, k)
+                    if dec.marks:
+                        kernels[name] = {"launches": n, "ms_per_step": round(ms / profiled, 4)}
+            dec.step_begin()
+
+        def __call__(self, lengths):
+            dec(lengths)
+
+    t0 = time.perf_counter()
+    summary = r.run(Decode())
+    wall = time.perf_counter() - t0
+    t = {k: v[profiled:] for k, v in dec.timings().items()}
+    token_bytes = cfg.token_bytes
+    kv_bytes = t["tokens"].astype(np.float64) * token_bytes
+    out = {
+        "config": "48 layers x 4 KV heads x 128 bf16 (1.5 MiB pages), 32 query heads, N_a=32, "
+                  "hot 40 GiB, cold 160 GiB device memory, synthetic trajectories",
+        "plateau_steps": int(len(t["step_ms"]) + profiled),
+        "timed_steps": int(len(t["step_ms"])),
+        "mean_batch": round(float(t["batch"].mean()), 2),
+        "kv_read_per_step_gib": round(float(kv_bytes.mean()) / 2 ** 30, 2),
+        "decode_ms": {"mean": round(float(t["decode_ms"].mean()), 3),
+                      "p50": round(float(np.percentile(t["decode_ms"], 50)), 3),
+                      "p99": round(float(np.percentile(t["decode_ms"], 99)), 3)},
+        "step_ms": {"mean": round(float(t["step_ms"].mean()), 3),
+                    "p50": round(float(np.percentile(t["step_ms"], 50)), 3),
+                    "p99": round(float(np.percentile(t["step_ms"], 99)), 3)},
+        "decode_GBps": round(float(kv_bytes.sum()) / (float(t["decode_ms"].sum()) / 1e3) / 1e9, 1),
+        "kernels_first_%d_steps" % profiled: kernels,
+        "replay": {k: summary[k] for k in ("resume_hit_rate", "resumes_per_s", "resume_miss_mib",
+                                           "sessions_resident", "kv_per_resident_session_gib",
+                                           "preemptions", "refused_admissions", "plateau_counts")},
+        "wall_s": round(wall, 1),
+    }
+    r.close()
+    hp.close()
+    del hp, dp, dec
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -496,6 +576,8 @@ def main():
         log("resume mix: %s" % json.dumps(result["resume48"]))
         result["resume_host_tier"] = measure_host_tier(args.seed)
         log("host tier: %s" % json.dumps(result["resume_host_tier"]))
+        result["agentic_replay"] = measure_agentic_replay(args.seed)
+        log("agentic replay: %s" % json.dumps(result["agentic_replay"]))
     if args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
     print(json.dumps(result), flush=True)

@@ -260,6 +260,17 @@ int kv_fill_synthetic(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed
                       float value_mult, kv_stream_t stream);
 
 /*
+ * kv_fill_synthetic restricted to logical pages [first_page, first_page +
+ * num_pages) of the session (every slot of each, whatever seq_len is); only
+ * those pages lose their cold copy.  A page holds the same values however
+ * often it is filled, so appending tokens can refill the tail page.
+ * Errors: KV_ERR_INVALID (range outside the session's pages), KV_ERR_STATE.
+ */
+int kv_fill_synthetic_pages(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed,
+                            float value_mult, int32_t first_page, int32_t num_pages,
+                            kv_stream_t stream);
+
+/*
  * Evict an ACTIVE session to the cold tier (data path 4) with write-on-evict
  * (Sec. III, "Memory hierarchy and write policy"): only pages without a valid
  * cold copy are copied, each into the lowest free cold page; pages that already
@@ -323,6 +334,17 @@ enum kv_combine_mode {
  * in different orders, so their results agree to float32 rounding, not bit for
  * bit; each mode on its own is deterministic. */
 int kv_pool_set_decode_combine(kv_pool* pool, int32_t mode);
+
+/*
+ * The page table of a decode batch: row i of `table` (device int32
+ * [n][max_pages_per_session]) becomes the pool's row for session sids[i]
+ * (device int32 [n]), read on `stream`; an id outside [0, max_sessions) gives
+ * a row of -1.  One launch per step serves every layer's paged_decode_attention
+ * over the sessions decoding, with pt_stride = max_pages_per_session.
+ * Errors: KV_ERR_INVALID (n < 0 or above 8192, NULL arrays).
+ */
+int paged_decode_gather_table(kv_pool* pool, const int32_t* sids, int32_t n, int32_t* table,
+                              kv_stream_t stream);
 
 /* Device workspace bytes paged_decode_attention needs for this batch. */
 size_t paged_decode_workspace_bytes(const kv_pool* pool, int32_t batch, int32_t num_q_heads);

@@ -48,6 +48,8 @@ constexpr int kMaxDecodeBatch = 8192;
 int decode_split_blocks_per_cu(int head_dim, int dtype, int batch);
 
 // (waves + batch * num_kv_heads) records of 4 int32: (b, g, first page, end page).
+hipError_t launch_gather_rows(const int32_t* pt, int64_t stride, int32_t max_sessions,
+                              const int32_t* sids, int32_t n, int32_t* out, hipStream_t s);
 hipError_t launch_partition(const int32_t* seq_lens, int batch, int num_kv_heads, int waves,
                             int64_t pt_stride, int32_t* slots, hipStream_t s);
 
@@ -72,7 +74,8 @@ struct SynthArgs {
     char* hot;
     int64_t page_bytes;
     const int32_t* row;  // device page-table row of the session
-    int32_t num_pages;   // pages of the session
+    int32_t first_page;  // first logical page filled
+    int32_t num_pages;   // pages filled
     int32_t num_layers, num_kv_heads, head_dim, dtype;
     int32_t gen_sid;
     uint64_t seed;

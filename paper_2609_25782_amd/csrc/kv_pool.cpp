@@ -760,21 +760,27 @@ int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin
     return KV_OK;
 }
 
-int kv_fill_synthetic(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed, float value_mult,
-                      kv_stream_t stream) {
+int kv_fill_synthetic_pages(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed,
+                            float value_mult, int32_t first_page, int32_t num_pages,
+                            kv_stream_t stream) {
     if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
     if (pool->meta) return fail(KV_ERR_INVALID, "metadata-only pool has no pages");
     Session* s = pool->session(sid);
     if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
     if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sid);
     if (gen_sid < 0 || gen_sid >= (1 << 20)) return fail(KV_ERR_INVALID, "gen_sid out of range");
-    if (s->hot.empty()) return KV_OK;
+    const int64_t have = static_cast<int64_t>(s->hot.size());
+    if (first_page < 0 || num_pages < 0 || first_page + static_cast<int64_t>(num_pages) > have)
+        return fail(KV_ERR_INVALID, "pages [%d, %d) outside the session's %lld", first_page,
+                    first_page + num_pages, static_cast<long long>(have));
+    if (num_pages == 0) return KV_OK;
     DeviceGuard g(pool->d.device);
     hck::SynthArgs a;
     a.hot = pool->hot;
     a.page_bytes = pool->page_bytes;
     a.row = pool->pt + static_cast<int64_t>(sid) * pool->d.max_pages_per_session;
-    a.num_pages = static_cast<int32_t>(s->hot.size());
+    a.first_page = first_page;
+    a.num_pages = num_pages;
     a.num_layers = pool->d.num_layers;
     a.num_kv_heads = pool->d.num_kv_heads;
     a.head_dim = pool->d.head_dim;
@@ -784,12 +790,22 @@ int kv_fill_synthetic(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed
     a.value_mult = value_mult;
     hipError_t e = hck::launch_fill_synthetic(a, pool->strm(stream));
     if (e != hipSuccess) return hip_fail(e, "fill_synthetic launch");
-    for (auto& c : s->cold)
-        if (c >= 0) {
-            pool->release_cold(c);
-            c = -1;
+    for (int32_t i = first_page; i < first_page + num_pages; ++i) {
+        if (s->cold[i] >= 0) {
+            pool->release_cold(s->cold[i]);
+            s->cold[i] = -1;
         }
+    }
     return KV_OK;
+}
+
+int kv_fill_synthetic(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed, float value_mult,
+                      kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    Session* s = pool->session(sid);
+    if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+    return kv_fill_synthetic_pages(pool, sid, gen_sid, seed, value_mult, 0,
+                                   static_cast<int32_t>(s->hot.size()), stream);
 }
 
 int kv_evict_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t stream) {
@@ -1034,6 +1050,20 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
     e = hipEventRecord(pool->decode_event, st);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord(decode)");
     pool->decode_pending = true;
+    return KV_OK;
+}
+
+int paged_decode_gather_table(kv_pool* pool, const int32_t* sids, int32_t n, int32_t* table,
+                              kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    if (pool->meta) return fail(KV_ERR_INVALID, "metadata-only pool");
+    if (n < 0 || n > kMaxDecodeBatch || (n > 0 && (!sids || !table)))
+        return fail(KV_ERR_INVALID, "bad arguments");
+    if (n == 0) return KV_OK;
+    DeviceGuard g(pool->d.device);
+    hipError_t e = hck::launch_gather_rows(pool->pt, pool->d.max_pages_per_session, pool->d.max_sessions,
+                                           sids, n, table, pool->strm(stream));
+    if (e != hipSuccess) return hip_fail(e, "gather launch");
     return KV_OK;
 }
 

@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kBlockThreads) void fill_synthetic_kernel(SynthArgs
     const uint64_t key = splitmix_mix(a.seed);
     for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; gi < total;
          gi += static_cast<int64_t>(gridDim.x) * kBlockThreads) {
-        const int page_idx = static_cast<int>(gi / groups_per_page);
+        const int page_idx = a.first_page + static_cast<int>(gi / groups_per_page);
         const int64_t byte = (gi % groups_per_page) * 16;
         const int32_t pid = a.row[page_idx];
         const int64_t lh = byte / (2 * tile);
@@ -197,6 +197,21 @@ __global__ __launch_bounds__(kBlockThreads) void partition_holes_kernel(int32_t*
     }
 }
 
+// Rows of the pool's page table for a batch of session ids; an id outside
+// [0, max_sessions) gives a row of -1.  One thread per output entry.
+__global__ __launch_bounds__(kBlockThreads) void gather_rows_kernel(const int32_t* pt, int64_t stride,
+                                                                    int32_t max_sessions,
+                                                                    const int32_t* sids, int32_t n,
+                                                                    int32_t* out) {
+    const int64_t total = static_cast<int64_t>(n) * stride;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; i < total;
+         i += static_cast<int64_t>(gridDim.x) * kBlockThreads) {
+        const int64_t row = i / stride;
+        const int32_t sid = sids[row];
+        out[i] = (sid >= 0 && sid < max_sessions) ? pt[static_cast<int64_t>(sid) * stride + i % stride] : -1;
+    }
+}
+
 // One thread per wave: enumerate its pieces exactly as the decode kernel does
 // (here the lanes of a hardware wave work on different decode waves).
 __global__ __launch_bounds__(kBlockThreads) void partition_kernel(const int32_t* seq_lens, int batch,
@@ -266,6 +281,15 @@ hipError_t launch_write_tokens(const WriteArgs& a, hipStream_t s) {
     const int64_t work = static_cast<int64_t>(a.n_tok) * a.num_kv_heads * (a.head_dim / x);
     if (work <= 0) return hipSuccess;
     hipLaunchKernelGGL(write_tokens_kernel, dim3(grid_for(work, 16384)), dim3(kBlockThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const int32_t* pt, int64_t stride, int32_t max_sessions,
+                              const int32_t* sids, int32_t n, int32_t* out, hipStream_t s) {
+    const int64_t total = static_cast<int64_t>(n) * stride;
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(gather_rows_kernel, dim3(grid_for(total, 4096)), dim3(kBlockThreads), 0, s, pt,
+                       stride, max_sessions, sids, n, out);
     return hipGetLastError();
 }
 

@@ -78,6 +78,7 @@ _SIGS = {
     "kv_session_info": (ctypes.c_int, [_P, _I32, _PI32, _PI32, _PI32, _PI32, _I32]),
     "kv_write_tokens": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P]),
     "kv_fill_synthetic": (ctypes.c_int, [_P, _I32, _I32, _U64, ctypes.c_float, _P]),
+    "kv_fill_synthetic_pages": (ctypes.c_int, [_P, _I32, _I32, _U64, ctypes.c_float, _I32, _I32, _P]),
     "kv_evict_session": (ctypes.c_int, [_P, _I32, _P]),
     "kv_evict_sessions": (ctypes.c_int, [_P, _PI32, _I32, _P]),
     "kv_resume_session": (ctypes.c_int, [_P, _I32, _P]),
@@ -90,6 +91,7 @@ _SIGS = {
     "paged_decode_attention": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _I32, _I32,
                                               ctypes.c_float, _P, _P, _SZ, _P]),
     "paged_decode_partition": (ctypes.c_int, [_P, _P, _I32, _I32, _P, _P]),
+    "paged_decode_gather_table": (ctypes.c_int, [_P, _P, _I32, _P, _P]),
     "kv_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "kv_last_error": (ctypes.c_char_p, []),
     "kv_pool_set_profiling": (ctypes.c_int, [_P, ctypes.c_int]),
@@ -206,6 +208,12 @@ def kv_fill_synthetic(pool: int, sid: int, gen_sid: int, seed: int, value_mult: 
            "kv_fill_synthetic")
 
 
+def kv_fill_synthetic_pages(pool: int, sid: int, gen_sid: int, seed: int, value_mult: float,
+                            first_page: int, num_pages: int, stream: int = 0) -> None:
+    _check(_lib.kv_fill_synthetic_pages(pool, sid, gen_sid, seed, value_mult, first_page, num_pages,
+                                        stream or None), "kv_fill_synthetic_pages")
+
+
 def kv_evict_session(pool: int, sid: int, stream: int = 0) -> None:
     _check(_lib.kv_evict_session(pool, sid, stream or None), "kv_evict_session")
 
@@ -253,6 +261,11 @@ def paged_decode_attention(pool: int, layer: int, q_ptr: int, page_table_ptr: in
                                        seq_lens_ptr or None, batch, num_q_heads, scale,
                                        out_ptr or None, workspace_ptr or None, ws_bytes,
                                        stream or None), "paged_decode_attention")
+
+
+def paged_decode_gather_table(pool: int, sids_ptr: int, n: int, table_ptr: int, stream: int = 0) -> None:
+    _check(_lib.paged_decode_gather_table(pool, sids_ptr or None, n, table_ptr or None, stream or None),
+           "paged_decode_gather_table")
 
 
 def paged_decode_partition(pool: int, seq_lens_ptr: int, batch: int, waves: int, slots_ptr: int,

@@ -98,6 +98,11 @@ class HotColdPool:
     def fill_synthetic(self, sid: int, gen_sid: int, seed: int, value_mult: float, stream=None) -> None:
         kv.kv_fill_synthetic(self.handle, sid, gen_sid, seed, float(value_mult), _stream(stream))
 
+    def fill_synthetic_pages(self, sid: int, gen_sid: int, seed: int, value_mult: float,
+                             first_page: int, num_pages: int, stream=None) -> None:
+        kv.kv_fill_synthetic_pages(self.handle, sid, gen_sid, seed, float(value_mult), int(first_page),
+                                   int(num_pages), _stream(stream))
+
     def evict(self, sids, stream=None) -> None:
         if isinstance(sids, int):
             kv.kv_evict_session(self.handle, sids, _stream(stream))
@@ -136,6 +141,16 @@ class HotColdPool:
         kv.paged_decode_attention(self.handle, layer, q.data_ptr(), pt.data_ptr(), pt.shape[1],
                                   seq_lens.data_ptr(), B, Hq, float(scale if scale is not None else D ** -0.5),
                                   out.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream))
+        return out
+
+    def gather_table(self, sids: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        """Page-table rows of the given sessions (device int32 ids), for decoding them as a batch."""
+        assert sids.dtype == torch.int32 and sids.is_contiguous() and sids.device == self.device
+        n = sids.shape[0]
+        if out is None:
+            out = torch.empty((n, self.stride), dtype=torch.int32, device=self.device)
+        assert out.shape[0] >= n and out.shape[1] == self.stride and out.is_contiguous()
+        kv.paged_decode_gather_table(self.handle, sids.data_ptr(), n, out.data_ptr(), _stream(stream))
         return out
 
     def partition(self, seq_lens: torch.Tensor, waves: int, stream=None) -> torch.Tensor:

@@ -162,6 +162,119 @@ class LibraryPool:
         self.h = None
 
 
+class DevicePool(LibraryPool):
+    """A device pool (paper_2609_25782_amd.pool.HotColdPool) under the replay:
+    the same pool calls, now moving real pages, plus the KV itself.  Each
+    session gets a generator id when it is created, and every page it is given
+    is filled (all layers, every slot) with the counter-based values of that
+    id, so the contents of any resident page are known without reading it."""
+
+    def __init__(self, cfg: ReplayConfig, pool, seed: int, value_mult: float):
+        super().__init__(cfg, pool.handle)
+        self.dev = pool
+        self.seed, self.mult = seed, value_mult
+        self.gen: Dict[int, int] = {}       # session id -> generator id
+        self.npages: Dict[int, int] = {}
+        self.next_gen = 0
+
+    def _fill(self, sid: int, first: int, n: int) -> None:
+        if n > 0:
+            kv.kv_fill_synthetic_pages(self.h, sid, self.gen[sid], self.seed, self.mult, first, n)
+
+    def create(self, n: int) -> int:
+        sid = kv.kv_session_create(self.h, n)
+        self.gen[sid] = self.next_gen % (1 << 20)
+        self.next_gen += 1
+        self.npages[sid] = _pages(n)
+        self._fill(sid, 0, _pages(n))
+        return sid
+
+    def extend(self, sid: int, n: int) -> None:
+        kv.kv_session_extend(self.h, sid, n)
+        old = self.npages[sid]
+        self.npages[sid] = max(old, _pages(n))
+        self._fill(sid, old, self.npages[sid] - old)
+
+    def write(self, sid: int, t0: int, n: int) -> None:
+        # Pages past the old tail were filled when extend allocated them.  The
+        # tail page that already held tokens is filled again (its values do not
+        # change) and so loses its cold copy, as a write records it.
+        if n > 0 and t0 % PAGE:
+            self._fill(sid, t0 // PAGE, 1)
+
+    def destroy(self, sid: int) -> None:
+        kv.kv_session_destroy(self.h, sid)
+        del self.gen[sid], self.npages[sid]
+
+    def close(self) -> None:
+        self.h = None                        # the HotColdPool owns the handle
+
+
+class DeviceDecode:
+    """The decode of one replay step on a device pool: the page-table rows of
+    the sessions decoding are gathered into a batch table once (one launch),
+    then every layer's paged attention runs over that batch.  Batch row i uses
+    query row i of q.  Records, per step, HIP events around the whole step and
+    around its decode."""
+
+    def __init__(self, pool, q, layers=None):
+        import torch
+        self.torch = torch
+        self.pool = pool
+        self.q = q                           # [max batch, num_q_heads, head_dim]
+        cap = q.shape[0]
+        self.out = torch.empty_like(q)
+        self.table = torch.empty((cap, pool.stride), dtype=torch.int32, device=pool.device)
+        self.meta = torch.zeros((2, cap), dtype=torch.int32, device=pool.device)   # lengths, ids
+        self.host = np.zeros((2, cap), np.int32)
+        self.n = 0
+        self.layers = list(range(pool.num_layers)) if layers is None else list(layers)
+        self.marks: List = []                # per step: (step start, decode start, decode end)
+        self.batch: List[int] = []
+        self.tokens: List[int] = []
+        self._start = None
+
+    def _event(self):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+    def step_begin(self) -> None:
+        self._start = self._event()
+
+    def __call__(self, lengths: List[Tuple[int, int]]) -> None:
+        n = len(lengths)
+        if n > self.q.shape[0]:
+            raise ValueError("batch of %d sessions exceeds the %d query rows" % (n, self.q.shape[0]))
+        self.n = n
+        self.host[0, :n] = [length for _, length in lengths]
+        self.host[1, :n] = [sid for sid, _ in lengths]
+        d0 = self._event()
+        if n:
+            self.meta[:, :n].copy_(self.torch.from_numpy(self.host[:, :n]))   # pageable: host-synchronous
+            self.pool.gather_table(self.meta[1, :n], out=self.table)
+            for layer in self.layers:
+                self.pool.decode(layer, self.q[:n], self.meta[0, :n], page_table=self.table[:n],
+                                 out=self.out[:n])
+        self.marks.append((self._start, d0, self._event()))
+        self.batch.append(n)
+        self.tokens.append(int(self.host[0, :n].sum()))
+
+    def last_batch(self) -> Tuple[List[int], List[int]]:
+        """(session ids, lengths) of the last decoded step, in batch order."""
+        return [int(x) for x in self.host[1, :self.n]], [int(x) for x in self.host[0, :self.n]]
+
+    def timings(self) -> Dict:
+        """Per-step GPU times in ms: the whole step (from its first launch to the
+        end of its decode: admissions, resumes, evictions, page fills, decode)
+        and the decode alone."""
+        self.torch.cuda.synchronize()
+        step = np.array([a.elapsed_time(c) for a, b, c in self.marks])
+        dec = np.array([b.elapsed_time(c) for a, b, c in self.marks])
+        return {"step_ms": step, "decode_ms": dec, "batch": np.array(self.batch),
+                "tokens": np.array(self.tokens)}
+
+
 @dataclass
 class _Agent:
     peak: int
@@ -171,6 +284,8 @@ class _Agent:
     turn: int = 0          # turn counter (stale events carry an older value)
     decode: int = 0        # tokens decoded in the current turn
     preempted: bool = False  # paused mid-turn; the turn continues on admission
+    len0: int = 0          # length when the current (part of the) turn was admitted
+    step0: int = 0         # step of that admission
 
 
 class Replay:
@@ -186,6 +301,7 @@ class Replay:
         self.ready: deque = deque()       # paused sessions whose idle gap is over
         self.preempted: deque = deque()   # sessions paused mid-turn, admitted first
         self.agents: Dict[int, _Agent] = {}
+        self.running: Dict[int, _Agent] = {}      # decoding this step
         self.active = 0
         self.next_id = 0
         self.seq = 0
@@ -257,6 +373,8 @@ class Replay:
             a.decode = self._uniform(self.cfg.turn_decode)
             a.target = a.length + a.decode
         a.turn += 1
+        a.len0, a.step0 = a.length, self.step
+        self.running[aid] = a
         remaining = a.target - a.length
         first_new = PAGE * _pages(a.length) - a.length   # decoded tokens before the next page
         if first_new < remaining:
@@ -274,6 +392,7 @@ class Replay:
             if not self.pool.refused(e):
                 raise
             self._preempt(a, n - 1)
+            del self.running[aid]
             self.preempted.append(aid)
             return
         self._set_length(a, n, True)
@@ -301,6 +420,7 @@ class Replay:
         self._set_length(a, a.target, True)
         self.active_pages -= _pages(a.length)
         self.active -= 1
+        del self.running[aid]
         if a.length >= a.peak:
             self.pool.destroy(a.sid)
             self.live_pages -= _pages(a.length)
@@ -317,8 +437,25 @@ class Replay:
         self.agents[aid] = _Agent(peak=self._uniform(self.cfg.peak))
         return aid
 
-    def _advance(self) -> None:
-        """One decode step."""
+    def decode_lengths(self) -> List[Tuple[int, int]]:
+        """(session id, context length) of every session decoding this step,
+        counting the token it produces."""
+        return [(a.sid, a.len0 + self.step - a.step0 + 1) for a in self.running.values()]
+
+    def _events(self, through_kind: int) -> None:
+        while self.events and self.events[0][0] <= self.step and self.events[0][1] <= through_kind:
+            _, kind, _, aid, turn = heapq.heappop(self.events)
+            a = self.agents.get(aid)
+            if a is None or a.turn != turn:
+                continue
+            if kind == _EXT:
+                self._on_ext(aid)
+            else:
+                self._on_end(aid)
+
+    def _advance(self, decode_fn=None) -> None:
+        """One decode step: admissions, page allocations for this step's tokens,
+        the decode itself (decode_fn, given decode_lengths()), turn ends."""
         while self.gaps and self.gaps[0][0] <= self.step:
             self.ready.append(heapq.heappop(self.gaps)[2])
         while self.active < self.cfg.n_active:
@@ -329,24 +466,24 @@ class Replay:
                     self.refused_admissions += 1
                     break
                 queue.popleft()
+            elif len(self.agents) >= self.cfg.max_sessions:   # every page-table row in use
+                self.refused_admissions += 1
+                break
             else:
                 aid = self._new_agent()
                 if not self._admit(aid):
                     del self.agents[aid]
                     self.refused_admissions += 1
                     break
-        while self.events and self.events[0][0] <= self.step:
-            _, kind, _, aid, turn = heapq.heappop(self.events)
-            a = self.agents.get(aid)
-            if a is None or a.turn != turn:
-                continue
-            if kind == _EXT:
-                self._on_ext(aid)
-            else:
-                self._on_end(aid)
+        self._events(_EXT)
+        if decode_fn is not None:
+            decode_fn(self.decode_lengths())
+        self._events(_END)
 
     # -- run -----------------------------------------------------------------
-    def run(self) -> Dict:
+    def run(self, decode_fn=None) -> Dict:
+        """Warm-up, then the plateau; decode_fn (if any) runs the decode of each
+        plateau step on a device pool."""
         cfg = self.cfg
         warm = int(round(cfg.warmup_s / cfg.step_s))
         total = warm + int(round(cfg.plateau_s / cfg.step_s))
@@ -357,7 +494,9 @@ class Replay:
         for self.step in range(total):
             if self.step == warm:
                 base = self.pool.stats()
-            self._advance()
+            if self.step >= warm and hasattr(decode_fn, "step_begin"):
+                decode_fn.step_begin()
+            self._advance(decode_fn if self.step >= warm else None)
             if self.step >= warm and (self.step - warm) % every == 0:
                 st = self.pool.stats()
                 samples.append((cfg.num_hot_pages - st["free_hot_pages"],

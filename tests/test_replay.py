@@ -187,3 +187,34 @@ def test_paper_scale_footprint_and_eviction_onset():
     assert 9.5 < mid["lifetime_years"]["all_kv_to_flash"] < 13.5
     assert mid["lifetime_years"]["write_on_evict"] > mid["lifetime_years"]["all_kv_to_flash"]
     assert mid["sessions_per_device"]["hbm_only"] == pytest.approx(165, rel=0.08)
+
+
+@pytest.mark.parametrize("hot_pages,n_active", [(26, 4), (18, 4), (100, 12)])
+def test_decode_lengths_stay_within_resident_pages(hot_pages, n_active):
+    """What a device decode would read: every length handed to the decode hook
+    belongs to an ACTIVE session, grows by one token a step, and stays within
+    the session's allocated pages, all of them resident."""
+    cfg = _tiny(n_active=n_active, prompt0=(10, 40), turn_prompt=(5, 30), turn_decode=(5, 40),
+                peak=(60, 160), gap_median_s=6.0, gap_mean_s=15.0, warmup_s=20, plateau_s=500)
+    cfg.hbm_bytes = _pages_bytes(cfg, hot_pages)
+    cfg.cold_bytes = _pages_bytes(cfg, 400)
+    r = rp.Replay(cfg)
+    last = {}
+    seen = [0]
+
+    def check(lengths):
+        sids = [s for s, _ in lengths]
+        assert len(sids) == len(set(sids)) and len(sids) <= n_active
+        aid_of = {a.sid: aid for aid, a in r.running.items()}   # session ids are reused
+        for sid, n in lengths:
+            state, L, hot, _ = rp.kv.kv_session_info(r.pool.h, sid)
+            assert state == rp.kv.KV_SESSION_ACTIVE
+            assert 0 < n <= 16 * len(hot) and all(p >= 0 for p in hot)
+            assert n >= L
+            assert last.get(aid_of[sid], 0) <= n
+            last[aid_of[sid]] = n
+            seen[0] += 1
+
+    r.run(check)
+    assert seen[0] > 1000
+    r.close()
