@@ -56,7 +56,8 @@ def _pages(n: int) -> int:
 
 def tbt_for(n_active: int) -> float:
     """Seconds per decode step: the straight line through the two points the
-    paper prints for its design (14 ms at N_a = 48, 27 ms at N_a = 128)."""
+    paper gives for its design (14 ms at N_a = 48, 27 ms at N_a = 128; Sec. IV,
+    "Capacity and latency")."""
     return 0.014 + (n_active - 48) * (0.027 - 0.014) / (128 - 48)
 
 
