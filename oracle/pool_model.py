@@ -33,6 +33,25 @@ Readings where the paper is silent (each is stated in the design notes):
 * Cold pages may be shared by several paused sessions (a virtualised cold
   pool); they are reference counted and freed when the last user lets go.
 * Every failing call leaves the whole state unchanged.
+
+Spill (a pool option; Sec. III: no hard pinning, blocks spill under extreme
+pressure instead of failing):
+
+* When a call needs more hot pages than are free plus evictable (the resident
+  pages of paused sessions), it first evicts all of those, then places the rest
+  in the cold tier: new pages (create, extend) get fresh cold pages, lowest id
+  first after the victims' write-back pages; missing pages of resumed sessions
+  stay where they are.  Pages are taken for hot residence in call order and
+  logical page order, the remainder spills.
+* A spilled page's page-table entry is its cold id with the cold tier bit set;
+  decode reads it from the cold tier.  Its cold copy is the page itself, so
+  evicting it writes nothing.  The entry keeps naming the cold page while the
+  session is paused, until the page is fetched or the whole session evicted.
+* Writing tokens into a spilled page writes the cold page in place; a cold page
+  shared with another session cannot be written (state error).
+* promote(n) moves up to n spilled pages of active sessions (session id order,
+  logical page order) into hot pages, evicting paused pages by LRU if needed,
+  since active pages are the more recently used.  Cold copies stay valid.
 """
 
 from __future__ import annotations
@@ -45,6 +64,8 @@ PAGE_TOKENS = 16
 FREE, ACTIVE, PAUSED = 0, 1, 2
 
 OK, ERR_INVALID, ERR_STATE, ERR_NO_HOT, ERR_NO_COLD = 0, -1, -2, -3, -4
+
+COLD_BIT = 1 << 30     # page-table entry names a cold-tier page
 
 
 class ModelError(Exception):
@@ -60,6 +81,7 @@ class _Session:
     stamp: int = 0
     hot: List[int] = field(default_factory=list)   # -1 = not resident
     cold: List[int] = field(default_factory=list)  # -1 = no valid cold copy
+    spilled: List[bool] = field(default_factory=list)  # row entry names the cold page
 
 
 def _pages(seq_len: int) -> int:
@@ -67,7 +89,9 @@ def _pages(seq_len: int) -> int:
 
 
 class PoolModel:
-    def __init__(self, num_hot: int, num_cold: int, max_sessions: int, max_pages_per_session: int):
+    def __init__(self, num_hot: int, num_cold: int, max_sessions: int, max_pages_per_session: int,
+                 spill: bool = False):
+        self.spill = spill
         self.num_hot, self.num_cold = num_hot, num_cold
         self.max_sessions, self.stride = max_sessions, max_pages_per_session
         self.hot_free = set(range(num_hot))
@@ -82,6 +106,8 @@ class PoolModel:
         self.resume_resident = 0      # pages found resident by resumes
         self.resume_total = 0         # pages of resumed sessions
         self.lru_evicted = 0          # pages evicted page by page
+        self.spilled_pages = 0        # pages placed or left in the cold tier by spill
+        self.promoted_pages = 0       # spilled pages moved back to the hot tier
 
     # -- helpers -----------------------------------------------------------
     @staticmethod
@@ -122,20 +148,26 @@ class PoolModel:
                     out.append((sid, i))
         return out
 
-    def _plan(self, k: int, exclude=()):
-        """k hot pages, with the LRU victims to evict first.  Changes nothing.
-        Returns (victims, cold pages for the dirty victims, the k hot pages)."""
+    def _plan(self, k: int, exclude=(), fresh_spill: bool = True, spill: Optional[bool] = None):
+        """k pages, hot ones with the LRU victims to evict first.  Changes nothing.
+        Returns (victims, cold pages for the dirty victims, the hot pages, and
+        the fresh cold pages of the spilled remainder).  Without spill the hot
+        pages number k or the call fails; with it, fewer hot pages leave the
+        remainder spilled (fresh cold pages only if fresh_spill)."""
+        spill = self.spill if spill is None else spill
         victims = []
         if k > len(self.hot_free):
             victims = self._lru(k - len(self.hot_free), exclude)
-            if len(victims) < k - len(self.hot_free):
+            if len(victims) < k - len(self.hot_free) and not spill:
                 raise ModelError(ERR_NO_HOT, "hot pool exhausted")
         dirty = sum(1 for sid, i in victims if self.sessions[sid].cold[i] < 0)
-        if dirty > len(self.cold_free):
+        n_hot = min(k, len(self.hot_free) + len(victims))
+        n_spill = (k - n_hot) if fresh_spill else 0
+        if dirty + n_spill > len(self.cold_free):
             raise ModelError(ERR_NO_COLD, "cold pool exhausted")
-        cold = self._lowest(self.cold_free, dirty)
+        both = self._lowest(self.cold_free, dirty + n_spill)
         after = set(self.hot_free) | {self.sessions[sid].hot[i] for sid, i in victims}
-        return victims, cold, self._lowest(after, k)
+        return victims, both[:dirty], self._lowest(after, n_hot), both[dirty:]
 
     def _evict_victims(self, victims, cold):
         """Apply the victims; returns their (hot_src, cold_dst) copies."""
@@ -158,6 +190,12 @@ class PoolModel:
         for p in pages:
             self.hot_free.remove(p)
 
+    def _take_cold(self, pages):
+        for c in pages:
+            self.cold_free.remove(c)
+            self.cold_ref[c] = 1
+        self.spilled_pages += len(pages)
+
     # -- calls ---------------------------------------------------------------
     def create(self, seq_len: int, pages: Optional[Sequence[int]] = None) -> int:
         if seq_len < 0 or _pages(seq_len) > self.stride:
@@ -169,11 +207,15 @@ class PoolModel:
             pages = [int(p) for p in pages]
             if len(pages) != n or len(set(pages)) != n or any(p not in self.hot_free for p in pages):
                 raise ModelError(ERR_INVALID, "pages not free/distinct")
+            spill = []
         else:
-            victims, cold, pages = self._plan(n)
+            victims, cold, pages, spill = self._plan(n)
         self.last_victim_copies = self._evict_victims(victims, cold)
         self._take_hot(pages)
-        self.sessions[sid] = _Session(ACTIVE, seq_len, 0, list(pages), [-1] * n)
+        self._take_cold(spill)
+        self.sessions[sid] = _Session(ACTIVE, seq_len, 0, list(pages) + [-1] * len(spill),
+                                      [-1] * len(pages) + list(spill),
+                                      [False] * len(pages) + [True] * len(spill))
         return sid
 
     def extend(self, sid: int, new_len: int) -> None:
@@ -183,11 +225,13 @@ class PoolModel:
         if new_len < s.seq_len or _pages(new_len) > self.stride:
             raise ModelError(ERR_INVALID, "bad length")
         add = _pages(new_len) - len(s.hot)
-        victims, cold, pages = self._plan(add)
+        victims, cold, pages, spill = self._plan(add)
         self.last_victim_copies = self._evict_victims(victims, cold)
         self._take_hot(pages)
-        s.hot += pages
-        s.cold += [-1] * add
+        self._take_cold(spill)
+        s.hot += list(pages) + [-1] * len(spill)
+        s.cold += [-1] * len(pages) + list(spill)
+        s.spilled += [False] * len(pages) + [True] * len(spill)
         s.seq_len = new_len
 
     def pause(self, sid: int) -> None:
@@ -218,7 +262,8 @@ class PoolModel:
         for p in cold_pages:
             self.cold_free.discard(p)
             self.cold_ref[p] += 1
-        self.sessions[sid] = _Session(PAUSED, seq_len, self._tick(), [-1] * n, list(cold_pages))
+        self.sessions[sid] = _Session(PAUSED, seq_len, self._tick(), [-1] * n, list(cold_pages),
+                                      [False] * n)
         return sid
 
     def evict(self, sid: int):
@@ -249,8 +294,10 @@ class PoolModel:
                     s.cold[i] = c
                     copies.append((s.hot[i], c))
                     self.cold_writes += 1
-                self.hot_free.add(s.hot[i])
+                if s.hot[i] >= 0:
+                    self.hot_free.add(s.hot[i])
                 s.hot[i] = -1
+                s.spilled[i] = False
             s.state = PAUSED
             s.stamp = self._tick()
             self.evicts += 1
@@ -269,19 +316,26 @@ class PoolModel:
             if s.state != PAUSED:
                 raise ModelError(ERR_STATE, "not paused")
             need += sum(1 for p in s.hot if p < 0)
-        victims, cold, pages = self._plan(need, exclude=set(sids))
+        victims, cold, pages, _ = self._plan(need, exclude=set(sids), fresh_spill=False)
         self.last_victim_copies = self._evict_victims(victims, cold)
         self._take_hot(pages)
+        self.spilled_pages += need - len(pages)
         out, it = [], iter(pages)
         for sid in sids:
             s = self.sessions[sid]
             per = []
+            resident = sum(1 for p in s.hot if p >= 0)
             for i, p in enumerate(s.hot):
                 if p < 0:
-                    s.hot[i] = next(it)
+                    h = next(it, None)
+                    if h is None:                 # stays in the cold tier
+                        s.spilled[i] = True
+                        continue
+                    s.hot[i] = h
+                    s.spilled[i] = False
                     per.append((s.cold[i], s.hot[i]))
             self.pages_to_hot += len(per)
-            self.resume_resident += len(s.hot) - len(per)
+            self.resume_resident += resident
             self.resume_total += len(s.hot)
             s.state = ACTIVE
             self.resumes += 1
@@ -294,8 +348,11 @@ class PoolModel:
             raise ModelError(ERR_INVALID if s.state == ACTIVE else ERR_STATE, "bad write")
         if n_tok == 0:
             return
-        for i in range(tok_begin // PAGE_TOKENS, (tok_begin + n_tok - 1) // PAGE_TOKENS + 1):
-            if s.cold[i] >= 0:
+        span = range(tok_begin // PAGE_TOKENS, (tok_begin + n_tok - 1) // PAGE_TOKENS + 1)
+        if any(s.hot[i] < 0 and self.cold_ref[s.cold[i]] > 1 for i in span):
+            raise ModelError(ERR_STATE, "spilled page shared with another session")
+        for i in span:
+            if s.hot[i] >= 0 and s.cold[i] >= 0:
                 self._release_cold(s.cold[i])
                 s.cold[i] = -1
 
@@ -309,11 +366,32 @@ class PoolModel:
                 self._release_cold(c)
         self.sessions[sid] = _Session()
 
+    def promote(self, n: int):
+        """Move up to n spilled pages of active sessions to the hot tier.
+        Returns the (cold_src, hot_dst) copies."""
+        if n < 0:
+            raise ModelError(ERR_INVALID, "negative count")
+        want = [(sid, i) for sid, s in enumerate(self.sessions) if s.state == ACTIVE
+                for i, p in enumerate(s.hot) if p < 0][:n]
+        victims, cold, pages, _ = self._plan(len(want), fresh_spill=False, spill=True)
+        self.last_victim_copies = self._evict_victims(victims, cold)
+        self._take_hot(pages)
+        copies = []
+        for (sid, i), h in zip(want, pages):
+            s = self.sessions[sid]
+            s.hot[i] = h
+            s.spilled[i] = False
+            copies.append((s.cold[i], h))
+        self.promoted_pages += len(copies)
+        self.pages_to_hot += len(copies)
+        return copies
+
     # -- views ---------------------------------------------------------------
     def row(self, sid: int) -> List[int]:
         """Expected page-table row (length = row stride)."""
         s = self.sessions[sid]
-        r = list(s.hot) if s.state != FREE else []
+        r = [] if s.state == FREE else [
+            h if h >= 0 else (c | COLD_BIT if sp else -1) for h, c, sp in zip(s.hot, s.cold, s.spilled)]
         return r + [-1] * (self.stride - len(r))
 
     def table(self) -> List[List[int]]:

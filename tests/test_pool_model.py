@@ -209,3 +209,111 @@ def test_residency_invariant_on_random_sequences():
                 assert all(p >= 0 for p in s.hot) and len(s.hot) == (s.seq_len + 15) // 16
             if s.state == PAUSED:
                 assert all(p >= 0 or c >= 0 for p, c in zip(s.hot, s.cold))
+
+
+def test_spill_hand_worked_trace():
+    """Spill (Sec. III: no pinning; blocks spill instead of failing): pages that
+    find no hot page live in the cold tier, named in the row with the cold bit;
+    promote brings them back by evicting paused pages first."""
+    from oracle.pool_model import COLD_BIT as C
+    m = PoolModel(num_hot=4, num_cold=10, max_sessions=3, max_pages_per_session=4, spill=True)
+    a = m.create(16 * 3)                          # hot 0,1,2
+    b = m.create(16 * 3)                          # hot 3, then two pages spill to cold 0,1
+    assert m.row(b) == [3, 0 | C, 1 | C, -1] and m.sessions[b].cold == [-1, 0, 1]
+    assert m.spilled_pages == 2 and m.free_hot() == 0
+    m.pause(a)
+    copies = m.promote(5)                         # evicts a's pages 0,1 (dirty -> cold 2,3)
+    assert m.last_victim_copies == [(0, 2), (1, 3)] and copies == [(0, 0), (1, 1)]
+    assert m.row(b) == [3, 0, 1, -1] and m.sessions[b].cold == [-1, 0, 1]
+    assert m.row(a) == [-1, -1, 2, -1] and m.sessions[a].cold == [2, 3, -1]
+    assert (m.cold_writes, m.lru_evicted, m.promoted_pages, m.pages_to_hot) == (2, 2, 2, 2)
+    m.write_tokens(b, 16, 1)                      # resident page 1 loses its cold copy 0
+    assert m.sessions[b].cold == [-1, -1, 1] and 0 in m.cold_free
+    assert m.resume([a]) == [[]]                  # nothing evictable: both pages stay cold
+    assert m.row(a) == [2 | C, 3 | C, 2, -1] and m.spilled_pages == 4
+    assert (m.resume_resident, m.resume_total) == (1, 3)
+    m.write_tokens(a, 0, 1)                       # in place in cold page 2
+    assert m.sessions[a].cold == [2, 3, -1]
+    assert m.evict(a) == [(2, 0)]                 # only the resident dirty page is written
+    assert m.row(a) == [-1, -1, -1, -1] and m.sessions[a].cold == [2, 3, 0]
+    assert m.cold_writes == 3
+
+
+def test_spill_refusals_change_nothing():
+    from oracle.pool_model import COLD_BIT as C
+    m = PoolModel(num_hot=2, num_cold=4, max_sessions=4, max_pages_per_session=8, spill=True)
+    a = m.create(16 * 4)                          # 2 hot + 2 spilled (cold 0,1)
+    before = copy.deepcopy(m.__dict__)
+    with pytest.raises(ModelError) as e:
+        m.create(16 * 3)                          # 3 pages to spill, 2 cold pages free
+    assert e.value.code == ERR_NO_COLD and m.__dict__ == before
+    b = m.import_cold(16, [2])
+    c = m.import_cold(16, [2])                    # cold page 2 shared by b and c
+    m.resume([b])                                 # no free or evictable hot page: stays cold
+    assert m.row(b)[0] == 2 | C and m.sessions[a].hot == [0, 1, -1, -1]
+    before = copy.deepcopy(m.__dict__)
+    with pytest.raises(ModelError) as e:          # a shared spilled page is not written in place
+        m.write_tokens(b, 0, 1)
+    assert e.value.code == ERR_STATE and m.__dict__ == before
+    m.destroy(c)
+    m.write_tokens(b, 0, 1)
+    assert m.row(b)[0] == 2 | C and m.sessions[b].cold == [2]
+    m.pause(a)
+    assert m.promote(3) == [(2, 0)]               # a's page 0 is written to cold 3 first
+    assert m.last_victim_copies == [(0, 3)] and m.row(b)[0] == 0
+    before = copy.deepcopy(m.__dict__)
+    with pytest.raises(ModelError) as e:          # a's dirty page 1 and one spilled page need
+        m.extend(b, 16 * 3)                       # two cold pages; none is free
+    assert e.value.code == ERR_NO_COLD and m.__dict__ == before
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_spill_invariants_on_random_sequences(seed):
+    from oracle.pool_model import COLD_BIT as C
+    rng = np.random.default_rng(100 + seed)
+    nh, nc, ms, stride = 12, 80, 6, 8
+    m = PoolModel(nh, nc, ms, stride, spill=True)
+    spills = 0
+    for step in range(3000):
+        op, sid = int(rng.integers(0, 8)), int(rng.integers(0, ms))
+        before = copy.deepcopy(m.__dict__)
+        try:
+            if op == 0:
+                m.create(int(rng.integers(0, 16 * stride + 1)))
+            elif op == 1:
+                m.pause(sid)
+            elif op == 2:
+                m.resume([sid])
+            elif op == 3:
+                m.extend(sid, int(rng.integers(0, 16 * stride + 1)))
+            elif op == 4:
+                m.promote(int(rng.integers(0, 6)))
+            elif op == 5:
+                m.evict(sid)
+            elif op == 6:
+                s = m.sessions[sid]
+                if s.state == ACTIVE and s.seq_len:
+                    t0 = int(rng.integers(0, s.seq_len))
+                    m.write_tokens(sid, t0, int(rng.integers(0, s.seq_len - t0 + 1)))
+            else:
+                m.destroy(sid)
+        except ModelError:
+            assert m.__dict__ == before
+        spills = max(spills, m.spilled_pages)
+        used = [p for s in m.sessions for p in s.hot if p >= 0]
+        assert len(used) == len(set(used)) and len(used) + m.free_hot() == nh
+        refs = [0] * nc
+        for s in m.sessions:
+            for c in s.cold:
+                if c >= 0:
+                    refs[c] += 1
+        assert refs == m.cold_ref
+        for sid2, s in enumerate(m.sessions):
+            if s.state == ACTIVE:
+                assert len(s.hot) == (s.seq_len + 15) // 16
+                assert all(h >= 0 or (sp and c >= 0) for h, c, sp in zip(s.hot, s.cold, s.spilled))
+            if s.state != 0:
+                for e, h, c, sp in zip(m.row(sid2), s.hot, s.cold, s.spilled):
+                    assert e == (h if h >= 0 else (c | C if sp else -1))
+                    assert not (sp and h >= 0)
+    assert spills > 20
