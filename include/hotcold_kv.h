@@ -95,13 +95,25 @@ enum kv_session_state { KV_SESSION_FREE = 0, KV_SESSION_ACTIVE = 1, KV_SESSION_P
 /* kv_pool_desc.flags */
 #define KV_POOL_METADATA_ONLY 1  /* bookkeeping only: no buffers, no device work */
 
+/*
+ * Page-table entry tags.  An entry below KV_PAGE_STAGED is a hot page id;
+ * KV_PAGE_COLD | c names page c of the cold pool (a spilled page, read by
+ * decode in place); KV_PAGE_STAGED | s names slot s of the staging buffer of
+ * the layer being decoded (see paged_decode_stage).  -1 and other negative
+ * values are "no page".  Tagged entries are read only by pools with spill
+ * enabled or a staging buffer set; elsewhere they are invalid ids.
+ */
+#define KV_PAGE_COLD (1 << 30)
+#define KV_PAGE_STAGED (1 << 29)
+
 /* Kernel ids for the profiling hook. */
 enum kv_kernel_id {
     KV_KERNEL_DECODE_SPLIT = 0,   /* split-K paged decode attention */
     KV_KERNEL_DECODE_COMBINE = 1, /* combine of split partials */
     KV_KERNEL_PAGE_COPY = 2,      /* resume gather (cold -> hot) */
     KV_KERNEL_EVICT_COPY = 3,     /* eviction scatter and row clears (hot -> cold) */
-    KV_KERNEL_COUNT = 4
+    KV_KERNEL_PREFETCH_COPY = 4,  /* one layer's slices of spilled pages -> staging */
+    KV_KERNEL_COUNT = 5
 };
 
 typedef void* kv_stream_t;
@@ -136,6 +148,8 @@ typedef struct kv_pool_stats {
     int64_t resume_pages_resident; /* pages already in the hot tier when their session resumed */
     int64_t resume_pages_total;    /* pages of resumed sessions (hit rate = resident / total) */
     int64_t lru_evicted_pages;     /* pages of paused sessions evicted page by page (LRU) */
+    int64_t spilled_pages;         /* pages placed or left in the cold tier by spill */
+    int64_t promoted_pages;        /* spilled pages moved back to the hot tier */
 } kv_pool_stats;
 
 /* ----------------------------------------------------------------------- */
@@ -211,6 +225,35 @@ int kv_session_pause(kv_pool* pool, int32_t sid);
  * Errors: KV_ERR_NO_COLD_PAGES (nothing changes).
  */
 int kv_evict_pages(kv_pool* pool, int32_t n, kv_stream_t stream, int32_t* evicted);
+
+/*
+ * Spill (enable = 1; off by default).  The paper does not pin active KV in HBM:
+ * when the active set alone outgrows it, blocks spill to the capacity tier
+ * instead of the call failing (Sec. III, "Eviction, resume and decode").  With
+ * spill on, an allocating call that finds too few hot pages even after
+ * evicting every resident page of paused sessions places the remaining new
+ * pages in fresh cold pages (kv_session_create, kv_session_extend; hot pages
+ * first in logical order), and a resume leaves the pages it cannot fetch in
+ * the cold tier.  Such a page's row entry is KV_PAGE_COLD | cold id; decode
+ * reads it from the cold tier, and kv_write_tokens / kv_fill_synthetic_pages
+ * write it in place (refused with KV_ERR_STATE if that cold page is shared
+ * with another session).  It is its own cold copy, so evicting it writes
+ * nothing; its entry keeps naming the cold page until the page is fetched or
+ * the whole session is evicted.
+ * Errors: KV_ERR_INVALID.
+ */
+int kv_pool_set_spill(kv_pool* pool, int32_t enable);
+
+/*
+ * Move up to n spilled pages of ACTIVE sessions (session id order, logical page
+ * order) back into hot pages, evicting resident pages of paused sessions by LRU
+ * when no hot page is free: active pages are the more recently used (Sec.
+ * III).  Their cold copies stay valid.  *promoted (nullable) gets the number
+ * moved; it is smaller than n when the hot tier is full of active pages.
+ * Errors: KV_ERR_INVALID, KV_ERR_NO_COLD_PAGES (evicted pages need cold copies;
+ * nothing changes).
+ */
+int kv_promote_pages(kv_pool* pool, int32_t n, kv_stream_t stream, int32_t* promoted);
 
 /*
  * Register a PAUSED session of seq_len tokens whose KV already sits in the given
@@ -345,6 +388,48 @@ int kv_pool_set_decode_combine(kv_pool* pool, int32_t mode);
  */
 int paged_decode_gather_table(kv_pool* pool, const int32_t* sids, int32_t n, int32_t* table,
                               kv_stream_t stream);
+
+/*
+ * One-step-ahead prefetch of spilled pages (Sec. III: decode knows which
+ * blocks it reads next and fetches them a step early).  Decode runs layer by
+ * layer, so the step here is a layer: while layer l is decoded, the slices of
+ * layer l + 1 of the batch's spilled pages are gathered from the cold tier into
+ * HBM, and layer l + 1 then reads only HBM.
+ *
+ * kv_pool_set_staging gives the pool a device buffer for this (256-byte
+ * aligned; NULL or 0 bytes removes it).  It holds two halves (even and odd
+ * layers) of `slots` slots each, a slot being one layer of one page:
+ * num_kv_heads * 2 * 16 * head_dim elements.  *slots (nullable) gets the slot
+ * count.  Decode calls of the pool must not be running.
+ * Errors: KV_ERR_INVALID (alignment, metadata-only pool).
+ */
+int kv_pool_set_staging(kv_pool* pool, void* staging, size_t bytes, int32_t* slots);
+
+/*
+ * Batch page table for sessions sids (host int32 [n], ACTIVE) written to
+ * `table` (device int32 [n][max_pages_per_session]) on `stream`: hot pages by
+ * id; spilled pages, in batch and logical order, take staging slots
+ * (KV_PAGE_STAGED | slot) while slots last and are read from the cold tier
+ * directly (KV_PAGE_COLD | id) after that; unused entries are -1.  The
+ * resulting plan (cold page per slot) stays with the pool until the next call.
+ * *staged (nullable) gets the number of staged pages.  The table is valid until
+ * the pool's bookkeeping of these sessions changes.
+ * Errors: KV_ERR_INVALID, KV_ERR_STATE (a session not ACTIVE).
+ */
+int paged_decode_stage(kv_pool* pool, const int32_t* sids, int32_t n, int32_t* table,
+                       kv_stream_t stream, int32_t* staged);
+
+/*
+ * Gather layer `layer`'s slices of the planned pages into the staging half of
+ * that layer's parity, on `copy_stream` (typically not the decode stream, so
+ * the gather overlaps the previous layer's decode).  The library orders it
+ * after the plan's upload and after the decode that last read that half, and
+ * orders the decode of `layer` after it.  Decoding a layer with staged entries
+ * whose slices were not gathered for that layer reads no staged data: those
+ * rows come out NaN.
+ * Errors: KV_ERR_INVALID (no staging buffer, bad layer), KV_ERR_HIP.
+ */
+int paged_decode_prefetch(kv_pool* pool, int32_t layer, kv_stream_t copy_stream);
 
 /* Device workspace bytes paged_decode_attention needs for this batch. */
 size_t paged_decode_workspace_bytes(const kv_pool* pool, int32_t batch, int32_t num_q_heads);

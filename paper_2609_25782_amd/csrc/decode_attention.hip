@@ -88,14 +88,44 @@ __device__ __forceinline__ float wave_sum_4(float x) {
     return x;
 }
 
-template <int D, bool BF16>
-__device__ __forceinline__ void load_page(PageRegs<D, BF16>& r, const char* lh_base,
-                                          int64_t page_bytes, int pid, int num_pages, bool& bad,
+// Where a piece's pages live, already offset to its layer and KV head: hot
+// pages, and for tiered entries the cold pool and this layer's staging slots.
+struct PageSrc {
+    const char* hot = nullptr;
+    const char* cold = nullptr;
+    const char* stage = nullptr;
+    int64_t page_bytes = 0, slice_bytes = 0;
+    unsigned num_hot = 0, num_cold = 0, num_stage = 0;
+};
+
+// Page ids are wave-uniform, so the tier choice is scalar.  An id outside its
+// pool (or a negative entry) reads nothing: the buffer resource gets no records
+// and the row is marked bad (NaN).
+template <int D, bool BF16, bool TIERED>
+__device__ __forceinline__ void load_page(PageRegs<D, BF16>& r, const PageSrc& ps, int pid, bool& bad,
                                           unsigned koff, unsigned voff) {
     using S = Shape<D, BF16>;
-    const bool ok = static_cast<unsigned>(pid) < static_cast<unsigned>(num_pages);
+    const char* lh_base = ps.hot;
+    int64_t stride = ps.page_bytes;
+    unsigned n = ps.num_hot;
+    unsigned id = static_cast<unsigned>(pid);
+    if constexpr (TIERED) {
+        const unsigned tag = id >> 29;  // 0 hot, 1 staged, 2 cold, otherwise invalid
+        id &= static_cast<unsigned>(kPageIdMask);
+        if (tag == 1) {
+            lh_base = ps.stage;
+            stride = ps.slice_bytes;
+            n = ps.num_stage;
+        } else if (tag == 2) {
+            lh_base = ps.cold;
+            n = ps.num_cold;
+        } else if (tag != 0) {
+            n = 0;
+        }
+    }
+    const bool ok = id < n;
     bad |= !ok;
-    const char* base = lh_base + static_cast<int64_t>(ok ? pid : 0) * page_bytes;
+    const char* base = lh_base + static_cast<int64_t>(ok ? id : 0) * stride;
     const __amdgpu_buffer_rsrc_t rs =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), static_cast<short>(0),
                                           ok ? 2 * S::kTile : 0, kRsrcWord3);
@@ -332,7 +362,7 @@ __device__ __forceinline__ int load_ids(const int32_t* __restrict__ row, int fir
 // Process pages [p0, p1) of row b, KV head g, and write the partial to its slot.
 // R page buffers form a ring: while one page is computed, the next R - 1 are
 // in flight.
-template <int D, bool BF16, int R>
+template <int D, bool BF16, int R, bool TIERED>
 __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_len, int lane,
                           int64_t seg_first_unit, int64_t total_units) {
     using S = Shape<D, BF16>;
@@ -355,7 +385,18 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
     bool bad = false;
 
     const int32_t* row = a.page_table + static_cast<int64_t>(pc.b) * a.pt_stride;
-    const char* lh_base = a.hot + a.layer_offset + static_cast<int64_t>(pc.g) * 2 * S::kTile;
+    const int64_t head_off = static_cast<int64_t>(pc.g) * 2 * S::kTile;
+    PageSrc ps;
+    ps.hot = a.hot + a.layer_offset + head_off;
+    ps.page_bytes = a.page_bytes;
+    ps.num_hot = static_cast<unsigned>(a.num_pages);
+    if constexpr (TIERED) {
+        ps.cold = a.cold + a.layer_offset + head_off;
+        ps.stage = a.stage + head_off;
+        ps.slice_bytes = a.slice_bytes;
+        ps.num_cold = static_cast<unsigned>(a.num_cold_pages);
+        ps.num_stage = static_cast<unsigned>(a.num_stage_slots);
+    }
     const unsigned koff = 16u * lane;
     const unsigned voff = BF16 ? (32u * (lane & 15) + 8u * qg) : (64u * (lane & 15) + 16u * qg);
     // valid tokens of the row's last page (16 when full)
@@ -379,8 +420,7 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
 #pragma unroll
     for (int r = 0; r < R - 1; ++r)
         if (pc.p0 + r < pc.p1)
-            load_page<D, BF16>(buf[r], lh_base, a.page_bytes, pid_at(pc.p0 + r), a.num_pages, bad,
-                               koff, voff);
+            load_page<D, BF16, TIERED>(buf[r], ps, pid_at(pc.p0 + r), bad, koff, voff);
     for (int i = pc.p0; i < pc.p1; i += R) {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
@@ -388,8 +428,7 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
             if (ip < pc.p1) {
                 const int ahead = ip + R - 1;
                 if (ahead < pc.p1)
-                    load_page<D, BF16>(buf[(r + R - 1) % R], lh_base, a.page_bytes, pid_at(ahead),
-                                       a.num_pages, bad, koff, voff);
+                    load_page<D, BF16, TIERED>(buf[(r + R - 1) % R], ps, pid_at(ahead), bad, koff, voff);
                 compute_page<D, BF16>(st, buf[r], ip == nb - 1 ? tail_valid : kPageTokens,
                                       a.scale_log2, qg);
             }
@@ -424,7 +463,7 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
     }
 }
 
-template <int D, bool BF16, int R>
+template <int D, bool BF16, int R, bool TIERED>
 __global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs a) {
     extern __shared__ int32_t s_pref[];
     block_prefix_pages(a.seq_lens, a.batch, a.pt_stride, s_pref);
@@ -451,7 +490,7 @@ __global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs 
         const int seq_len = L < kPageTokens * nb ? L : kPageTokens * nb;
         const int64_t seg_first = static_cast<int64_t>(lds_uniform(s_pref + pc.b)) * a.num_kv_heads +
                                   static_cast<int64_t>(pc.g) * nb;
-        run_piece<D, BF16, R>(a, pc, nb, seq_len, lane, seg_first, total);
+        run_piece<D, BF16, R, TIERED>(a, pc, nb, seq_len, lane, seg_first, total);
         u += pc.p1 - pc.p0;
     }
 }
@@ -555,17 +594,18 @@ constexpr int ring_depth() {
 }
 
 template <int D, bool BF16>
-const void* split_kernel_ptr() {
-    return reinterpret_cast<const void*>(&decode_split_kernel<D, BF16, ring_depth<D, BF16>()>);
+const void* split_kernel_ptr(bool tiered) {
+    return tiered ? reinterpret_cast<const void*>(&decode_split_kernel<D, BF16, ring_depth<D, BF16>(), true>)
+                  : reinterpret_cast<const void*>(&decode_split_kernel<D, BF16, ring_depth<D, BF16>(), false>);
 }
 
-const void* pick_split(int head_dim, int dtype) {
+const void* pick_split(int head_dim, int dtype, bool tiered) {
     if (dtype == kDtypeBf16) {
-        if (head_dim == 128) return split_kernel_ptr<128, true>();
-        if (head_dim == 64) return split_kernel_ptr<64, true>();
+        if (head_dim == 128) return split_kernel_ptr<128, true>(tiered);
+        if (head_dim == 64) return split_kernel_ptr<64, true>(tiered);
     } else {
-        if (head_dim == 128) return split_kernel_ptr<128, false>();
-        if (head_dim == 64) return split_kernel_ptr<64, false>();
+        if (head_dim == 128) return split_kernel_ptr<128, false>(tiered);
+        if (head_dim == 64) return split_kernel_ptr<64, false>(tiered);
     }
     return nullptr;
 }
@@ -586,7 +626,7 @@ size_t prefix_lds_bytes(int batch) { return static_cast<size_t>(batch + 1) * siz
 }  // namespace
 
 hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s) {
-    const void* k = pick_split(head_dim, dtype);
+    const void* k = pick_split(head_dim, dtype, a.tiered != 0);
     if (!k || a.waves <= 0) return hipErrorInvalidValue;
     const int blocks = (a.waves + kBlockWaves - 1) / kBlockWaves;
     void* args[] = {const_cast<DecodeArgs*>(&a)};
@@ -604,7 +644,7 @@ hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, h
 }
 
 int decode_split_blocks_per_cu(int head_dim, int dtype, int batch) {
-    const void* k = pick_split(head_dim, dtype);
+    const void* k = pick_split(head_dim, dtype, false);
     if (!k) return 0;
     int n = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kBlockThreads, prefix_lds_bytes(batch)) !=

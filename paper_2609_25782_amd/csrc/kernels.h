@@ -5,7 +5,14 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "hotcold_kv.h"
+
 namespace hck {
+
+// Page-table entry tags (KV_PAGE_COLD, KV_PAGE_STAGED) and the id below them.
+constexpr int32_t kPageCold = KV_PAGE_COLD;
+constexpr int32_t kPageStaged = KV_PAGE_STAGED;
+constexpr int32_t kPageIdMask = KV_PAGE_STAGED - 1;
 
 enum { kDtypeBf16 = 0, kDtypeF32 = 1 };
 
@@ -33,6 +40,14 @@ struct DecodeArgs {
     void* out;                // [batch][num_q_heads][head_dim]
     int32_t* counters;        // [batch * num_kv_heads] arrival counters, zero between calls
     int32_t fused;            // 1: the last wave of each (b, g) merges its partials
+    // Tiered entries (honoured when `tiered` is set): KV_PAGE_COLD names a page
+    // of the cold pool, KV_PAGE_STAGED a slot of this layer's staging buffer.
+    int32_t tiered;
+    const char* cold;         // cold pool base (device-visible address)
+    int32_t num_cold_pages;
+    const char* stage;        // staging buffer of this layer: [slot][kv_head][K tile, V tile]
+    int32_t num_stage_slots;
+    int64_t slice_bytes;      // bytes of one staging slot
 };
 
 // Bytes of partial results for `slots` slots.
@@ -68,10 +83,19 @@ hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_b
                             const CopyEntry* entries, int32_t n, int32_t* page_table,
                             int32_t max_blocks, hipStream_t s);
 
+// The general form: `bytes` (a multiple of 4 KiB) from src_base + e.src *
+// src_stride to dst_base + e.dst * dst_stride.  With src_base at a layer's
+// offset inside cold pages and dst the staging buffer, it gathers one layer's
+// slices of spilled pages.
+hipError_t launch_slice_copy(const char* src_base, int64_t src_stride, char* dst_base,
+                             int64_t dst_stride, int64_t bytes, const CopyEntry* entries, int32_t n,
+                             int32_t* page_table, int32_t max_blocks, hipStream_t s);
+
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t s);
 
 struct SynthArgs {
     char* hot;
+    char* cold;          // for rows naming spilled pages (KV_PAGE_COLD)
     int64_t page_bytes;
     const int32_t* row;  // device page-table row of the session
     int32_t first_page;  // first logical page filled
@@ -85,6 +109,7 @@ hipError_t launch_fill_synthetic(const SynthArgs& a, hipStream_t s);
 
 struct WriteArgs {
     char* hot;
+    char* cold;          // for rows naming spilled pages (KV_PAGE_COLD)
     int64_t page_bytes;
     const int32_t* row;  // device page-table row of the session
     int32_t num_kv_heads, head_dim, dtype, layer;

@@ -87,6 +87,7 @@ struct Session {
     int64_t stamp = 0;          // pause time (LRU order) while PAUSED
     std::vector<int32_t> hot;   // hot page per logical page, -1 = not resident
     std::vector<int32_t> cold;  // cold page per logical page, -1 = no valid copy
+    std::vector<uint8_t> spilled;  // 1: the row entry names the cold page (spill)
 };
 
 // One resident page of a paused session chosen for eviction.
@@ -99,6 +100,7 @@ struct Alloc {
     std::vector<Victim> victims;       // LRU pages evicted first
     std::vector<int32_t> victim_cold;  // cold page for each victim without a valid copy
     std::vector<int32_t> pages;        // hot pages handed out, ascending
+    std::vector<int32_t> spill_cold;   // fresh cold pages for the pages that spill
 };
 
 constexpr int kStagingSlots = 4;
@@ -178,6 +180,20 @@ struct kv_pool {
     int cus = 0;
     int32_t waves_override = 0;
     int32_t copy_blocks = 0;  // cap of the page-copy grid (0: default)
+    bool spill = false;       // place pages in the cold tier instead of failing
+    // staging of spilled pages for decode (one layer's slices, two halves)
+    char* stage = nullptr;
+    int32_t stage_slots = 0;  // slots per half
+    int64_t slice_bytes = 0;  // one layer of one page
+    std::vector<int32_t> plan;            // cold page per staging slot
+    hck::CopyEntry* plan_dev = nullptr;   // the plan as copy entries (device)
+    hck::CopyEntry* plan_host = nullptr;  // pinned upload buffer of the plan
+    int32_t plan_cap = 0;
+    hipEvent_t plan_ready = nullptr, prefetch_done = nullptr;
+    bool plan_ready_pending = false, prefetch_pending = false;
+    hipEvent_t half_ready[2] = {nullptr, nullptr}, half_free[2] = {nullptr, nullptr};
+    bool half_ready_pending[2] = {false, false}, half_free_pending[2] = {false, false};
+    int32_t half_layer[2] = {-1, -1};     // layer gathered into each half for the current plan
     StagingSlot ring[kStagingSlots];
     int ring_next = 0;
     hipEvent_t free_event = nullptr;
@@ -211,7 +227,31 @@ struct kv_pool {
                 (void)hipEventDestroy(r.stop);
             }
         for (auto e : spare_events) (void)hipEventDestroy(e);
+        free_staging_state();
+        for (hipEvent_t e : {plan_ready, prefetch_done, half_ready[0], half_ready[1], half_free[0],
+                             half_free[1]})
+            if (e) (void)hipEventDestroy(e);
     }
+
+    // Wait for every use of the plan buffers, then free them.
+    void free_staging_state() {
+        if (prefetch_pending) (void)hipEventSynchronize(prefetch_done);
+        if (plan_ready_pending) (void)hipEventSynchronize(plan_ready);
+        for (int b = 0; b < 2; ++b)
+            if (half_free_pending[b]) (void)hipEventSynchronize(half_free[b]);
+        prefetch_pending = plan_ready_pending = false;
+        half_free_pending[0] = half_free_pending[1] = false;
+        half_ready_pending[0] = half_ready_pending[1] = false;
+        if (plan_dev) (void)hipFree(plan_dev);
+        if (plan_host) (void)hipHostFree(plan_host);
+        plan_dev = nullptr;
+        plan_host = nullptr;
+        plan_cap = 0;
+        plan.clear();
+        half_layer[0] = half_layer[1] = -1;
+    }
+
+    bool tiered() const { return spill || stage_slots > 0; }
 
     hipStream_t strm(kv_stream_t s) const { return static_cast<hipStream_t>(s); }
 
@@ -341,6 +381,19 @@ struct kv_pool {
         return false;
     }
 
+    static bool has_row_entries(const Session& s) {
+        for (size_t i = 0; i < s.hot.size(); ++i)
+            if (s.hot[i] >= 0 || s.spilled[i]) return true;
+        return false;
+    }
+
+    // Page-table entries of new pages: hot ids, then the spilled pages' cold ids.
+    static std::vector<int32_t> new_entries(const Alloc& a) {
+        std::vector<int32_t> v(a.pages);
+        for (int32_t c : a.spill_cold) v.push_back(c | KV_PAGE_COLD);
+        return v;
+    }
+
     // Least-recently-used resident pages of paused sessions: oldest pause first,
     // lowest logical page first, skipping `exclude`; at most `need` of them.
     void plan_lru(int64_t need, const std::vector<int32_t>& exclude, std::vector<Victim>& out) const {
@@ -365,25 +418,48 @@ struct kv_pool {
         return KV_OK;
     }
 
-    // Plan k hot pages, evicting LRU pages of paused sessions (never those of
-    // `exclude`) when too few are free.  Changes nothing.
-    int plan_alloc(int64_t k, const std::vector<int32_t>& exclude, Alloc& a) {
+    // Plan k pages, evicting LRU pages of paused sessions (never those of
+    // `exclude`) when too few hot pages are free.  Without spill all k are hot
+    // or the call fails; with spill (the pool's, or `allow_spill`) the pages
+    // that find no hot page spill: fresh cold pages if `fresh_spill`, else they
+    // stay where they are.  Changes nothing.
+    int plan_alloc(int64_t k, const std::vector<int32_t>& exclude, Alloc& a, bool fresh_spill = true,
+                   bool allow_spill = false) {
         a = Alloc();
         const int64_t have = hot_free.free_count();
-        if (k > have) {
-            plan_lru(k - have, exclude, a.victims);
-            if (static_cast<int64_t>(a.victims.size()) < k - have)
-                return fail(KV_ERR_NO_HOT_PAGES, "need %lld hot pages: %lld free, %zu evictable",
-                            static_cast<long long>(k), static_cast<long long>(have), a.victims.size());
-            int rc = plan_victim_cold(a);
-            if (rc) return rc;
-            PageSet after = hot_free;
-            for (const Victim& v : a.victims) after.give(sessions[v.sid].hot[v.page]);
-            after.lowest(static_cast<int32_t>(k), a.pages);
-        } else {
+        if (k <= have) {
             hot_free.lowest(static_cast<int32_t>(k), a.pages);
+            return KV_OK;
         }
+        plan_lru(k - have, exclude, a.victims);
+        const int64_t short_by = k - have - static_cast<int64_t>(a.victims.size());
+        if (short_by > 0 && !(spill || allow_spill))
+            return fail(KV_ERR_NO_HOT_PAGES, "need %lld hot pages: %lld free, %zu evictable",
+                        static_cast<long long>(k), static_cast<long long>(have), a.victims.size());
+        const int64_t n_hot = k - std::max<int64_t>(short_by, 0);
+        const int64_t n_spill = fresh_spill ? std::max<int64_t>(short_by, 0) : 0;
+        int64_t dirty = 0;
+        for (const Victim& v : a.victims) dirty += sessions[v.sid].cold[v.page] < 0;
+        if (dirty + n_spill > cold_free.free_count())
+            return fail(KV_ERR_NO_COLD_PAGES, "need %lld cold pages (%lld evicted, %lld spilled), %d free",
+                        static_cast<long long>(dirty + n_spill), static_cast<long long>(dirty),
+                        static_cast<long long>(n_spill), cold_free.free_count());
+        std::vector<int32_t> both;
+        cold_free.lowest(static_cast<int32_t>(dirty + n_spill), both);
+        a.victim_cold.assign(both.begin(), both.begin() + dirty);
+        a.spill_cold.assign(both.begin() + dirty, both.end());
+        PageSet after = hot_free;
+        for (const Victim& v : a.victims) after.give(sessions[v.sid].hot[v.page]);
+        after.lowest(static_cast<int32_t>(n_hot), a.pages);
         return KV_OK;
+    }
+
+    void commit_spill(const Alloc& a) {
+        for (int32_t c : a.spill_cold) {
+            cold_free.take(c);
+            cold_ref[c] = 1;
+        }
+        st.spilled_pages += static_cast<int64_t>(a.spill_cold.size());
     }
 
     // Enqueue the victims' cold writes and row clears (one launch), before any
@@ -581,22 +657,29 @@ int kv_session_create(kv_pool* pool, int32_t seq_len, const int32_t* hot_pages, 
         int rc = pool->plan_alloc(n, {}, a);
         if (rc) return rc;
     }
+    const std::vector<int32_t> entries = kv_pool::new_entries(a);
     if (!pool->meta && n > 0) {
         DeviceGuard g(pool->d.device);
         hipStream_t s = pool->strm(stream);
         int rc = pool->order_after_frees(s);
         if (!rc) rc = pool->submit_victims(a, s);
-        if (!rc) rc = pool->submit_row_at(sid, 0, a.pages.data(), n, s);
+        if (!rc) rc = pool->submit_row_at(sid, 0, entries.data(), n, s);
         if (rc) return rc;
     }
     pool->commit_victims(a);
+    pool->commit_spill(a);
     for (int32_t p : a.pages) pool->hot_free.take(p);
+    const size_t nh = a.pages.size(), ns = a.spill_cold.size();
     Session& ss = pool->sessions[sid];
     ss = Session();
     ss.state = KV_SESSION_ACTIVE;
     ss.seq_len = seq_len;
     ss.hot = a.pages;
-    ss.cold.assign(n, -1);
+    ss.hot.resize(nh + ns, -1);
+    ss.cold.assign(nh, -1);
+    ss.cold.insert(ss.cold.end(), a.spill_cold.begin(), a.spill_cold.end());
+    ss.spilled.assign(nh, 0);
+    ss.spilled.resize(nh + ns, 1);
     *sid_out = sid;
     return KV_OK;
 }
@@ -613,20 +696,26 @@ int kv_session_extend(kv_pool* pool, int32_t sid, int32_t new_seq_len, kv_stream
         return fail(KV_ERR_INVALID, "%d pages exceed the row stride %d", n_new,
                     pool->d.max_pages_per_session);
     Alloc a;
-    int rc = pool->plan_alloc(n_new - n_old, {}, a);
+    int rc = pool->plan_alloc(std::max(n_new - n_old, 0), {}, a);
     if (rc) return rc;
+    const std::vector<int32_t> entries = kv_pool::new_entries(a);
     if (!pool->meta && n_new > n_old) {
         DeviceGuard g(pool->d.device);
         hipStream_t st = pool->strm(stream);
         rc = pool->order_after_frees(st);
         if (!rc) rc = pool->submit_victims(a, st);
-        if (!rc) rc = pool->submit_row_at(sid, n_old, a.pages.data(), n_new - n_old, st);
+        if (!rc) rc = pool->submit_row_at(sid, n_old, entries.data(), n_new - n_old, st);
         if (rc) return rc;
     }
     pool->commit_victims(a);
+    pool->commit_spill(a);
     for (int32_t p : a.pages) pool->hot_free.take(p);
     s->hot.insert(s->hot.end(), a.pages.begin(), a.pages.end());
-    s->cold.resize(n_new, -1);
+    s->hot.resize(n_new, -1);
+    s->cold.resize(n_old + a.pages.size(), -1);
+    s->cold.insert(s->cold.end(), a.spill_cold.begin(), a.spill_cold.end());
+    s->spilled.resize(n_old + a.pages.size(), 0);
+    s->spilled.resize(n_new, 1);
     s->seq_len = new_seq_len;
     return KV_OK;
 }
@@ -683,6 +772,7 @@ int kv_session_import_cold(kv_pool* pool, int32_t seq_len, const int32_t* cold_p
     ss.stamp = ++pool->clock;
     ss.hot.assign(n, -1);
     ss.cold = pages;
+    ss.spilled.assign(n, 0);
     *sid_out = sid;
     return KV_OK;
 }
@@ -692,8 +782,7 @@ int kv_session_destroy(kv_pool* pool, int32_t sid, kv_stream_t stream) {
     Session* s = pool->session(sid);
     if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
     if (s->state == KV_SESSION_FREE) return fail(KV_ERR_STATE, "session %d is not in use", sid);
-    const bool resident = kv_pool::has_resident(*s);
-    if (!pool->meta && resident) {
+    if (!pool->meta && kv_pool::has_row_entries(*s)) {
         DeviceGuard g(pool->d.device);
         hipStream_t st = pool->strm(stream);
         int rc = pool->clear_row(sid, static_cast<int32_t>(s->hot.size()), st);
@@ -733,11 +822,16 @@ int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin
     if (tok_begin < 0 || n_tok < 0 || static_cast<int64_t>(tok_begin) + n_tok > s->seq_len)
         return fail(KV_ERR_INVALID, "token range outside the session");
     if (n_tok == 0) return KV_OK;
+    const int32_t first = tok_begin / KV_PAGE_TOKENS, last = (tok_begin + n_tok - 1) / KV_PAGE_TOKENS;
+    for (int32_t i = first; i <= last; ++i)
+        if (s->hot[i] < 0 && pool->cold_ref[s->cold[i]] > 1)
+            return fail(KV_ERR_STATE, "page %d is spilled to a cold page shared with another session", i);
     if (!pool->meta) {
         if (!k || !v) return fail(KV_ERR_INVALID, "NULL k or v");
         DeviceGuard g(pool->d.device);
         hck::WriteArgs a;
         a.hot = pool->hot;
+        a.cold = pool->cold;
         a.page_bytes = pool->page_bytes;
         a.row = pool->pt + static_cast<int64_t>(sid) * pool->d.max_pages_per_session;
         a.num_kv_heads = pool->d.num_kv_heads;
@@ -751,8 +845,8 @@ int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin
         hipError_t e = hck::launch_write_tokens(a, pool->strm(stream));
         if (e != hipSuccess) return hip_fail(e, "write_tokens launch");
     }
-    for (int32_t i = tok_begin / KV_PAGE_TOKENS; i <= (tok_begin + n_tok - 1) / KV_PAGE_TOKENS; ++i) {
-        if (s->cold[i] >= 0) {
+    for (int32_t i = first; i <= last; ++i) {
+        if (s->hot[i] >= 0 && s->cold[i] >= 0) {   // a spilled page is written in place
             pool->release_cold(s->cold[i]);
             s->cold[i] = -1;
         }
@@ -774,9 +868,13 @@ int kv_fill_synthetic_pages(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_
         return fail(KV_ERR_INVALID, "pages [%d, %d) outside the session's %lld", first_page,
                     first_page + num_pages, static_cast<long long>(have));
     if (num_pages == 0) return KV_OK;
+    for (int32_t i = first_page; i < first_page + num_pages; ++i)
+        if (s->hot[i] < 0 && pool->cold_ref[s->cold[i]] > 1)
+            return fail(KV_ERR_STATE, "page %d is spilled to a cold page shared with another session", i);
     DeviceGuard g(pool->d.device);
     hck::SynthArgs a;
     a.hot = pool->hot;
+    a.cold = pool->cold;
     a.page_bytes = pool->page_bytes;
     a.row = pool->pt + static_cast<int64_t>(sid) * pool->d.max_pages_per_session;
     a.first_page = first_page;
@@ -791,7 +889,7 @@ int kv_fill_synthetic_pages(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_
     hipError_t e = hck::launch_fill_synthetic(a, pool->strm(stream));
     if (e != hipSuccess) return hip_fail(e, "fill_synthetic launch");
     for (int32_t i = first_page; i < first_page + num_pages; ++i) {
-        if (s->cold[i] >= 0) {
+        if (s->hot[i] >= 0 && s->cold[i] >= 0) {   // a spilled page is written in place
             pool->release_cold(s->cold[i]);
             s->cold[i] = -1;
         }
@@ -806,6 +904,55 @@ int kv_fill_synthetic(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed
     if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
     return kv_fill_synthetic_pages(pool, sid, gen_sid, seed, value_mult, 0,
                                    static_cast<int32_t>(s->hot.size()), stream);
+}
+
+int kv_pool_set_spill(kv_pool* pool, int32_t enable) {
+    if (!pool || (enable != 0 && enable != 1)) return fail(KV_ERR_INVALID, "bad arguments");
+    pool->spill = enable != 0;
+    return KV_OK;
+}
+
+int kv_promote_pages(kv_pool* pool, int32_t n, kv_stream_t stream, int32_t* promoted) {
+    if (!pool || n < 0) return fail(KV_ERR_INVALID, "bad arguments");
+    // spilled pages of active sessions: session id order, logical page order
+    std::vector<Victim> want;
+    for (int32_t sid = 0; sid < pool->d.max_sessions && static_cast<int32_t>(want.size()) < n; ++sid) {
+        const Session& s = pool->sessions[sid];
+        if (s.state != KV_SESSION_ACTIVE) continue;
+        for (size_t i = 0; i < s.hot.size() && static_cast<int32_t>(want.size()) < n; ++i)
+            if (s.hot[i] < 0) want.push_back(Victim{sid, static_cast<int32_t>(i)});
+    }
+    Alloc a;
+    int rc = pool->plan_alloc(static_cast<int64_t>(want.size()), {}, a, /*fresh_spill=*/false,
+                              /*allow_spill=*/true);
+    if (rc) return rc;
+    if (!pool->meta && !a.pages.empty()) {
+        DeviceGuard g(pool->d.device);
+        hipStream_t st = pool->strm(stream);
+        std::vector<hck::CopyEntry> entries;
+        for (size_t k = 0; k < a.pages.size(); ++k) {
+            const Victim& w = want[k];
+            entries.push_back(hck::CopyEntry{pool->sessions[w.sid].cold[w.page], a.pages[k],
+                                             w.sid * pool->d.max_pages_per_session + w.page, a.pages[k]});
+        }
+        rc = pool->order_after_frees(st);
+        if (!rc) rc = pool->submit_victims(a, st);
+        if (!rc) rc = pool->submit_copies(pool->cold, pool->hot, entries, st, KV_KERNEL_PAGE_COPY);
+        if (rc) return rc;
+    }
+    pool->commit_victims(a);
+    for (size_t k = 0; k < a.pages.size(); ++k) {
+        Session& s = pool->sessions[want[k].sid];
+        s.hot[want[k].page] = a.pages[k];
+        s.spilled[want[k].page] = 0;
+        pool->hot_free.take(a.pages[k]);
+    }
+    const int64_t m = static_cast<int64_t>(a.pages.size());
+    pool->st.promoted_pages += m;
+    pool->st.pages_to_hot += m;
+    pool->st.bytes_to_hot += m * pool->page_bytes;
+    if (promoted) *promoted = static_cast<int32_t>(m);
+    return KV_OK;
 }
 
 int kv_evict_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t stream) {
@@ -861,8 +1008,9 @@ int kv_evict_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t
                 s.cold[i] = dst[k++];
                 ++written;
             }
-            pool->hot_free.give(s.hot[i]);
+            if (s.hot[i] >= 0) pool->hot_free.give(s.hot[i]);
             s.hot[i] = -1;
+            s.spilled[i] = 0;
         }
         s.state = KV_SESSION_PAUSED;
         s.stamp = ++pool->clock;
@@ -894,9 +1042,10 @@ int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_
         if (s->state != KV_SESSION_PAUSED) return fail(KV_ERR_STATE, "session %d is not paused", sid);
         for (int32_t p : s->hot) need += p < 0;
     }
-    // the sessions being resumed keep their resident pages: never evict those
+    // the sessions being resumed keep their resident pages: never evict those;
+    // with spill, pages that find no hot page stay in the cold tier
     Alloc a;
-    int rc = pool->plan_alloc(need, ids, a);
+    int rc = pool->plan_alloc(need, ids, a, /*fresh_spill=*/false);
     if (rc) return rc;
     if (!pool->meta) {
         DeviceGuard g(pool->d.device);
@@ -907,10 +1056,13 @@ int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_
             const Session& s = pool->sessions[sid];
             const int32_t row = sid * pool->d.max_pages_per_session;
             for (size_t i = 0; i < s.hot.size(); ++i) {
-                if (s.hot[i] < 0) {
+                if (s.hot[i] < 0 && k < a.pages.size()) {
                     entries.push_back(hck::CopyEntry{s.cold[i], a.pages[k], row + static_cast<int32_t>(i),
                                                      a.pages[k]});
                     ++k;
+                } else if (s.hot[i] < 0) {
+                    entries.push_back(hck::CopyEntry{-1, -1, row + static_cast<int32_t>(i),
+                                                     s.cold[i] | KV_PAGE_COLD});
                 } else {
                     entries.push_back(hck::CopyEntry{-1, -1, row + static_cast<int32_t>(i), s.hot[i]});
                 }
@@ -925,19 +1077,25 @@ int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_
     size_t k = 0;
     for (int32_t sid : ids) {
         Session& s = pool->sessions[sid];
-        int64_t fetched = 0;
+        int64_t fetched = 0, resident = 0;
         for (size_t i = 0; i < s.hot.size(); ++i) {
-            if (s.hot[i] < 0) {
+            if (s.hot[i] >= 0) {
+                ++resident;
+            } else if (k < a.pages.size()) {
                 s.hot[i] = a.pages[k++];
+                s.spilled[i] = 0;
                 pool->hot_free.take(s.hot[i]);
                 ++fetched;
+            } else {
+                s.spilled[i] = 1;
+                pool->st.spilled_pages += 1;
             }
         }
         pool->lru.erase(s.stamp);
         s.state = KV_SESSION_ACTIVE;
         pool->st.pages_to_hot += fetched;
         pool->st.bytes_to_hot += fetched * pool->page_bytes;
-        pool->st.resume_pages_resident += static_cast<int64_t>(s.hot.size()) - fetched;
+        pool->st.resume_pages_resident += resident;
         pool->st.resume_pages_total += static_cast<int64_t>(s.hot.size());
         pool->st.resumes += 1;
     }
@@ -1031,11 +1189,27 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
     a.out = out;
     a.counters = pool->counters;
     a.fused = pool->combine_mode == KV_COMBINE_FUSED ? 1 : 0;
+    a.tiered = pool->tiered() ? 1 : 0;
+    a.cold = pool->cold;
+    a.num_cold_pages = pool->cold ? pool->d.num_cold_pages : 0;
+    a.slice_bytes = pool->slice_bytes;
+    a.stage = nullptr;
+    a.num_stage_slots = 0;
+    const int half = layer & 1;
+    const bool staged = pool->stage_slots > 0 && !pool->plan.empty() && pool->half_layer[half] == layer;
+    if (staged) {
+        a.stage = pool->stage + static_cast<int64_t>(half) * pool->stage_slots * pool->slice_bytes;
+        a.num_stage_slots = static_cast<int32_t>(pool->plan.size());
+    }
     hipStream_t st = pool->strm(stream);
     // decode calls of one pool share its counters: order them across streams
     if (pool->decode_pending) {
         hipError_t w = hipStreamWaitEvent(st, pool->decode_event, 0);
         if (w != hipSuccess) return hip_fail(w, "hipStreamWaitEvent(decode)");
+    }
+    if (staged && pool->half_ready_pending[half]) {
+        hipError_t w = hipStreamWaitEvent(st, pool->half_ready[half], 0);
+        if (w != hipSuccess) return hip_fail(w, "hipStreamWaitEvent(staging)");
     }
     hipEvent_t p = pool->prof_begin(st);
     hipError_t e = hck::launch_decode_split(a, pool->d.head_dim, pool->d.dtype, st);
@@ -1050,6 +1224,141 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
     e = hipEventRecord(pool->decode_event, st);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord(decode)");
     pool->decode_pending = true;
+    if (staged) {
+        e = hipEventRecord(pool->half_free[half], st);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
+        pool->half_free_pending[half] = true;
+    }
+    return KV_OK;
+}
+
+int kv_pool_set_staging(kv_pool* pool, void* staging, size_t bytes, int32_t* slots) {
+    if (!pool || pool->meta) return fail(KV_ERR_INVALID, "no device pool");
+    if (reinterpret_cast<uintptr_t>(staging) & 255) return fail(KV_ERR_INVALID, "staging must be 256-byte aligned");
+    DeviceGuard g(pool->d.device);
+    if (pool->decode_pending) (void)hipEventSynchronize(pool->decode_event);
+    pool->free_staging_state();
+    const int64_t slice = static_cast<int64_t>(pool->d.num_kv_heads) * 2 * KV_PAGE_TOKENS *
+                          pool->d.head_dim * static_cast<int64_t>(elt_size(pool->d.dtype));
+    const int64_t n = staging ? static_cast<int64_t>(bytes) / (2 * slice) : 0;
+    pool->slice_bytes = slice;
+    pool->stage = n > 0 ? static_cast<char*>(staging) : nullptr;
+    pool->stage_slots = static_cast<int32_t>(std::min<int64_t>(n, int64_t(1) << 28));
+    if (pool->stage_slots > 0) {
+        for (hipEvent_t* e : {&pool->plan_ready, &pool->prefetch_done, &pool->half_ready[0],
+                              &pool->half_ready[1], &pool->half_free[0], &pool->half_free[1]})
+            if (!*e && hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess)
+                return fail(KV_ERR_OOM, "event creation failed");
+        const size_t eb = static_cast<size_t>(pool->stage_slots) * sizeof(hck::CopyEntry);
+        if (hipMalloc(&pool->plan_dev, eb) != hipSuccess ||
+            hipHostMalloc(reinterpret_cast<void**>(&pool->plan_host), eb, hipHostMallocDefault) != hipSuccess) {
+            pool->stage = nullptr;
+            pool->stage_slots = 0;
+            return fail(KV_ERR_OOM, "staging plan allocation failed");
+        }
+        pool->plan_cap = pool->stage_slots;
+    }
+    if (slots) *slots = pool->stage_slots;
+    return KV_OK;
+}
+
+int paged_decode_stage(kv_pool* pool, const int32_t* sids, int32_t n, int32_t* table,
+                       kv_stream_t stream, int32_t* staged) {
+    if (!pool || pool->meta) return fail(KV_ERR_INVALID, "no device pool");
+    if (n < 0 || n > kMaxDecodeBatch || (n > 0 && (!sids || !table))) return fail(KV_ERR_INVALID, "bad arguments");
+    for (int32_t i = 0; i < n; ++i) {
+        const Session* s = pool->session(sids[i]);
+        if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sids[i]);
+        if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sids[i]);
+    }
+    DeviceGuard g(pool->d.device);
+    hipStream_t st = pool->strm(stream);
+    // the previous plan's buffers must no longer be in use
+    if (pool->prefetch_pending) {
+        hipError_t e = hipEventSynchronize(pool->prefetch_done);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(prefetch)");
+        pool->prefetch_pending = false;
+    }
+    if (pool->plan_ready_pending) {
+        hipError_t e = hipEventSynchronize(pool->plan_ready);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(plan)");
+        pool->plan_ready_pending = false;
+    }
+    const int32_t stride = pool->d.max_pages_per_session;
+    std::vector<int32_t> rows(static_cast<size_t>(n) * stride, -1);
+    std::vector<int32_t> plan;
+    for (int32_t b = 0; b < n; ++b) {
+        const Session& s = pool->sessions[sids[b]];
+        int32_t* r = rows.data() + static_cast<size_t>(b) * stride;
+        for (size_t i = 0; i < s.hot.size(); ++i) {
+            if (s.hot[i] >= 0) {
+                r[i] = s.hot[i];
+            } else if (static_cast<int32_t>(plan.size()) < pool->stage_slots) {
+                r[i] = static_cast<int32_t>(plan.size()) | KV_PAGE_STAGED;
+                plan.push_back(s.cold[i]);
+            } else {
+                r[i] = s.cold[i] | KV_PAGE_COLD;
+            }
+        }
+    }
+    // the batch table, through the staging ring in pieces of whole rows
+    const size_t row_bytes = static_cast<size_t>(stride) * sizeof(int32_t);
+    const int32_t rows_per_slot = static_cast<int32_t>(kStagingBytes / row_bytes);
+    for (int32_t b0 = 0; b0 < n; b0 += rows_per_slot) {
+        const int32_t m = std::min(rows_per_slot, n - b0);
+        StagingSlot* slot;
+        int rc = pool->acquire_slot(&slot);
+        if (rc) return rc;
+        std::memcpy(slot->host, rows.data() + static_cast<size_t>(b0) * stride, m * row_bytes);
+        hipError_t e = hipMemcpyAsync(table + static_cast<size_t>(b0) * stride, slot->host, m * row_bytes,
+                                      hipMemcpyHostToDevice, st);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(batch table)");
+        e = hipEventRecord(slot->done, st);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
+        slot->pending = true;
+    }
+    if (!plan.empty()) {
+        for (size_t k = 0; k < plan.size(); ++k)
+            pool->plan_host[k] = hck::CopyEntry{plan[k], static_cast<int32_t>(k), -1, 0};
+        hipError_t e = hipMemcpyAsync(pool->plan_dev, pool->plan_host, plan.size() * sizeof(hck::CopyEntry),
+                                      hipMemcpyHostToDevice, st);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(staging plan)");
+        e = hipEventRecord(pool->plan_ready, st);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord(plan)");
+        pool->plan_ready_pending = true;
+    }
+    pool->plan = std::move(plan);
+    pool->half_layer[0] = pool->half_layer[1] = -1;
+    if (staged) *staged = static_cast<int32_t>(pool->plan.size());
+    return KV_OK;
+}
+
+int paged_decode_prefetch(kv_pool* pool, int32_t layer, kv_stream_t copy_stream) {
+    if (!pool || pool->meta || pool->stage_slots <= 0) return fail(KV_ERR_INVALID, "no staging buffer");
+    if (layer < 0 || layer >= pool->d.num_layers) return fail(KV_ERR_INVALID, "bad layer %d", layer);
+    const int half = layer & 1;
+    pool->half_layer[half] = -1;
+    if (pool->plan.empty()) return KV_OK;
+    DeviceGuard g(pool->d.device);
+    hipStream_t cs = pool->strm(copy_stream);
+    hipError_t e = hipSuccess;
+    if (pool->plan_ready_pending) e = hipStreamWaitEvent(cs, pool->plan_ready, 0);
+    if (e == hipSuccess && pool->half_free_pending[half]) e = hipStreamWaitEvent(cs, pool->half_free[half], 0);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(prefetch)");
+    const int64_t layer_offset = static_cast<int64_t>(layer) * pool->slice_bytes;
+    char* dst = pool->stage + static_cast<int64_t>(half) * pool->stage_slots * pool->slice_bytes;
+    hipEvent_t p = pool->prof_begin(cs);
+    e = hck::launch_slice_copy(pool->cold + layer_offset, pool->page_bytes, dst, pool->slice_bytes,
+                               pool->slice_bytes, pool->plan_dev, static_cast<int32_t>(pool->plan.size()),
+                               nullptr, pool->copy_blocks, cs);
+    pool->prof_end(KV_KERNEL_PREFETCH_COPY, p, cs);
+    if (e != hipSuccess) return hip_fail(e, "prefetch launch");
+    e = hipEventRecord(pool->half_ready[half], cs);
+    if (e == hipSuccess) e = hipEventRecord(pool->prefetch_done, cs);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord(prefetch)");
+    pool->half_ready_pending[half] = true;
+    pool->prefetch_pending = true;
+    pool->half_layer[half] = layer;
     return KV_OK;
 }
 

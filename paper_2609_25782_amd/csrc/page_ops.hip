@@ -26,6 +26,13 @@ namespace {
 #define HCK_COPY_MAX_BLOCKS 16384
 #endif
 
+// Address of the page a session row names: a hot page, or a spilled page of the
+// cold pool (KV_PAGE_COLD).  The host writes rows only with such entries.
+__device__ __forceinline__ char* page_address(char* hot, char* cold, int32_t pid, int64_t page_bytes) {
+    return (pid & kPageCold) ? cold + static_cast<int64_t>(pid & kPageIdMask) * page_bytes
+                             : hot + static_cast<int64_t>(pid) * page_bytes;
+}
+
 // A block copies chunks of `U` x 4 KiB: every thread moves U 16-byte words, all
 // loads issued before the first store.  The host picks U so that a chunk
 // divides the page, so the body has no bounds checks (pages are always a
@@ -35,8 +42,8 @@ namespace {
 // millions of short ones.
 template <int U>
 __global__ __launch_bounds__(kBlockThreads) void page_copy_kernel(
-    const char* __restrict__ src_base, char* __restrict__ dst_base, int64_t page_bytes,
-    const CopyEntry* __restrict__ entries, int32_t n, int chunks_per_page,
+    const char* __restrict__ src_base, int64_t src_stride, char* __restrict__ dst_base,
+    int64_t dst_stride, const CopyEntry* __restrict__ entries, int32_t n, int chunks_per_page,
     int32_t* __restrict__ page_table) {
     const int64_t total = static_cast<int64_t>(n) * chunks_per_page;
     for (int64_t flat = blockIdx.x; flat < total; flat += gridDim.x) {
@@ -47,8 +54,8 @@ __global__ __launch_bounds__(kBlockThreads) void page_copy_kernel(
         if (e.src < 0) continue;
         const int64_t base = static_cast<int64_t>(chunk) * U * kBlockThreads * 16;
         const u32x4* s =
-            reinterpret_cast<const u32x4*>(src_base + e.src * page_bytes + base) + threadIdx.x;
-        u32x4* d = reinterpret_cast<u32x4*>(dst_base + e.dst * page_bytes + base) + threadIdx.x;
+            reinterpret_cast<const u32x4*>(src_base + e.src * src_stride + base) + threadIdx.x;
+        u32x4* d = reinterpret_cast<u32x4*>(dst_base + e.dst * dst_stride + base) + threadIdx.x;
         u32x4 buf[U];
 #pragma unroll
         for (int i = 0; i < U; ++i)
@@ -151,7 +158,7 @@ __global__ __launch_bounds__(kBlockThreads) void fill_synthetic_kernel(SynthArgs
                                           a.value_mult));
             }
         }
-        *reinterpret_cast<u32x4*>(a.hot + static_cast<int64_t>(pid) * a.page_bytes + byte) =
+        *reinterpret_cast<u32x4*>(page_address(a.hot, a.cold, pid, a.page_bytes) + byte) =
             u32x4{words[0], words[1], words[2], words[3]};
     }
 }
@@ -171,7 +178,7 @@ __global__ __launch_bounds__(kBlockThreads) void write_tokens_kernel(WriteArgs a
         const int t = a.tok_begin + tok;
         const int32_t pid = a.row[t / kPageTokens];
         const int slot = t % kPageTokens;
-        char* lh = a.hot + static_cast<int64_t>(pid) * a.page_bytes +
+        char* lh = page_address(a.hot, a.cold, pid, a.page_bytes) +
                    (static_cast<int64_t>(a.layer) * a.num_kv_heads + head) * 2 * tile;
         const int64_t src_elem = (static_cast<int64_t>(tok) * a.num_kv_heads + head) * a.head_dim + cd * x;
         // K: the group's x dims are contiguous in the tile
@@ -243,10 +250,17 @@ int grid_for(int64_t work, int cap) {
 hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_bytes,
                             const CopyEntry* entries, int32_t n, int32_t* page_table,
                             int32_t max_blocks, hipStream_t s) {
+    return launch_slice_copy(src_base, page_bytes, dst_base, page_bytes, page_bytes, entries, n,
+                             page_table, max_blocks, s);
+}
+
+hipError_t launch_slice_copy(const char* src_base, int64_t src_stride, char* dst_base,
+                             int64_t dst_stride, int64_t bytes, const CopyEntry* entries, int32_t n,
+                             int32_t* page_table, int32_t max_blocks, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     constexpr int64_t kRow = static_cast<int64_t>(kBlockThreads) * 16;  // 4 KiB
-    if (page_bytes % kRow) return hipErrorInvalidValue;
-    const int64_t rows = page_bytes / kRow;
+    if (bytes % kRow || bytes <= 0) return hipErrorInvalidValue;
+    const int64_t rows = bytes / kRow;
     const int u = rows % 8 == 0 ? 8 : rows % 4 == 0 ? 4 : rows % 2 == 0 ? 2 : 1;
     const int64_t chunks = rows / u;
     const int64_t work = chunks * n;
@@ -255,10 +269,10 @@ hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_b
     const dim3 grid(static_cast<unsigned>(blocks)), block(kBlockThreads);
     const int cpp = static_cast<int>(chunks);
     switch (u) {
-        case 8: hipLaunchKernelGGL(page_copy_kernel<8>, grid, block, 0, s, src_base, dst_base, page_bytes, entries, n, cpp, page_table); break;
-        case 4: hipLaunchKernelGGL(page_copy_kernel<4>, grid, block, 0, s, src_base, dst_base, page_bytes, entries, n, cpp, page_table); break;
-        case 2: hipLaunchKernelGGL(page_copy_kernel<2>, grid, block, 0, s, src_base, dst_base, page_bytes, entries, n, cpp, page_table); break;
-        default: hipLaunchKernelGGL(page_copy_kernel<1>, grid, block, 0, s, src_base, dst_base, page_bytes, entries, n, cpp, page_table); break;
+        case 8: hipLaunchKernelGGL(page_copy_kernel<8>, grid, block, 0, s, src_base, src_stride, dst_base, dst_stride, entries, n, cpp, page_table); break;
+        case 4: hipLaunchKernelGGL(page_copy_kernel<4>, grid, block, 0, s, src_base, src_stride, dst_base, dst_stride, entries, n, cpp, page_table); break;
+        case 2: hipLaunchKernelGGL(page_copy_kernel<2>, grid, block, 0, s, src_base, src_stride, dst_base, dst_stride, entries, n, cpp, page_table); break;
+        default: hipLaunchKernelGGL(page_copy_kernel<1>, grid, block, 0, s, src_base, src_stride, dst_base, dst_stride, entries, n, cpp, page_table); break;
     }
     return hipGetLastError();
 }

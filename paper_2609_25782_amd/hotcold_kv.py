@@ -25,6 +25,8 @@ KV_COLD_DEVICE, KV_COLD_PINNED_HOST = 0, 1
 KV_SESSION_FREE, KV_SESSION_ACTIVE, KV_SESSION_PAUSED = 0, 1, 2
 KV_POOL_METADATA_ONLY = 1
 KV_KERNEL_DECODE_SPLIT, KV_KERNEL_DECODE_COMBINE, KV_KERNEL_PAGE_COPY, KV_KERNEL_EVICT_COPY = 0, 1, 2, 3
+KV_KERNEL_PREFETCH_COPY = 4
+KV_PAGE_COLD, KV_PAGE_STAGED = 1 << 30, 1 << 29
 KV_COMBINE_SEPARATE, KV_COMBINE_FUSED = 0, 1
 
 
@@ -48,7 +50,8 @@ class kv_pool_stats(ctypes.Structure):
                 ("bytes_to_cold", ctypes.c_int64), ("bytes_to_hot", ctypes.c_int64),
                 ("resumes", ctypes.c_int64), ("evicts", ctypes.c_int64),
                 ("resume_pages_resident", ctypes.c_int64), ("resume_pages_total", ctypes.c_int64),
-                ("lru_evicted_pages", ctypes.c_int64)]
+                ("lru_evicted_pages", ctypes.c_int64), ("spilled_pages", ctypes.c_int64),
+                ("promoted_pages", ctypes.c_int64)]
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}
@@ -80,6 +83,11 @@ _SIGS = {
     "kv_fill_synthetic": (ctypes.c_int, [_P, _I32, _I32, _U64, ctypes.c_float, _P]),
     "kv_fill_synthetic_pages": (ctypes.c_int, [_P, _I32, _I32, _U64, ctypes.c_float, _I32, _I32, _P]),
     "kv_evict_session": (ctypes.c_int, [_P, _I32, _P]),
+    "kv_pool_set_spill": (ctypes.c_int, [_P, _I32]),
+    "kv_promote_pages": (ctypes.c_int, [_P, _I32, _P, _PI32]),
+    "kv_pool_set_staging": (ctypes.c_int, [_P, _P, _SZ, _PI32]),
+    "paged_decode_stage": (ctypes.c_int, [_P, _PI32, _I32, _P, _P, _PI32]),
+    "paged_decode_prefetch": (ctypes.c_int, [_P, _I32, _P]),
     "kv_evict_sessions": (ctypes.c_int, [_P, _PI32, _I32, _P]),
     "kv_resume_session": (ctypes.c_int, [_P, _I32, _P]),
     "kv_resume_sessions": (ctypes.c_int, [_P, _PI32, _I32, _P]),
@@ -212,6 +220,34 @@ def kv_fill_synthetic_pages(pool: int, sid: int, gen_sid: int, seed: int, value_
                             first_page: int, num_pages: int, stream: int = 0) -> None:
     _check(_lib.kv_fill_synthetic_pages(pool, sid, gen_sid, seed, value_mult, first_page, num_pages,
                                         stream or None), "kv_fill_synthetic_pages")
+
+
+def kv_pool_set_spill(pool: int, enable: bool) -> None:
+    _check(_lib.kv_pool_set_spill(pool, 1 if enable else 0), "kv_pool_set_spill")
+
+
+def kv_promote_pages(pool: int, n: int, stream: int = 0) -> int:
+    got = ctypes.c_int32()
+    _check(_lib.kv_promote_pages(pool, n, stream or None, ctypes.byref(got)), "kv_promote_pages")
+    return got.value
+
+
+def kv_pool_set_staging(pool: int, staging_ptr: int, nbytes: int) -> int:
+    slots = ctypes.c_int32()
+    _check(_lib.kv_pool_set_staging(pool, staging_ptr or None, nbytes, ctypes.byref(slots)),
+           "kv_pool_set_staging")
+    return slots.value
+
+
+def paged_decode_stage(pool: int, sids: Sequence[int], table_ptr: int, stream: int = 0) -> int:
+    staged = ctypes.c_int32()
+    _check(_lib.paged_decode_stage(pool, _i32_array(sids), len(sids), table_ptr or None, stream or None,
+                                   ctypes.byref(staged)), "paged_decode_stage")
+    return staged.value
+
+
+def paged_decode_prefetch(pool: int, layer: int, copy_stream: int = 0) -> None:
+    _check(_lib.paged_decode_prefetch(pool, layer, copy_stream or None), "paged_decode_prefetch")
 
 
 def kv_evict_session(pool: int, sid: int, stream: int = 0) -> None:

@@ -1,0 +1,278 @@
+"""Spill and decode from the cold tier (GPU).
+
+With spill on, pages that find no hot page live in the cold tier and the page
+table names them with KV_PAGE_COLD.  Checked here against the oracle: the
+device page table and every page's bytes follow the pool model through random
+spill / promote / resume / evict sequences; decode reads spilled pages directly
+(device memory or pinned host memory over PCIe) or through the staging buffer
+that the one-layer-ahead prefetch fills, and matches the fp64 oracle; writes
+into spilled pages land in the cold tier; promotion copies them back bit for
+bit.  A layer decoded without its prefetch reads no staged data (NaN rows).
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from helpers import Case, to_device, to_host, tolerance_check
+from oracle.pool_model import COLD_BIT, PoolModel
+
+pytestmark = pytest.mark.gpu
+
+COLD_TIERS = ["device", "host"]
+SEED = 23
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch.device("cuda", 0)
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _random_fill(pool, seed):
+    g = torch.Generator(device=pool.device)
+    g.manual_seed(seed)
+    pool.hot.copy_(torch.randint(0, 256, pool.hot.shape, dtype=torch.uint8, device=pool.device, generator=g))
+    pool.cold.copy_(torch.randint(0, 256, pool.cold.shape, dtype=torch.uint8, device=pool.device, generator=g))
+
+
+@pytest.mark.parametrize("cold", COLD_TIERS)
+def test_spill_sequences_match_model(dev, cold):
+    """Random create / extend / pause / resume / promote / evict / LRU-evict /
+    destroy in spill mode: the device page table (cold-tagged entries
+    included), the statistics and the bytes of every resident page and valid
+    cold copy follow the model."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+    _say("spill sequences, cold tier in %s memory" % cold)
+    nh, nc, ms, stride = 14, 70, 6, 8
+    pool = HotColdPool(2, 2, 64, "bf16", nh, nc, ms, stride, cold_location=cold)
+    kv.kv_pool_set_spill(pool.handle, True)
+    model = PoolModel(nh, nc, ms, stride, spill=True)
+    _random_fill(pool, 5)
+    torch.cuda.synchronize()
+    hot_img = pool.hot.view(nh, -1).cpu().numpy().copy()
+    cold_img = pool.cold.view(nc, -1).cpu().numpy().copy()
+    rng = np.random.default_rng(6)
+
+    def both(model_call, lib_call):
+        try:
+            r = model_call()
+        except Exception:
+            with pytest.raises(kv.KVError):
+                lib_call()
+            return None
+        got = lib_call()
+        return r, got
+
+    for step in range(300):
+        op, sid = int(rng.integers(0, 8)), int(rng.integers(0, ms))
+        if op == 0:
+            L = int(rng.integers(0, 16 * stride + 1))
+            r = both(lambda: model.create(L), lambda: pool.create_session(L))
+            if r:
+                assert r[0] == r[1]
+                for h, c in model.last_victim_copies:
+                    cold_img[c] = hot_img[h]
+        elif op == 1:
+            both(lambda: model.pause(sid), lambda: pool.pause(sid))
+        elif op == 2:
+            r = both(lambda: model.resume([sid]), lambda: pool.resume([sid]))
+            if r:
+                for h, c in model.last_victim_copies:
+                    cold_img[c] = hot_img[h]
+                for c, h in r[0][0]:
+                    hot_img[h] = cold_img[c]
+        elif op == 3:
+            L = int(rng.integers(0, 16 * stride + 1))
+            r = both(lambda: model.extend(sid, L), lambda: pool.extend(sid, L))
+            if r:
+                for h, c in model.last_victim_copies:
+                    cold_img[c] = hot_img[h]
+        elif op == 4:
+            n = int(rng.integers(0, 6))
+            r = both(lambda: model.promote(n), lambda: kv.kv_promote_pages(pool.handle, n))
+            if r:
+                assert len(r[0]) == r[1]
+                for h, c in model.last_victim_copies:
+                    cold_img[c] = hot_img[h]
+                for c, h in r[0]:
+                    hot_img[h] = cold_img[c]
+        elif op == 5:
+            r = both(lambda: model.evict(sid), lambda: pool.evict(sid))
+            if r:
+                for h, c in r[0]:
+                    cold_img[c] = hot_img[h]
+        elif op == 6:
+            n = int(rng.integers(0, 5))
+            r = both(lambda: model.evict_pages(n), lambda: pool.evict_pages(n))
+            if r:
+                assert r[0][0] == r[1]
+                for h, c in r[0][1]:
+                    cold_img[c] = hot_img[h]
+        else:
+            both(lambda: model.destroy(sid), lambda: pool.destroy_session(sid))
+        torch.cuda.synchronize()
+        got = pool.page_table.cpu().numpy()
+        assert np.array_equal(got, np.array(model.table(), np.int32)), "step %d op %d" % (step, op)
+    st = pool.stats()
+    assert st["spilled_pages"] == model.spilled_pages > 10
+    assert st["promoted_pages"] == model.promoted_pages > 3
+    assert np.any((got >= 0) & ((got & COLD_BIT) != 0))
+    hot_now = pool.hot.view(nh, -1).cpu().numpy()
+    cold_now = pool.cold.view(nc, -1).cpu().numpy()
+    for s in model.sessions:
+        for h, c in zip(s.hot, s.cold):
+            if h >= 0:
+                assert np.array_equal(hot_now[h], hot_img[h])
+            if c >= 0:
+                assert np.array_equal(cold_now[c], cold_img[c])
+    pool.close()
+
+
+def _spilled_pool(dev, cold, lens, hot_pages, layers=2, fill=True):
+    """Sessions b = 0.. of the given lengths created in spill mode with fewer hot
+    pages than they need, filled with generator id b (so the oracle's Case
+    regenerates them)."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+    n_pages = sum(synth.pages_for(L) for L in lens)
+    stride = max(synth.pages_for(L) for L in lens) + 1
+    pool = HotColdPool(layers, 2, 128, "bf16", hot_pages, n_pages + 8, len(lens) + 2, stride,
+                       cold_location=cold)
+    kv.kv_pool_set_spill(pool.handle, True)
+    for b, L in enumerate(lens):
+        assert pool.create_session(L) == b
+        if fill:
+            pool.fill_synthetic(b, b, SEED, float(synth.value_multiplier(1.0)))
+    return pool
+
+
+def _oracle(lens, layer, num_layers=2):
+    return Case(num_layers, 8, 2, 128, "bf16", lens, seed=SEED, layer=layer)
+
+
+LENS = [200, 333, 64, 517, 1]
+
+
+@pytest.mark.parametrize("cold", COLD_TIERS)
+def test_decode_reads_spilled_pages(dev, cold):
+    """Direct reads: the pool's rows name spilled pages with KV_PAGE_COLD and
+    the tiered decode reads them from the cold tier."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    _say("decode of spilled pages read in place, cold tier in %s memory" % cold)
+    pool = _spilled_pool(dev, cold, LENS, hot_pages=30)
+    st = pool.stats()
+    assert st["spilled_pages"] == sum(synth.pages_for(L) for L in LENS) - 30
+    sids = torch.arange(len(LENS), dtype=torch.int32, device=dev)
+    table = pool.gather_table(sids)
+    t = table.cpu().numpy()
+    assert np.any((t >= 0) & ((t & COLD_BIT) != 0))
+    sl = torch.tensor(LENS, dtype=torch.int32, device=dev)
+    for layer in (0, 1):
+        case = _oracle(LENS, layer)
+        got = to_host(pool.decode(layer, to_device(case.q, "bf16", dev), sl, page_table=table))
+        torch.cuda.synchronize()
+        tolerance_check(got, case.oracle_out())
+    pool.close()
+
+
+@pytest.mark.parametrize("cold,slots", [("device", 64), ("host", 64), ("device", 11)])
+def test_decode_through_prefetched_staging(dev, cold, slots):
+    """Staged reads: paged_decode_stage puts spilled pages in staging slots
+    (the rest, when slots run out, stay direct cold reads); each layer's slices
+    are gathered on a second stream one layer ahead of its decode."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    _say("decode through staging, cold tier in %s memory, %d slots" % (cold, slots))
+    pool = _spilled_pool(dev, cold, LENS, hot_pages=30)
+    spilled = pool.stats()["spilled_pages"]
+    slice_bytes = 2 * 2 * 16 * 128 * 2
+    staging = torch.empty(2 * slots * slice_bytes, dtype=torch.uint8, device=dev)
+    assert kv.kv_pool_set_staging(pool.handle, staging.data_ptr(), staging.numel()) == slots
+    table = torch.empty((len(LENS), pool.stride), dtype=torch.int32, device=dev)
+    staged = kv.paged_decode_stage(pool.handle, list(range(len(LENS))), table.data_ptr())
+    assert staged == min(slots, spilled)
+    t = table.cpu().numpy()
+    assert np.sum((t >= 0) & ((t & kv.KV_PAGE_STAGED) != 0) & ((t & COLD_BIT) == 0)) == staged
+    assert np.sum((t >= 0) & ((t & COLD_BIT) != 0)) == spilled - staged
+    sl = torch.tensor(LENS, dtype=torch.int32, device=dev)
+    copy_stream = torch.cuda.Stream()
+    cases = [_oracle(LENS, layer) for layer in (0, 1)]
+    qs = [to_device(c.q, "bf16", dev) for c in cases]
+    kv.paged_decode_prefetch(pool.handle, 0, copy_stream.cuda_stream)
+    outs = []
+    for layer in (0, 1):
+        if layer + 1 < 2:
+            kv.paged_decode_prefetch(pool.handle, layer + 1, copy_stream.cuda_stream)
+        outs.append(pool.decode(layer, qs[layer], sl, page_table=table))
+    torch.cuda.synchronize()
+    for layer in (0, 1):
+        tolerance_check(to_host(outs[layer]), cases[layer].oracle_out())
+    # the next step reuses the plan: prefetch again, decode again, same result
+    for layer in (0, 1):
+        kv.paged_decode_prefetch(pool.handle, layer, copy_stream.cuda_stream)
+        got = to_host(pool.decode(layer, qs[layer], sl, page_table=table))
+        tolerance_check(got, cases[layer].oracle_out())
+    # a layer decoded without its gather reads no staged data: rows with staged
+    # pages are NaN, rows without them are still right
+    kv.paged_decode_stage(pool.handle, list(range(len(LENS))), table.data_ptr())
+    got = to_host(pool.decode(1, qs[1], sl, page_table=table))
+    torch.cuda.synchronize()
+    has_staged = [bool(np.any((r >= 0) & ((r & kv.KV_PAGE_STAGED) != 0))) for r in table.cpu().numpy()]
+    assert any(has_staged)
+    ref = cases[1].oracle_out()
+    for b, flag in enumerate(has_staged):
+        if flag:
+            assert np.all(np.isnan(got[b]))
+        else:
+            tolerance_check(got[b], ref[b])
+    kv.kv_pool_set_staging(pool.handle, 0, 0)
+    pool.close()
+
+
+def test_promote_and_write_into_spilled_pages(dev):
+    """Tokens written into spilled pages land in the cold tier; after the other
+    session is evicted, promotion copies spilled pages into the freed hot pages
+    bit for bit; resuming the evicted session with no hot page left leaves it
+    entirely in the cold tier.  Decode matches the oracle throughout."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    lens = [150, 260]                     # 10 and 17 pages; 12 hot pages
+    pool = _spilled_pool(dev, "device", lens, hot_pages=12, fill=False)
+    assert pool.stats()["spilled_pages"] == 15
+    for layer in (0, 1):                  # every token of both layers through kv_write_tokens
+        for b, L in enumerate(lens):
+            k, v = synth.session_kv(SEED, b, L, layer, 2, 128, 1.0, "bf16")
+            pool.write_tokens(b, layer, 0, to_device(k, "bf16", dev), to_device(v, "bf16", dev))
+    sids = torch.arange(2, dtype=torch.int32, device=dev)
+    sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+
+    def check():
+        table = pool.gather_table(sids)
+        for layer in (0, 1):
+            case = _oracle(lens, layer)
+            got = to_host(pool.decode(layer, to_device(case.q, "bf16", dev), sl, page_table=table))
+            tolerance_check(got, case.oracle_out())
+
+    check()
+    pool.evict(0)                         # 10 dirty pages written, 10 hot pages free
+    assert kv.kv_promote_pages(pool.handle, 100) == 10
+    torch.cuda.synchronize()
+    st, L1, hot1, cold1 = pool.info(1)
+    assert sum(h < 0 for h in hot1) == 5
+    pb = pool.page_bytes
+    for h, c in zip(hot1, cold1):
+        if h >= 0 and c >= 0:
+            assert torch.equal(pool.hot.view(-1, pb)[h], pool.cold.view(-1, pb)[c])
+    pool.resume(0)                        # nothing free or evictable: stays in the cold tier
+    assert all(h < 0 for h in pool.info(0)[2])
+    check()
+    assert pool.stats()["promoted_pages"] == 10
+    pool.close()

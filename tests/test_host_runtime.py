@@ -39,11 +39,13 @@ def _same(kv, pool, model, ms):
     assert st["resume_pages_resident"] == model.resume_resident
     assert st["resume_pages_total"] == model.resume_total
     assert st["lru_evicted_pages"] == model.lru_evicted
+    assert st["spilled_pages"] == model.spilled_pages
+    assert st["promoted_pages"] == model.promoted_pages
 
 
 def _random_call(kv, pool, rng, nh, nc, ms, stride):
     """One random call as a (model call, library call) pair."""
-    op = int(rng.integers(0, 10))
+    op = int(rng.integers(0, 11))
     sid = int(rng.integers(-1, ms + 1))
     if op == 0:
         L = int(rng.integers(-2, 16 * stride + 20))
@@ -69,6 +71,9 @@ def _random_call(kv, pool, rng, nh, nc, ms, stride):
     if op == 8:
         new_len = int(rng.integers(0, 16 * stride + 20))
         return (lambda m: m.extend(sid, new_len)), (lambda: kv.kv_session_extend(pool, sid, new_len))
+    if op == 10:
+        n = int(rng.integers(0, 8))
+        return (lambda m: len(m.promote(n))), (lambda: kv.kv_promote_pages(pool, n))
     if op == 9:
         t0, n_tok = int(rng.integers(-2, 16 * stride)), int(rng.integers(0, 40))
         return (lambda m: m.write_tokens(sid, t0, n_tok)), \
@@ -79,12 +84,14 @@ def _random_call(kv, pool, rng, nh, nc, ms, stride):
     return (lambda m: m.import_cold(L, cold)), (lambda: kv.kv_session_import_cold(pool, L, cold))
 
 
-@pytest.mark.parametrize("seed", range(4))
-def test_random_sequences_follow_the_model(seed):
+@pytest.mark.parametrize("seed,spill", [(0, False), (1, False), (2, False), (3, False),
+                                        (4, True), (5, True), (6, True)])
+def test_random_sequences_follow_the_model(seed, spill):
     kv = _lib()
-    nh, nc, ms, stride = 60, 45, 7, 9
+    nh, nc, ms, stride = (60, 45, 7, 9) if not spill else (20, 90, 7, 9)
     pool = _meta_pool(kv, nh, nc, ms, stride)
-    model = PoolModel(nh, nc, ms, stride)
+    kv.kv_pool_set_spill(pool, spill)
+    model = PoolModel(nh, nc, ms, stride, spill=spill)
     rng = np.random.default_rng(seed)
     refused = 0
     for step in range(1500):
@@ -103,6 +110,8 @@ def test_random_sequences_follow_the_model(seed):
             assert got == expect
         _same(kv, pool, model, ms)
     assert 100 < refused < 1400
+    if spill:
+        assert model.spilled_pages > 20 and model.promoted_pages > 5
     kv.kv_pool_destroy(pool)
 
 
