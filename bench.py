@@ -393,6 +393,79 @@ def measure_agentic_replay(seed: int, plateau_s: float = 20.0):
     return out
 
 
+def measure_spill(seed: int, steps: int = 6, warmup: int = 2):
+    """Decode from the cold tier: 32 active sessions of 4,096 tokens at the
+    paper's shape (48 layers, 4 KV heads, 128, bf16; 32 query heads), 12 GiB of
+    KV, with a fraction of their pages spilled to the cold tier (device memory or
+    pinned host memory over PCIe).  Each step decodes all 48 layers, reading the
+    spilled pages in place ("direct") or through the staging buffer that a
+    second stream fills one layer ahead ("prefetch").  Spilling everything to
+    the host tier is the paper's configuration without tiering: the hot set
+    read over PCIe every step."""
+    import torch
+    import synth
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+
+    n_s, L, hq = 32, 4096, 32
+    pages = n_s * synth.pages_for(L)
+    mult = float(synth.value_multiplier(1.0 / math.sqrt(128)))
+    q = torch.randn(n_s, hq, 128, generator=torch.Generator().manual_seed(seed)).to(torch.bfloat16).cuda()
+    sl = torch.full((n_s,), L, dtype=torch.int32, device="cuda")
+    kv_bytes = 48 * sum(decode_bytes([L] * n_s, hq, 4, 128, 2))
+    rows = []
+    copy_stream = torch.cuda.Stream()
+    for tier in ("device", "host"):
+        for frac in ((0.0, 0.25, 0.5, 1.0) if tier == "device" else (0.25, 0.5, 1.0)):
+            hot = pages - int(round(frac * pages))
+            pool = HotColdPool(48, 4, 128, "bf16", max(hot, 1), pages + 16, n_s, synth.pages_for(L) + 1,
+                               cold_location=tier)
+            kv.kv_pool_set_spill(pool.handle, True)
+            for b in range(n_s):
+                pool.create_session(L)
+                pool.fill_synthetic(b, b, seed, mult)
+            spilled = pool.stats()["spilled_pages"]
+            sids = torch.arange(n_s, dtype=torch.int32, device="cuda")
+            direct = pool.gather_table(sids)
+            out = torch.empty_like(q)
+            staging = table = None
+            if spilled:
+                staging = torch.empty(2 * spilled * pool.page_bytes // 48, dtype=torch.uint8, device="cuda")
+                kv.kv_pool_set_staging(pool.handle, staging.data_ptr(), staging.numel())
+                table = torch.empty((n_s, pool.stride), dtype=torch.int32, device="cuda")
+                kv.paged_decode_stage(pool.handle, list(range(n_s)), table.data_ptr())
+            torch.cuda.synchronize()
+            for mode in (("direct", "prefetch") if spilled else ("hot", "hot_tiered_kernel")):
+                # all pages hot: the plain kernel, then the tier-aware one (spill on)
+                kv.kv_pool_set_spill(pool.handle, mode != "hot")
+                times = []
+                for it in range(warmup + steps):
+                    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    t0.record()
+                    if mode == "prefetch":
+                        copy_stream.wait_event(t0)
+                        kv.paged_decode_prefetch(pool.handle, 0, copy_stream.cuda_stream)
+                    for layer in range(48):
+                        if mode == "prefetch" and layer + 1 < 48:
+                            kv.paged_decode_prefetch(pool.handle, layer + 1, copy_stream.cuda_stream)
+                        pool.decode(layer, q, sl, page_table=table if mode == "prefetch" else direct, out=out)
+                    t1.record()
+                    torch.cuda.synchronize()
+                    if it >= warmup:
+                        times.append(t0.elapsed_time(t1))
+                ms = float(np.median(times))
+                rows.append({"cold_tier": tier, "spilled_frac": round(spilled / pages, 3), "mode": mode,
+                             "step_ms": round(ms, 3), "GBps": round(kv_bytes / (ms / 1e3) / 1e9, 1)})
+                log("spill: %s" % json.dumps(rows[-1]))
+            if spilled:
+                kv.kv_pool_set_staging(pool.handle, 0, 0)
+            pool.close()
+            del pool, staging, table, direct
+            torch.cuda.empty_cache()
+    return {"config": "32 sessions x 4,096 tokens, 48 layers x 4 KV heads x 128 bf16, 32 query heads "
+                      "(12 GiB of KV per step)", "kv_bytes_per_step": kv_bytes, "rows": rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -407,9 +480,16 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--no-check", action="store_true", help="skip the sampled oracle check")
-    ap.add_argument("--no-resume-mix", action="store_true",
-                    help="skip the 48-layer resume-heavy measurement (needs ~235 GB of HBM)")
+    ap.add_argument("--sections", default="resume48,host,replay,spill",
+                    help="measurements after the hot-path step, comma separated: resume48 (48-layer "
+                         "resume mix, ~235 GB of HBM), host (pinned-host cold tier), replay (agentic "
+                         "replay on a device pool), spill (decode from the cold tier); 'none' for none")
+    ap.add_argument("--no-resume-mix", action="store_true", help="same as --sections none")
     args = ap.parse_args()
+    sections = set() if args.no_resume_mix else {x for x in args.sections.split(",") if x and x != "none"}
+    unknown = sections - {"resume48", "host", "replay", "spill"}
+    if unknown:
+        ap.error("unknown sections: %s" % ", ".join(sorted(unknown)))
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -571,13 +651,17 @@ def main():
     pool.close()
     del pool
     torch.cuda.empty_cache()
-    if not args.no_resume_mix:
+    if "resume48" in sections:
         result["resume48"] = measure_resume_mix(args.seed, max(3, args.steps // 4), 1)
         log("resume mix: %s" % json.dumps(result["resume48"]))
+    if "host" in sections:
         result["resume_host_tier"] = measure_host_tier(args.seed)
         log("host tier: %s" % json.dumps(result["resume_host_tier"]))
+    if "replay" in sections:
         result["agentic_replay"] = measure_agentic_replay(args.seed)
         log("agentic replay: %s" % json.dumps(result["agentic_replay"]))
+    if "spill" in sections:
+        result["spill_decode"] = measure_spill(args.seed)
     if args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
     print(json.dumps(result), flush=True)
