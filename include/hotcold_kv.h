@@ -150,6 +150,7 @@ typedef struct kv_pool_stats {
     int64_t lru_evicted_pages;     /* pages of paused sessions evicted page by page (LRU) */
     int64_t spilled_pages;         /* pages placed or left in the cold tier by spill */
     int64_t promoted_pages;        /* spilled pages moved back to the hot tier */
+    int64_t cold_active_pages;     /* now: pages of ACTIVE sessions living in the cold tier */
 } kv_pool_stats;
 
 /* ----------------------------------------------------------------------- */

@@ -402,3 +402,7 @@ class PoolModel:
 
     def free_cold(self) -> int:
         return len(self.cold_free)
+
+    def cold_active(self) -> int:
+        """Pages of active sessions living in the cold tier (spilled)."""
+        return sum(1 for s in self.sessions if s.state == ACTIVE for h in s.hot if h < 0)

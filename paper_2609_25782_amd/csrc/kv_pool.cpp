@@ -624,10 +624,14 @@ int kv_pool_stats_get(const kv_pool* pool, kv_pool_stats* out) {
     out->free_hot_pages = pool->hot_free.free_count();
     out->free_cold_pages = pool->cold_free.free_count();
     int32_t a = 0, p = 0;
+    int64_t cold_active = 0;
     for (const auto& s : pool->sessions) {
         a += s.state == KV_SESSION_ACTIVE;
         p += s.state == KV_SESSION_PAUSED;
+        if (s.state == KV_SESSION_ACTIVE)
+            for (int32_t h : s.hot) cold_active += h < 0;
     }
+    out->cold_active_pages = cold_active;
     out->active_sessions = a;
     out->paused_sessions = p;
     return KV_OK;

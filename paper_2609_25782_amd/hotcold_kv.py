@@ -51,7 +51,7 @@ class kv_pool_stats(ctypes.Structure):
                 ("resumes", ctypes.c_int64), ("evicts", ctypes.c_int64),
                 ("resume_pages_resident", ctypes.c_int64), ("resume_pages_total", ctypes.c_int64),
                 ("lru_evicted_pages", ctypes.c_int64), ("spilled_pages", ctypes.c_int64),
-                ("promoted_pages", ctypes.c_int64)]
+                ("promoted_pages", ctypes.c_int64), ("cold_active_pages", ctypes.c_int64)]
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}

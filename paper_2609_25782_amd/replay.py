@@ -82,6 +82,8 @@ class ReplayConfig:
     gap_median_s: float = 8.0
     gap_mean_s: float = 23.0
     max_sessions: int = 4096              # rows of the pool's page table
+    spill: bool = False                   # no pinning: spill to the cold tier instead of preempting
+    promote_s: float = 0.5                # with spill: move spilled active pages back this often
     pe_cycles: float = 1e5
     waf: float = 1.02
     hbm_pj_per_bit: float = 3.5
@@ -130,6 +132,7 @@ class LibraryPool:
                                    cfg.max_sessions, cfg.stride, 0, kv.KV_POOL_METADATA_ONLY)
             handle = kv.kv_pool_create(desc, 0, 0, 0, 0, 0)
         self.h = handle
+        kv.kv_pool_set_spill(self.h, cfg.spill)
 
     REFUSED = (kv.KV_ERR_NO_HOT_PAGES, kv.KV_ERR_NO_COLD_PAGES)
 
@@ -153,6 +156,9 @@ class LibraryPool:
 
     def destroy(self, sid: int) -> None:
         kv.kv_session_destroy(self.h, sid)
+
+    def promote(self, n: int) -> int:
+        return kv.kv_promote_pages(self.h, n)
 
     def stats(self) -> Dict[str, int]:
         return kv.kv_pool_stats_get(self.h)
@@ -489,6 +495,7 @@ class Replay:
         warm = int(round(cfg.warmup_s / cfg.step_s))
         total = warm + int(round(cfg.plateau_s / cfg.step_s))
         every = max(1, int(round(cfg.sample_s / cfg.step_s)))
+        promote_every = max(1, int(round(cfg.promote_s / cfg.step_s)))
         self.plateau_start = warm
         base = None
         samples = []
@@ -498,11 +505,14 @@ class Replay:
             if self.step >= warm and hasattr(decode_fn, "step_begin"):
                 decode_fn.step_begin()
             self._advance(decode_fn if self.step >= warm else None)
+            if cfg.spill and self.step % promote_every == 0:
+                self.pool.promote(1 << 30)
             if self.step >= warm and (self.step - warm) % every == 0:
                 st = self.pool.stats()
                 samples.append((cfg.num_hot_pages - st["free_hot_pages"],
                                 cfg.num_cold_pages - st["free_cold_pages"],
-                                len(self.agents), self.live_pages, self.active_pages, self.active))
+                                len(self.agents), self.live_pages, self.active_pages, self.active,
+                                st.get("cold_active_pages", 0)))
         return self._summary(base, self.pool.stats(), np.array(samples, dtype=np.float64),
                              (total - warm) * cfg.step_s)
 
@@ -512,7 +522,10 @@ class Replay:
         d = {k: end[k] - base[k] for k in ("pages_to_cold", "pages_to_hot", "resumes",
                                           "resume_pages_resident", "resume_pages_total",
                                           "lru_evicted_pages")}
-        hot_used, cold_used, live, live_pages, active_pages, batch = samples.mean(axis=0)
+        for k in ("spilled_pages", "promoted_pages"):
+            if k in end:
+                d[k] = end[k] - base[k]
+        hot_used, cold_used, live, live_pages, active_pages, batch, cold_active = samples.mean(axis=0)
         write_bps = d["pages_to_cold"] * pb / secs
         fetch_bps = d["pages_to_hot"] * pb / secs
         produced_bps = self.produced_tokens * cfg.token_bytes / secs
@@ -556,6 +569,7 @@ class Replay:
                 "with_flash": round(acc.sessions_per_device(cfg.hbm_bytes, cfg.weight_bytes, per_session,
                                                             cfg.cold_bytes), 1) if per_session else None},
             "mean_batch": round(float(batch), 2),
+            "spill": self._spill_summary(cold_active, active_pages) if cfg.spill else None,
             "decode_tokens_per_s": round(batch / cfg.step_s, 1),
             "plateau_counts": dict(d, produced_tokens=self.produced_tokens),
             "refused_admissions": self.refused_admissions,
@@ -563,6 +577,16 @@ class Replay:
             "sessions_started": self.sessions_started,
             "sessions_finished": self.sessions_finished,
         }
+
+    def _spill_summary(self, cold_active: float, active_pages: float) -> Dict:
+        """Decode reads of spilled pages: the share of the hot set living in the
+        cold tier and the step time each tier's bandwidth adds to read it."""
+        cfg = self.cfg
+        cold_bytes = cold_active * cfg.page_bytes
+        return {"cold_share_of_hot_set": round(cold_active / active_pages, 4) if active_pages else 0.0,
+                "cold_read_per_step_mib": round(cold_bytes / 2 ** 20, 1),
+                "added_tbt_ms": {name: round((cold_bytes / bw + (lat if cold_bytes else 0.0)) * 1e3, 3)
+                                 for name, bw, lat in cfg.tiers}}
 
     def close(self) -> None:
         self.pool.close()

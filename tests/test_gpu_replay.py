@@ -27,12 +27,13 @@ def dev():
     return torch.device("cuda", 0)
 
 
-def _cfg():
+def _cfg(spill=False):
     from paper_2609_25782_amd import replay as rp
     cfg = rp.ReplayConfig(n_active=6, num_layers=2, num_kv_heads=2, head_dim=64, elt_bytes=2,
                           weight_bytes=0.0, tbt_s=1.0, warmup_s=80, plateau_s=320, sample_s=1.0,
                           prompt0=(10, 40), turn_prompt=(5, 30), turn_decode=(5, 40), peak=(60, 160),
-                          gap_median_s=6.0, gap_mean_s=15.0, max_sessions=64, seed=3)
+                          gap_median_s=6.0, gap_mean_s=15.0, max_sessions=64, seed=3,
+                          spill=spill, promote_s=7.0)
     cfg.hbm_bytes = 40 * cfg.page_bytes       # LRU pressure, partial resumes and preemptions
     cfg.cold_bytes = 2000 * cfg.page_bytes
     return cfg
@@ -46,13 +47,15 @@ def _oracle(lens, gens, q, layer):
 
 
 @pytest.mark.timeout(300)
-def test_device_replay_follows_metadata_and_keeps_kv(dev):
+@pytest.mark.parametrize("spill", [False, True])
+def test_device_replay_follows_metadata_and_keeps_kv(dev, spill):
     import torch
     from paper_2609_25782_amd import hotcold_kv as kv
     from paper_2609_25782_amd import replay as rp
     from paper_2609_25782_amd.pool import HotColdPool
 
-    cfg = _cfg()
+    cfg = _cfg(spill)
+    print("replay, spill %s" % spill, flush=True)
     meta = rp.Replay(cfg)
     want = meta.run()
     print("metadata replay:", want["plateau_counts"], flush=True)
@@ -71,6 +74,9 @@ def test_device_replay_follows_metadata_and_keeps_kv(dev):
         assert kv.kv_session_info(dp.h, sid) == kv.kv_session_info(meta.pool.h, sid)
     c = got["plateau_counts"]
     assert c["pages_to_cold"] > 0 and 0 < c["resume_pages_resident"] < c["resume_pages_total"]
+    if spill:                      # decode read spilled pages in place, then they came back
+        assert got["preemptions"] == 0 and c["spilled_pages"] > 0 and c["promoted_pages"] > 0
+        assert got["spill"]["cold_share_of_hot_set"] > 0
     t = dec.timings()
     assert len(t["step_ms"]) == int(cfg.plateau_s / cfg.step_s) and np.all(t["decode_ms"] > 0)
 

@@ -41,6 +41,7 @@ def _same(kv, pool, model, ms):
     assert st["lru_evicted_pages"] == model.lru_evicted
     assert st["spilled_pages"] == model.spilled_pages
     assert st["promoted_pages"] == model.promoted_pages
+    assert st["cold_active_pages"] == model.cold_active()
 
 
 def _random_call(kv, pool, rng, nh, nc, ms, stride):

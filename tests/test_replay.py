@@ -20,7 +20,8 @@ class ModelPool:
     """The oracle's pool model behind the replay's pool interface."""
 
     def __init__(self, cfg):
-        self.m = PoolModel(cfg.num_hot_pages, cfg.num_cold_pages, cfg.max_sessions, cfg.stride)
+        self.m = PoolModel(cfg.num_hot_pages, cfg.num_cold_pages, cfg.max_sessions, cfg.stride,
+                           spill=cfg.spill)
 
     def refused(self, e):
         return isinstance(e, ModelError) and e.code in (ERR_NO_HOT, ERR_NO_COLD)
@@ -43,12 +44,17 @@ class ModelPool:
     def destroy(self, sid):
         self.m.destroy(sid)
 
+    def promote(self, n):
+        return len(self.m.promote(n))
+
     def stats(self):
         m = self.m
         return {"free_hot_pages": m.free_hot(), "free_cold_pages": m.free_cold(),
                 "pages_to_cold": m.cold_writes, "pages_to_hot": m.pages_to_hot,
                 "resumes": m.resumes, "resume_pages_resident": m.resume_resident,
-                "resume_pages_total": m.resume_total, "lru_evicted_pages": m.lru_evicted}
+                "resume_pages_total": m.resume_total, "lru_evicted_pages": m.lru_evicted,
+                "spilled_pages": m.spilled_pages, "promoted_pages": m.promoted_pages,
+                "cold_active_pages": m.cold_active()}
 
     def close(self):
         pass
@@ -87,7 +93,8 @@ def test_hand_worked_cycle():
         s = r.run()
         assert s["plateau_counts"] == {                          # plateau: two cycles
             "resumes": 4, "resume_pages_resident": 4, "resume_pages_total": 8,
-            "pages_to_cold": 4, "pages_to_hot": 4, "lru_evicted_pages": 4, "produced_tokens": 256}
+            "pages_to_cold": 4, "pages_to_hot": 4, "lru_evicted_pages": 4, "produced_tokens": 256,
+            "spilled_pages": 0, "promoted_pages": 0}
         assert s["resume_hit_rate"] == 0.5
         st = r.pool.stats()                                       # three cycles in all
         assert (st["resumes"], st["pages_to_cold"], st["pages_to_hot"]) == (6, 6, 6)
@@ -217,4 +224,45 @@ def test_decode_lengths_stay_within_resident_pages(hot_pages, n_active):
 
     r.run(check)
     assert seen[0] > 1000
+    r.close()
+
+
+def test_spill_replaces_preemption_and_follows_the_model():
+    """The over-full configuration of the preemption test with spill on: no
+    session is paused mid-turn; pages spill to the cold tier and are promoted
+    back, with the library and the model taking the same decisions."""
+    cfg = _tiny(n_active=4, prompt0=(30, 40), turn_prompt=(10, 20), turn_decode=(60, 80),
+                peak=(150, 200), gap_median_s=2.0, gap_mean_s=4.0, warmup_s=50, plateau_s=800,
+                spill=True, promote_s=3.0)
+    cfg.hbm_bytes = _pages_bytes(cfg, 18)
+    cfg.cold_bytes = _pages_bytes(cfg, 400)
+    lib = rp.Replay(cfg)
+    a = lib.run()
+    b = rp.Replay(cfg, ModelPool(cfg)).run()
+    assert a == b
+    assert a["preemptions"] == 0 and a["sessions_finished"] > 5
+    c = a["plateau_counts"]
+    assert c["spilled_pages"] > 0 and c["promoted_pages"] > 0
+    assert 0 < a["spill"]["cold_share_of_hot_set"] < 1
+    lib.close()
+
+
+def test_spill_decode_lengths_stay_within_allocated_pages():
+    cfg = _tiny(n_active=4, prompt0=(30, 40), turn_prompt=(10, 20), turn_decode=(60, 80),
+                peak=(150, 200), gap_median_s=2.0, gap_mean_s=4.0, warmup_s=20, plateau_s=400,
+                spill=True)
+    cfg.hbm_bytes = _pages_bytes(cfg, 18)
+    cfg.cold_bytes = _pages_bytes(cfg, 400)
+    r = rp.Replay(cfg)
+    spilled_seen = [0]
+
+    def check(lengths):
+        for sid, n in lengths:
+            state, L, hot, cold = rp.kv.kv_session_info(r.pool.h, sid)
+            assert state == rp.kv.KV_SESSION_ACTIVE and 0 < n <= 16 * len(hot)
+            assert all(h >= 0 or c >= 0 for h, c in zip(hot, cold))
+            spilled_seen[0] += sum(h < 0 for h in hot)
+
+    r.run(check)
+    assert spilled_seen[0] > 0
     r.close()
