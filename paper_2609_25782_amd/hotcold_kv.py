@@ -25,7 +25,7 @@ KV_COLD_DEVICE, KV_COLD_PINNED_HOST = 0, 1
 KV_SESSION_FREE, KV_SESSION_ACTIVE, KV_SESSION_PAUSED = 0, 1, 2
 KV_POOL_METADATA_ONLY = 1
 KV_KERNEL_DECODE_SPLIT, KV_KERNEL_DECODE_COMBINE, KV_KERNEL_PAGE_COPY, KV_KERNEL_EVICT_COPY = 0, 1, 2, 3
-KV_KERNEL_PREFETCH_COPY = 4
+KV_KERNEL_PREFETCH_COPY, KV_KERNEL_COUNT = 4, 5
 KV_PAGE_COLD, KV_PAGE_STAGED = 1 << 30, 1 << 29
 KV_COMBINE_SEPARATE, KV_COMBINE_FUSED = 0, 1
 
