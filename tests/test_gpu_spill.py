@@ -138,7 +138,7 @@ def test_spill_sequences_match_model(dev, cold):
     pool.close()
 
 
-def _spilled_pool(dev, cold, lens, hot_pages, layers=2, fill=True):
+def _spilled_pool(dev, cold, lens, hot_pages, layers=2, fill=True, dtype="bf16", d=128):
     """Sessions b = 0.. of the given lengths created in spill mode with fewer hot
     pages than they need, filled with generator id b (so the oracle's Case
     regenerates them)."""
@@ -146,7 +146,7 @@ def _spilled_pool(dev, cold, lens, hot_pages, layers=2, fill=True):
     from paper_2609_25782_amd.pool import HotColdPool
     n_pages = sum(synth.pages_for(L) for L in lens)
     stride = max(synth.pages_for(L) for L in lens) + 1
-    pool = HotColdPool(layers, 2, 128, "bf16", hot_pages, n_pages + 8, len(lens) + 2, stride,
+    pool = HotColdPool(layers, 2, d, dtype, hot_pages, n_pages + 8, len(lens) + 2, stride,
                        cold_location=cold)
     kv.kv_pool_set_spill(pool.handle, True)
     for b, L in enumerate(lens):
@@ -156,20 +156,22 @@ def _spilled_pool(dev, cold, lens, hot_pages, layers=2, fill=True):
     return pool
 
 
-def _oracle(lens, layer, num_layers=2):
-    return Case(num_layers, 8, 2, 128, "bf16", lens, seed=SEED, layer=layer)
+def _oracle(lens, layer, num_layers=2, dtype="bf16", d=128):
+    return Case(num_layers, 8, 2, d, dtype, lens, seed=SEED, layer=layer)
 
 
 LENS = [200, 333, 64, 517, 1]
 
 
-@pytest.mark.parametrize("cold", COLD_TIERS)
-def test_decode_reads_spilled_pages(dev, cold):
+@pytest.mark.parametrize("cold,dtype,d", [("device", "bf16", 128), ("host", "bf16", 128),
+                                         ("device", "f32", 64), ("host", "f32", 128),
+                                         ("device", "bf16", 64)])
+def test_decode_reads_spilled_pages(dev, cold, dtype, d):
     """Direct reads: the pool's rows name spilled pages with KV_PAGE_COLD and
-    the tiered decode reads them from the cold tier."""
+    the tiered decode reads them from the cold tier (every shape's kernel)."""
     from paper_2609_25782_amd import hotcold_kv as kv
-    _say("decode of spilled pages read in place, cold tier in %s memory" % cold)
-    pool = _spilled_pool(dev, cold, LENS, hot_pages=30)
+    _say("decode of spilled pages read in place, cold tier in %s memory, %s d=%d" % (cold, dtype, d))
+    pool = _spilled_pool(dev, cold, LENS, hot_pages=30, dtype=dtype, d=d)
     st = pool.stats()
     assert st["spilled_pages"] == sum(synth.pages_for(L) for L in LENS) - 30
     sids = torch.arange(len(LENS), dtype=torch.int32, device=dev)
@@ -177,24 +179,26 @@ def test_decode_reads_spilled_pages(dev, cold):
     t = table.cpu().numpy()
     assert np.any((t >= 0) & ((t & COLD_BIT) != 0))
     sl = torch.tensor(LENS, dtype=torch.int32, device=dev)
+    tol = {} if dtype == "bf16" else {"max_norm": 1e-5}
     for layer in (0, 1):
-        case = _oracle(LENS, layer)
-        got = to_host(pool.decode(layer, to_device(case.q, "bf16", dev), sl, page_table=table))
+        case = _oracle(LENS, layer, dtype=dtype, d=d)
+        got = to_host(pool.decode(layer, to_device(case.q, dtype, dev), sl, page_table=table))
         torch.cuda.synchronize()
-        tolerance_check(got, case.oracle_out())
+        tolerance_check(got, case.oracle_out(), **tol)
     pool.close()
 
 
-@pytest.mark.parametrize("cold,slots", [("device", 64), ("host", 64), ("device", 11)])
-def test_decode_through_prefetched_staging(dev, cold, slots):
+@pytest.mark.parametrize("cold,slots,dtype,d", [("device", 64, "bf16", 128), ("host", 64, "bf16", 128),
+                                               ("device", 11, "bf16", 128), ("device", 20, "f32", 64)])
+def test_decode_through_prefetched_staging(dev, cold, slots, dtype, d):
     """Staged reads: paged_decode_stage puts spilled pages in staging slots
     (the rest, when slots run out, stay direct cold reads); each layer's slices
     are gathered on a second stream one layer ahead of its decode."""
     from paper_2609_25782_amd import hotcold_kv as kv
-    _say("decode through staging, cold tier in %s memory, %d slots" % (cold, slots))
-    pool = _spilled_pool(dev, cold, LENS, hot_pages=30)
+    _say("decode through staging, cold tier in %s memory, %d slots, %s d=%d" % (cold, slots, dtype, d))
+    pool = _spilled_pool(dev, cold, LENS, hot_pages=30, dtype=dtype, d=d)
     spilled = pool.stats()["spilled_pages"]
-    slice_bytes = 2 * 2 * 16 * 128 * 2
+    slice_bytes = 2 * 2 * 16 * d * (2 if dtype == "bf16" else 4)
     staging = torch.empty(2 * slots * slice_bytes, dtype=torch.uint8, device=dev)
     assert kv.kv_pool_set_staging(pool.handle, staging.data_ptr(), staging.numel()) == slots
     table = torch.empty((len(LENS), pool.stride), dtype=torch.int32, device=dev)
@@ -205,8 +209,9 @@ def test_decode_through_prefetched_staging(dev, cold, slots):
     assert np.sum((t >= 0) & ((t & COLD_BIT) != 0)) == spilled - staged
     sl = torch.tensor(LENS, dtype=torch.int32, device=dev)
     copy_stream = torch.cuda.Stream()
-    cases = [_oracle(LENS, layer) for layer in (0, 1)]
-    qs = [to_device(c.q, "bf16", dev) for c in cases]
+    cases = [_oracle(LENS, layer, dtype=dtype, d=d) for layer in (0, 1)]
+    qs = [to_device(c.q, dtype, dev) for c in cases]
+    tol = {} if dtype == "bf16" else {"max_norm": 1e-5}
     kv.paged_decode_prefetch(pool.handle, 0, copy_stream.cuda_stream)
     outs = []
     for layer in (0, 1):
@@ -215,12 +220,12 @@ def test_decode_through_prefetched_staging(dev, cold, slots):
         outs.append(pool.decode(layer, qs[layer], sl, page_table=table))
     torch.cuda.synchronize()
     for layer in (0, 1):
-        tolerance_check(to_host(outs[layer]), cases[layer].oracle_out())
+        tolerance_check(to_host(outs[layer]), cases[layer].oracle_out(), **tol)
     # the next step reuses the plan: prefetch again, decode again, same result
     for layer in (0, 1):
         kv.paged_decode_prefetch(pool.handle, layer, copy_stream.cuda_stream)
         got = to_host(pool.decode(layer, qs[layer], sl, page_table=table))
-        tolerance_check(got, cases[layer].oracle_out())
+        tolerance_check(got, cases[layer].oracle_out(), **tol)
     # a layer decoded without its gather reads no staged data: rows with staged
     # pages are NaN, rows without them are still right
     kv.paged_decode_stage(pool.handle, list(range(len(LENS))), table.data_ptr())
@@ -233,7 +238,7 @@ def test_decode_through_prefetched_staging(dev, cold, slots):
         if flag:
             assert np.all(np.isnan(got[b]))
         else:
-            tolerance_check(got[b], ref[b])
+            tolerance_check(got[b], ref[b], **tol)
     kv.kv_pool_set_staging(pool.handle, 0, 0)
     pool.close()
 
