@@ -233,6 +233,41 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
         budget.append({"copy_blocks": blocks, "resume_ms_per_session": round(ms_b / len(sids), 3),
                        "decode48_ms_with_concurrent_resume": round(ev[0].elapsed_time(ev[1]), 3)})
     pool.set_copy_blocks(0)
+    # lazy resume: no copy when the sessions resume (their pages are read in
+    # place from the cold tier), then promotion under a per-step page budget on a
+    # second stream while the 48 layers decode; versus the eager resume above
+    pool.set_spill(True)
+    lazy = {"budgets": []}
+    for per_step in (256, 1024, 4096):
+        sids = picks[k % len(picks)]
+        k += 1
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pool.resume_lazy(sids, stream=main_s)
+        lazy["host_ms_per_call"] = round(1e3 * (time.perf_counter() - t0), 3)
+        steps_needed, dec_ms, moved = 0, [], 0
+        while True:
+            side.wait_stream(main_s)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            n = pool.promote(per_step, stream=side)
+            ev[0].record(main_s)
+            decode48(main_s)
+            ev[1].record(main_s)
+            main_s.wait_stream(side)
+            torch.cuda.synchronize()
+            moved += n
+            if n == 0:
+                break
+            steps_needed += 1
+            dec_ms.append(ev[0].elapsed_time(ev[1]))
+        lazy["budgets"].append({"pages_per_step": per_step,
+                                "gb_per_step": round(per_step * pool.page_bytes / 1e9, 2),
+                                "decode48_ms_while_promoting": round(float(np.mean(dec_ms)), 3),
+                                "steps_to_promote": steps_needed, "pages_promoted": moved})
+        log("lazy resume: %s" % json.dumps(lazy["budgets"][-1]))
+        pool.evict(sids, stream=main_s)
+    pool.set_spill(False)
+    torch.cuda.synchronize()
     # partial residency: sessions paused with all pages resident, a fraction of
     # their pages evicted page by page (LRU; clean, so no cold writes), resumed
     partial = []
@@ -277,6 +312,7 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
         "decode48_GBps": round(48 * sum(decode_bytes(w.seq_lens, 32, 4, 128, 2)) / (decode_ms / 1e3) / 1e9, 1),
         "partial_residency": partial,
         "copy_budget": budget,
+        "lazy_resume": lazy,
     }
 
 

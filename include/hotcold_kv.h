@@ -257,6 +257,17 @@ int kv_pool_set_spill(kv_pool* pool, int32_t enable);
 int kv_promote_pages(kv_pool* pool, int32_t n, kv_stream_t stream, int32_t* promoted);
 
 /*
+ * Lazy resume (spill on): the PAUSED sessions become ACTIVE without any copy;
+ * their non-resident pages stay in the cold tier, named by KV_PAGE_COLD
+ * entries, and decode reads them in place until kv_promote_pages moves them.
+ * The paper fetches before decoding (Sec. III); with a cold tier as fast as
+ * HBM this spreads the fetch over later steps under the caller's copy budget
+ * instead of stalling the step that resumes.  Rows are rewritten on `stream`.
+ * Errors: KV_ERR_INVALID (spill off, bad or duplicate ids), KV_ERR_STATE.
+ */
+int kv_resume_sessions_lazy(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t stream);
+
+/*
  * Register a PAUSED session of seq_len tokens whose KV already sits in the given
  * cold pages (host array of ceil(seq_len / 16) distinct ids).  Cold pages may be
  * shared with other paused sessions: KV never changes once written (Sec. II), so

@@ -52,6 +52,8 @@ pressure instead of failing):
 * promote(n) moves up to n spilled pages of active sessions (session id order,
   logical page order) into hot pages, evicting paused pages by LRU if needed,
   since active pages are the more recently used.  Cold copies stay valid.
+* resume_lazy resumes without fetching: missing pages are read in place from
+  the cold tier and promoted later, so the copy work can be spread over steps.
 """
 
 from __future__ import annotations
@@ -341,6 +343,29 @@ class PoolModel:
             self.resumes += 1
             out.append(per)
         return out
+
+    def resume_lazy(self, sids: Sequence[int]) -> None:
+        """Resume without fetching: every non-resident page stays in the cold tier
+        (spilled, read in place) until promoted.  Needs the spill option.
+        Atomic as a whole."""
+        sids = [int(x) for x in sids]
+        if not self.spill:
+            raise ModelError(ERR_INVALID, "lazy resume needs spill")
+        if len(set(sids)) != len(sids):
+            raise ModelError(ERR_INVALID, "duplicate session")
+        for sid in sids:
+            if self._session(sid).state != PAUSED:
+                raise ModelError(ERR_STATE, "not paused")
+        for sid in sids:
+            s = self.sessions[sid]
+            missing = [i for i, p in enumerate(s.hot) if p < 0]
+            for i in missing:
+                s.spilled[i] = True
+            self.spilled_pages += len(missing)
+            self.resume_resident += len(s.hot) - len(missing)
+            self.resume_total += len(s.hot)
+            s.state = ACTIVE
+            self.resumes += 1
 
     def write_tokens(self, sid: int, tok_begin: int, n_tok: int) -> None:
         s = self._session(sid)

@@ -1106,6 +1106,54 @@ int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_
     return KV_OK;
 }
 
+int kv_resume_sessions_lazy(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t stream) {
+    if (!pool || (n > 0 && !sids) || n < 0) return fail(KV_ERR_INVALID, "bad arguments");
+    if (!pool->spill) return fail(KV_ERR_INVALID, "lazy resume needs spill on");
+    if (n == 0) return KV_OK;
+    std::vector<int32_t> ids(sids, sids + n);
+    {
+        std::vector<int32_t> sorted = ids;
+        std::sort(sorted.begin(), sorted.end());
+        if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end())
+            return fail(KV_ERR_INVALID, "duplicate session in batch");
+    }
+    for (int32_t sid : ids) {
+        Session* s = pool->session(sid);
+        if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
+        if (s->state != KV_SESSION_PAUSED) return fail(KV_ERR_STATE, "session %d is not paused", sid);
+    }
+    if (!pool->meta) {
+        DeviceGuard g(pool->d.device);
+        hipStream_t st = pool->strm(stream);
+        for (int32_t sid : ids) {
+            const Session& s = pool->sessions[sid];
+            std::vector<int32_t> row(s.hot.size());
+            for (size_t i = 0; i < s.hot.size(); ++i)
+                row[i] = s.hot[i] >= 0 ? s.hot[i] : (s.cold[i] | KV_PAGE_COLD);
+            int rc = pool->submit_row_at(sid, 0, row.data(), static_cast<int32_t>(row.size()), st);
+            if (rc) return rc;
+        }
+    }
+    for (int32_t sid : ids) {
+        Session& s = pool->sessions[sid];
+        int64_t resident = 0;
+        for (size_t i = 0; i < s.hot.size(); ++i) {
+            if (s.hot[i] >= 0) {
+                ++resident;
+            } else {
+                s.spilled[i] = 1;
+                pool->st.spilled_pages += 1;
+            }
+        }
+        pool->lru.erase(s.stamp);
+        s.state = KV_SESSION_ACTIVE;
+        pool->st.resume_pages_resident += resident;
+        pool->st.resume_pages_total += static_cast<int64_t>(s.hot.size());
+        pool->st.resumes += 1;
+    }
+    return KV_OK;
+}
+
 int kv_resume_session(kv_pool* pool, int32_t sid, kv_stream_t stream) {
     return kv_resume_sessions(pool, &sid, 1, stream);
 }

@@ -85,6 +85,7 @@ _SIGS = {
     "kv_evict_session": (ctypes.c_int, [_P, _I32, _P]),
     "kv_pool_set_spill": (ctypes.c_int, [_P, _I32]),
     "kv_promote_pages": (ctypes.c_int, [_P, _I32, _P, _PI32]),
+    "kv_resume_sessions_lazy": (ctypes.c_int, [_P, _PI32, _I32, _P]),
     "kv_pool_set_staging": (ctypes.c_int, [_P, _P, _SZ, _PI32]),
     "paged_decode_stage": (ctypes.c_int, [_P, _PI32, _I32, _P, _P, _PI32]),
     "paged_decode_prefetch": (ctypes.c_int, [_P, _I32, _P]),
@@ -230,6 +231,11 @@ def kv_promote_pages(pool: int, n: int, stream: int = 0) -> int:
     got = ctypes.c_int32()
     _check(_lib.kv_promote_pages(pool, n, stream or None, ctypes.byref(got)), "kv_promote_pages")
     return got.value
+
+
+def kv_resume_sessions_lazy(pool: int, sids: Sequence[int], stream: int = 0) -> None:
+    _check(_lib.kv_resume_sessions_lazy(pool, _i32_array(sids), len(sids), stream or None),
+           "kv_resume_sessions_lazy")
 
 
 def kv_pool_set_staging(pool: int, staging_ptr: int, nbytes: int) -> int:

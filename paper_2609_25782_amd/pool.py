@@ -115,6 +115,16 @@ class HotColdPool:
         else:
             kv.kv_resume_sessions(self.handle, list(sids), _stream(stream))
 
+    def resume_lazy(self, sids, stream=None) -> None:
+        kv.kv_resume_sessions_lazy(self.handle, [sids] if isinstance(sids, int) else list(sids),
+                                   _stream(stream))
+
+    def set_spill(self, enable: bool) -> None:
+        kv.kv_pool_set_spill(self.handle, enable)
+
+    def promote(self, n: int, stream=None) -> int:
+        return kv.kv_promote_pages(self.handle, int(n), _stream(stream))
+
     def set_copy_blocks(self, blocks: int) -> None:
         kv.kv_pool_set_copy_blocks(self.handle, int(blocks))
 

@@ -281,3 +281,53 @@ def test_promote_and_write_into_spilled_pages(dev):
     check()
     assert pool.stats()["promoted_pages"] == 10
     pool.close()
+
+
+@pytest.mark.parametrize("cold", COLD_TIERS)
+def test_lazy_resume_decodes_in_place_then_promotes(dev, cold):
+    """Lazy resume: no copy at resume, the rows name the cold pages and decode
+    reads them in place; promotion in budgeted chunks then moves them into HBM.
+    The page table follows the model after every call, decode matches the
+    oracle throughout, promoted pages equal their cold copies bit for bit."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    _say("lazy resume, cold tier in %s memory" % cold)
+    lens = [300, 170, 45]
+    n_pages = sum(synth.pages_for(L) for L in lens)
+    pool = _spilled_pool(dev, cold, lens, hot_pages=n_pages + 4)
+    model = PoolModel(n_pages + 4, n_pages + 8, len(lens) + 2, pool.stride, spill=True)
+    for L in lens:
+        model.create(L)
+    pool.evict([0, 1, 2])
+    model.evict_many([0, 1, 2])
+    st0 = pool.stats()
+    pool.resume_lazy([0, 1, 2])
+    model.resume_lazy([0, 1, 2])
+    assert pool.stats()["pages_to_hot"] == st0["pages_to_hot"]      # nothing copied
+    sids = torch.arange(3, dtype=torch.int32, device=dev)
+    sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+
+    def check():
+        torch.cuda.synchronize()
+        assert np.array_equal(pool.page_table.cpu().numpy(), np.array(model.table(), np.int32))
+        table = pool.gather_table(sids)
+        for layer in (0, 1):
+            case = _oracle(lens, layer)
+            got = to_host(pool.decode(layer, to_device(case.q, "bf16", dev), sl, page_table=table))
+            tolerance_check(got, case.oracle_out())
+
+    check()
+    moved = 0
+    while True:
+        n = pool.promote(7)
+        assert len(model.promote(7)) == n
+        moved += n
+        check()
+        if n == 0:
+            break
+    assert moved == n_pages and pool.stats()["cold_active_pages"] == 0
+    pb = pool.page_bytes
+    for sid in range(3):
+        _, _, hot, cold_ids = pool.info(sid)
+        for h, c in zip(hot, cold_ids):
+            assert torch.equal(pool.hot.view(-1, pb)[h].cpu(), pool.cold.view(-1, pb)[c].cpu())
+    pool.close()

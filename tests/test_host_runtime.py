@@ -46,7 +46,7 @@ def _same(kv, pool, model, ms):
 
 def _random_call(kv, pool, rng, nh, nc, ms, stride):
     """One random call as a (model call, library call) pair."""
-    op = int(rng.integers(0, 11))
+    op = int(rng.integers(0, 12))
     sid = int(rng.integers(-1, ms + 1))
     if op == 0:
         L = int(rng.integers(-2, 16 * stride + 20))
@@ -72,6 +72,9 @@ def _random_call(kv, pool, rng, nh, nc, ms, stride):
     if op == 8:
         new_len = int(rng.integers(0, 16 * stride + 20))
         return (lambda m: m.extend(sid, new_len)), (lambda: kv.kv_session_extend(pool, sid, new_len))
+    if op == 11:
+        sids = [int(x) for x in rng.integers(-1, ms + 1, size=int(rng.integers(1, 3)))]
+        return (lambda m: m.resume_lazy(sids)), (lambda: kv.kv_resume_sessions_lazy(pool, sids))
     if op == 10:
         n = int(rng.integers(0, 8))
         return (lambda m: len(m.promote(n))), (lambda: kv.kv_promote_pages(pool, n))

@@ -317,3 +317,21 @@ def test_spill_invariants_on_random_sequences(seed):
                     assert e == (h if h >= 0 else (c | C if sp else -1))
                     assert not (sp and h >= 0)
     assert spills > 20
+
+
+def test_lazy_resume_hand_worked():
+    """Lazy resume: nothing is fetched; missing pages are named in the cold tier
+    until promote moves them, lowest hot ids first."""
+    from oracle.pool_model import COLD_BIT as C
+    m = PoolModel(num_hot=6, num_cold=10, max_sessions=3, max_pages_per_session=4, spill=True)
+    a = m.create(16 * 3)                          # hot 0,1,2
+    m.evict(a)                                    # cold 0,1,2; hot free
+    m.resume([a]); m.pause(a)                     # resident again (hot 0,1,2), cold copies valid
+    assert m.evict_pages(2)[0] == 2               # pages 0,1 of a leave HBM (clean)
+    m.resume_lazy([a])
+    assert m.row(a) == [0 | C, 1 | C, 2, -1] and m.pages_to_hot == 3
+    assert (m.resume_resident, m.resume_total) == (0 + 1, 3 + 3) and m.spilled_pages == 2
+    assert m.promote(1) == [(0, 0)] and m.row(a) == [0, 1 | C, 2, -1]
+    assert m.promote(5) == [(1, 1)] and m.row(a) == [0, 1, 2, -1]
+    with pytest.raises(ModelError):
+        PoolModel(4, 4, 2, 2).resume_lazy([0])    # needs spill
