@@ -331,3 +331,36 @@ def test_lazy_resume_decodes_in_place_then_promotes(dev, cold):
         for h, c in zip(hot, cold_ids):
             assert torch.equal(pool.hot.view(-1, pb)[h].cpu(), pool.cold.view(-1, pb)[c].cpu())
     pool.close()
+
+
+def test_staging_error_paths(dev):
+    """Misuse of the staging calls fails with an error and leaves decode intact:
+    prefetch without a staging buffer, a misaligned buffer, a paused session in
+    the batch, a bad layer."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    pool = _spilled_pool(dev, "device", [100, 40], hot_pages=5)
+    for call, code in ((lambda: kv.paged_decode_prefetch(pool.handle, 0), kv.KV_ERR_INVALID),):
+        with pytest.raises(kv.KVError) as e:
+            call()
+        assert e.value.status == code
+    staging = torch.empty(2 * 8 * 16384 + 512, dtype=torch.uint8, device=dev)
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_pool_set_staging(pool.handle, staging.data_ptr() + 16, 2 * 8 * 16384)
+    assert e.value.status == kv.KV_ERR_INVALID
+    assert kv.kv_pool_set_staging(pool.handle, staging.data_ptr(), 2 * 8 * 16384) == 8
+    table = torch.empty((2, pool.stride), dtype=torch.int32, device=dev)
+    pool.pause(1)
+    with pytest.raises(kv.KVError) as e:
+        kv.paged_decode_stage(pool.handle, [0, 1], table.data_ptr())
+    assert e.value.status == kv.KV_ERR_STATE
+    with pytest.raises(kv.KVError) as e:
+        kv.paged_decode_prefetch(pool.handle, 2)
+    assert e.value.status == kv.KV_ERR_INVALID
+    assert kv.paged_decode_stage(pool.handle, [0], table.data_ptr()) == 2   # 7 pages, 5 hot
+    kv.paged_decode_prefetch(pool.handle, 1)
+    case = _oracle([100], 1)
+    got = to_host(pool.decode(1, to_device(case.q, "bf16", dev), torch.tensor([100], dtype=torch.int32, device=dev),
+                              page_table=table[:1]))
+    tolerance_check(got, case.oracle_out())
+    kv.kv_pool_set_staging(pool.handle, 0, 0)
+    pool.close()

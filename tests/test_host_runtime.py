@@ -152,3 +152,35 @@ def test_metadata_write_drops_cold_copies():
     st = kv.kv_pool_stats_get(pool)
     assert st["pages_to_cold"] == 5 and kv.kv_session_info(pool, a)[3] == [0, 1, 2]
     kv.kv_pool_destroy(pool)
+
+
+def test_spill_entry_points_error_codes():
+    """Errors of the spill entry points on a metadata-only pool, each leaving the
+    pool unchanged."""
+    kv = _lib()
+    pool = _meta_pool(kv, 4, 8, 3, 4)
+    a = kv.kv_session_create(pool, 32)
+    kv.kv_session_pause(pool, a)
+    before = _snapshot(kv, pool, 3)
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_resume_sessions_lazy(pool, [a])          # spill off
+    assert e.value.status == kv.KV_ERR_INVALID
+    assert kv._lib.kv_pool_set_spill(pool, 2) == kv.KV_ERR_INVALID   # the C call: 0 or 1 only
+    kv.kv_pool_set_spill(pool, True)
+    for bad, code in (([a, a], kv.KV_ERR_INVALID), ([7], kv.KV_ERR_INVALID), ([1], kv.KV_ERR_STATE)):
+        with pytest.raises(kv.KVError) as e:
+            kv.kv_resume_sessions_lazy(pool, bad)
+        assert e.value.status == code
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_promote_pages(pool, -1)
+    assert e.value.status == kv.KV_ERR_INVALID
+    assert _snapshot(kv, pool, 3) == before
+    for call in (lambda: kv.kv_pool_set_staging(pool, 0, 0),
+                 lambda: kv.paged_decode_stage(pool, [a], 0),
+                 lambda: kv.paged_decode_prefetch(pool, 0)):
+        with pytest.raises(kv.KVError) as e:           # no device pool
+            call()
+        assert e.value.status == kv.KV_ERR_INVALID
+    kv.kv_resume_sessions_lazy(pool, [a])              # all pages resident: nothing spills
+    assert kv.kv_pool_stats_get(pool)["spilled_pages"] == 0
+    kv.kv_pool_destroy(pool)
