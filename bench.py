@@ -117,7 +117,19 @@ def cpu_baseline(w, budget_s: float):
             log("cpu baseline: %d session decodes, %.1f s of oracle time" % (calls, spent))
         if spent >= budget_s:
             break
+    # the same oracle on one thread, over the first two sessions
+    t1_s, t1_bytes = 0.0, 0
+    for b in range(min(2, w.batch)):
+        pool, n, pt = packed[b]
+        L = int(w.seq_lens[b])
+        t0 = time.perf_counter()
+        oracle.paged_attention(pool, n, 1, hkv, d, oracle.BF16, 0, q_all[b:b + 1], pt,
+                               np.array([L], np.int32), 1.0 / math.sqrt(d), num_threads=1)
+        t1_s += time.perf_counter() - t0
+        t1_bytes += sum(decode_bytes([L], hq, hkv, d, 2))
+    log("cpu baseline: one thread, 2 sessions, %.1f s" % t1_s)
     return {"value": round(nbytes / spent / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "value_1_thread": round(t1_bytes / t1_s / 1e9, 4),
             "kind": "oracle",
             "sample": "fp64 C oracle (OpenMP over query heads): %d whole-session decodes cycling over "
                       "the workload's %d sessions (%.2f passes, %d tokens, all 32 query heads), %.1f s" % (
@@ -199,6 +211,20 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
     torch.cuda.synchronize()
     n_copy, copy_ms = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_PAGE_COPY)
     kv.kv_pool_set_profiling(pool.handle, False)
+    # one session resumed alone: events around the call
+    single = []
+    for j in range(3):
+        sid = picks[k][j]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(main_s)
+        pool.resume([sid], stream=main_s)
+        e1.record(main_s)
+        torch.cuda.synchronize()
+        single.append({"bytes": synth.pages_for(pool.info(sid)[1]) * pool.page_bytes,
+                       "ms": round(e0.elapsed_time(e1), 3)})
+        pool.evict([sid], stream=main_s)
+    k += 1
     # both at once: resumes on a second stream while the 48 layers decode
     e = [torch.cuda.Event(enable_timing=True) for _ in range(2 * steps)]
     torch.cuda.synchronize()
@@ -306,6 +332,7 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
         "copy_GBps": round(gbs, 1),
         "frac_of_copy_roofline": round(gbs / HBM_PEAK_GBS, 4),
         "host_ms_per_call": round(1e3 * host_s / steps, 3),
+        "single_session": single,
         "decode48_ms": round(decode_ms, 3),
         "decode48_ms_with_concurrent_resume": round(both_ms, 3),
         "tbt_impact": round(both_ms / decode_ms, 3),
@@ -435,6 +462,82 @@ def measure_agentic_replay(seed: int, plateau_s: float = 20.0):
     return out
 
 
+def _pct(xs):
+    xs = np.asarray(xs, dtype=np.float64)
+    return {"median": round(float(np.median(xs)), 3), "p10": round(float(np.percentile(xs, 10)), 3),
+            "p90": round(float(np.percentile(xs, 90)), 3)}
+
+
+def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
+    """Decode throughput on the other workloads: the tiny one (launch-bound), the
+    48-layer step (B=64, lognormal lengths, all 48 layers per step, ~170 GB) and
+    the skewed one (B=128, power-law lengths up to 256K, one layer timed, also
+    scaled to 48).  HIP events around each decode call (or each 48-layer step);
+    median, p10, p90.  Also the same run's device-to-device copy bandwidth, as
+    context for the 8 TB/s peak."""
+    import torch
+    import synth
+    from paper_2609_25782_amd.pool import HotColdPool
+    out = {}
+    dev = torch.device("cuda", 0)
+    for name, w in (("tiny", synth.config_tiny(seed)), ("step48", synth.config_step48(seed)),
+                    ("skewed", synth.config_skewed(seed))):
+        pool = HotColdPool(w.num_layers, w.num_kv_heads, w.head_dim, w.dtype, w.hot_pages, 0, w.batch,
+                           max(synth.pages_for(int(w.seq_lens.max())), 1))
+        mult = float(synth.value_multiplier(w.value_scale))
+        for b in range(w.batch):
+            pool.create_session(int(w.seq_lens[b]), [int(p) for p in w.placement[b]])
+            pool.fill_synthetic(b, b, w.seed, mult)
+        q_np = synth.queries(w.seed + 1, w.batch, w.num_q_heads, w.head_dim, w.value_scale, w.dtype)
+        if w.dtype == "bf16":
+            q = torch.from_numpy(q_np.view(np.int16)).to(dev).view(torch.bfloat16)
+        else:
+            q = torch.from_numpy(np.ascontiguousarray(q_np, dtype=np.float32)).to(dev)
+        seq = torch.from_numpy(w.seq_lens.copy()).to(dev)
+        pt = pool.page_table[:w.batch]
+        o = torch.empty_like(q)
+        layers = list(range(w.num_layers))
+        times = []
+        for it in range(warmup + steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for layer in layers:
+                pool.decode(layer, q, seq, page_table=pt, out=o)
+            e1.record()
+            torch.cuda.synchronize()
+            if it >= warmup:
+                times.append(1e3 * e0.elapsed_time(e1))
+        elt = 2 if w.dtype == "bf16" else 4
+        nbytes = len(layers) * sum(decode_bytes(w.seq_lens, w.num_q_heads, w.num_kv_heads, w.head_dim, elt))
+        med = float(np.median(times))
+        out[name] = {"workload": w.name, "batch": w.batch, "layers": len(layers),
+                     "tokens": int(w.seq_lens.sum()), "bytes_per_call": nbytes,
+                     "us_per_call": _pct(times), "GBps": round(nbytes / (med * 1e-6) / 1e9, 1),
+                     "pct_of_peak": round(100.0 * nbytes / (med * 1e-6) / 1e9 / HBM_PEAK_GBS, 2)}
+        if name == "skewed":
+            out[name]["scaled_to_48_layers_ms"] = round(48 * med / 1e3, 3)
+        log("configs: %s %s" % (name, json.dumps(out[name])))
+        pool.close()
+        del pool
+        torch.cuda.empty_cache()
+    a = torch.empty(2 ** 31, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    times = []
+    for it in range(8):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        b.copy_(a)
+        e1.record()
+        torch.cuda.synchronize()
+        if it >= 2:
+            times.append(e0.elapsed_time(e1))
+    out["context"] = {"dtod_copy_GBps": round(2 * a.numel() / (float(np.median(times)) / 1e3) / 1e9, 1),
+                      "note": "2 GiB device-to-device copy (torch), read + write bytes"}
+    del a, b
+    torch.cuda.empty_cache()
+    return out
+
+
 def measure_spill(seed: int, steps: int = 6, warmup: int = 2):
     """Decode from the cold tier: 32 active sessions of 4,096 tokens at the
     paper's shape (48 layers, 4 KV heads, 128, bf16; 32 query heads), 12 GiB of
@@ -522,14 +625,15 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--no-check", action="store_true", help="skip the sampled oracle check")
-    ap.add_argument("--sections", default="resume48,host,replay,spill",
+    ap.add_argument("--sections", default="resume48,host,replay,spill,configs",
                     help="measurements after the hot-path step, comma separated: resume48 (48-layer "
                          "resume mix, ~235 GB of HBM), host (pinned-host cold tier), replay (agentic "
-                         "replay on a device pool), spill (decode from the cold tier); 'none' for none")
+                         "replay on a device pool), spill (decode from the cold tier), configs (the "
+                         "tiny, 48-layer and skewed workloads); 'none' for none")
     ap.add_argument("--no-resume-mix", action="store_true", help="same as --sections none")
     args = ap.parse_args()
     sections = set() if args.no_resume_mix else {x for x in args.sections.split(",") if x and x != "none"}
-    unknown = sections - {"resume48", "host", "replay", "spill"}
+    unknown = sections - {"resume48", "host", "replay", "spill", "configs"}
     if unknown:
         ap.error("unknown sections: %s" % ", ".join(sorted(unknown)))
 
@@ -689,6 +793,7 @@ def main():
         "pct_of_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
         "decode_us": round(1e6 * dec_s, 2),
         "decode_call_us": round(1e3 * decode_ms, 2),
+        "decode_call_us_dist": _pct([1e3 * a.elapsed_time(b) for a, b in ev]),
         "decode_bytes": dec_bytes,
         "resume": {
             "ms_per_session": round(1e3 * res_s / R, 5),
@@ -726,6 +831,8 @@ def main():
         log("agentic replay: %s" % json.dumps(result["agentic_replay"]))
     if "spill" in sections:
         result["spill_decode"] = measure_spill(args.seed)
+    if "configs" in sections:
+        result["configs"] = measure_configs(args.seed)
     if args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
     print(json.dumps(result), flush=True)

@@ -496,21 +496,33 @@ __global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs 
 }
 
 // Merge the partials of one (b, g) for one query head and write its output row.
-// One wave per (b, g, h): the D/4 lanes of a lane group each own four output
-// dims, and the wave's lane groups take every kGroups-th partial; loads for
-// four partials are issued before any of them is merged, then the lane groups
-// are merged with cross-lane exchanges.
-template <int D, bool BF16>
+// The D/4 lanes of a lane group each own four output dims, and lane groups take
+// every stride-th partial; loads for four partials are issued before any of
+// them is merged.  Narrow: one wave per (b, g, h), four heads per block.  Wide
+// (many partials per segment, i.e. small batches): the block's four waves share
+// one (b, g, h) and merge their results through LDS.  The partials of a segment
+// are those of waves k_first..k_last when there are fewer waves than units, and
+// one per unit (the wave that owns it) otherwise.
+#ifndef HCK_WIDE_COMBINE_PIECES
+#define HCK_WIDE_COMBINE_PIECES 12
+#endif
+constexpr int kWideCombinePieces = HCK_WIDE_COMBINE_PIECES;
+
+template <int D, bool BF16, bool WIDE>
 __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArgs a) {
     constexpr int kQuads = D / 4;
     constexpr int kGroups = kWave / kQuads;
     constexpr int kUnroll = 4;
+    constexpr int kStride = WIDE ? kBlockWaves * kGroups : kGroups;
+    __shared__ float s_merge[WIDE ? kBlockWaves : 1][kQuads][6];
     const int seg = blockIdx.x;
-    const int h = blockIdx.y * kBlockWaves + threadIdx.x / kWave;
-    if (h >= a.group) return;
+    const int wave = threadIdx.x / kWave;
+    const int h = WIDE ? static_cast<int>(blockIdx.y) : static_cast<int>(blockIdx.y) * kBlockWaves + wave;
+    if (h >= a.group) return;  // never taken by a wide block: its grid has one block per head
     const int b = seg / a.num_kv_heads, g = seg % a.num_kv_heads;
     const int lane = threadIdx.x & (kWave - 1);
     const int quad = lane % kQuads, grp = lane / kQuads;
+    const int gid = WIDE ? wave * kGroups + grp : grp;
 
     int64_t before = 0, total = 0;
     for (int r = lane; r < a.batch; r += kWave) {
@@ -527,29 +539,26 @@ __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArg
     const bool invalid = L < 0 || static_cast<int64_t>(L) > kPageTokens * a.pt_stride;
     const int nb = row_pages(L, a.pt_stride);
     f32x4 res;
-    if (invalid) {
-        const float nan = __builtin_nanf("");
-        res = f32x4{nan, nan, nan, nan};
-    } else if (nb == 0) {
-        res = f32x4{0.f, 0.f, 0.f, 0.f};
-    } else {
+    float M = -INFINITY, den = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    if (!invalid && nb > 0) {
         const int64_t T = total * a.num_kv_heads;
         const int64_t u_a = before * a.num_kv_heads + static_cast<int64_t>(g) * nb;
-        const int64_t u_e = u_a + nb;
         const int N = a.waves;
         const int k_first = static_cast<int>(((u_a + 1) * N - 1) / T);
-        const int k_last = static_cast<int>((u_e * N - 1) / T);
-        float M = -INFINITY, den = 0.f;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int k0 = k_first + grp; k0 <= k_last; k0 += kUnroll * kGroups) {
+        const int k_last = static_cast<int>(((u_a + nb) * N - 1) / T);
+        const bool per_unit = N > T;  // every non-empty wave holds exactly one unit
+        const int count = per_unit ? nb : k_last - k_first + 1;
+        for (int i0 = gid; i0 < count; i0 += kUnroll * kStride) {
             float mk[kUnroll], lk[kUnroll];
             f32x4 ok[kUnroll];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
-                const int k = k0 + u * kGroups;
+                const int i = i0 + u * kStride;
+                const int k = per_unit ? static_cast<int>(((u_a + i + 1) * N - 1) / T) : k_first + i;
                 // waves whose own unit range is empty wrote nothing to their slot
-                const bool use = k <= k_last &&
-                                 static_cast<int64_t>(k) * T / N != static_cast<int64_t>(k + 1) * T / N;
+                const bool use = i < count &&
+                                 (per_unit || static_cast<int64_t>(k) * T / N != static_cast<int64_t>(k + 1) * T / N);
                 const int64_t slot = static_cast<int64_t>(use ? k : 0) + seg;
                 const float* pml = a.part_ml + slot * 2 * a.group;
                 const float m_raw = pml[h], l_raw = pml[a.group + h];
@@ -570,6 +579,30 @@ __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArg
             for (int j = 0; j < 4; ++j) acc2[j] = __shfl_xor(acc[j], off);
             lse_merge(M, den, acc, M2, den2, acc2);
         }
+    }
+    if constexpr (WIDE) {
+        // the block's waves took disjoint partials: merge their results in LDS
+        if (grp == 0) {
+            float* e = s_merge[wave][quad];
+            e[0] = M;
+            e[1] = den;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) e[2 + j] = acc[j];
+        }
+        __syncthreads();
+        if (wave != 0) return;
+#pragma unroll
+        for (int w = 1; w < kBlockWaves; ++w) {
+            const float* e = s_merge[w][quad];
+            lse_merge(M, den, acc, e[0], e[1], f32x4{e[2], e[3], e[4], e[5]});
+        }
+    }
+    if (invalid) {
+        const float nan = __builtin_nanf("");
+        res = f32x4{nan, nan, nan, nan};
+    } else if (nb == 0) {
+        res = f32x4{0.f, 0.f, 0.f, 0.f};
+    } else {
         res = acc / den;
     }
     if (grp == 0) {
@@ -610,13 +643,19 @@ const void* pick_split(int head_dim, int dtype, bool tiered) {
     return nullptr;
 }
 
-const void* pick_combine(int head_dim, int dtype) {
+template <int D, bool BF16>
+const void* combine_kernel_ptr(bool wide) {
+    return wide ? reinterpret_cast<const void*>(&decode_combine_kernel<D, BF16, true>)
+                : reinterpret_cast<const void*>(&decode_combine_kernel<D, BF16, false>);
+}
+
+const void* pick_combine(int head_dim, int dtype, bool wide) {
     if (dtype == kDtypeBf16) {
-        if (head_dim == 128) return reinterpret_cast<const void*>(&decode_combine_kernel<128, true>);
-        if (head_dim == 64) return reinterpret_cast<const void*>(&decode_combine_kernel<64, true>);
+        if (head_dim == 128) return combine_kernel_ptr<128, true>(wide);
+        if (head_dim == 64) return combine_kernel_ptr<64, true>(wide);
     } else {
-        if (head_dim == 128) return reinterpret_cast<const void*>(&decode_combine_kernel<128, false>);
-        if (head_dim == 64) return reinterpret_cast<const void*>(&decode_combine_kernel<64, false>);
+        if (head_dim == 128) return combine_kernel_ptr<128, false>(wide);
+        if (head_dim == 64) return combine_kernel_ptr<64, false>(wide);
     }
     return nullptr;
 }
@@ -634,13 +673,16 @@ hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hip
 }
 
 hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s) {
-    const void* k = pick_combine(head_dim, dtype);
-    if (!k) return hipErrorInvalidValue;
     const int segs = a.batch * a.num_kv_heads;
     if (segs == 0) return hipSuccess;
+    // Many partials per segment (waves well above segments): four waves per head.
+    const bool wide = static_cast<int64_t>(a.waves) >= static_cast<int64_t>(kWideCombinePieces) * segs;
+    const void* k = pick_combine(head_dim, dtype, wide);
+    if (!k) return hipErrorInvalidValue;
     void* args[] = {const_cast<DecodeArgs*>(&a)};
-    return hipLaunchKernel(k, dim3(segs, (a.group + kBlockWaves - 1) / kBlockWaves),
-                           dim3(kBlockThreads), args, 0, s);
+    const unsigned y = wide ? static_cast<unsigned>(a.group)
+                            : static_cast<unsigned>((a.group + kBlockWaves - 1) / kBlockWaves);
+    return hipLaunchKernel(k, dim3(segs, y), dim3(kBlockThreads), args, 0, s);
 }
 
 int decode_split_blocks_per_cu(int head_dim, int dtype, int batch) {
