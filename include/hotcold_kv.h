@@ -251,6 +251,11 @@ int kv_pool_set_spill(kv_pool* pool, int32_t enable);
  * when no hot page is free: active pages are the more recently used (Sec.
  * III).  Their cold copies stay valid.  *promoted (nullable) gets the number
  * moved; it is smaller than n when the hot tier is full of active pages.
+ * The row entries are rewritten on `stream` only after the copies, so a decode
+ * of the same sessions on another stream may run meanwhile: it reads each page
+ * either from its (unchanged) cold copy or from the finished hot copy.  The
+ * LRU victims evicted to make room are pages of paused sessions, which decode
+ * does not read.
  * Errors: KV_ERR_INVALID, KV_ERR_NO_COLD_PAGES (evicted pages need cold copies;
  * nothing changes).
  */

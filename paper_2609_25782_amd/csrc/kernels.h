@@ -93,6 +93,10 @@ hipError_t launch_slice_copy(const char* src_base, int64_t src_stride, char* dst
 
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t s);
 
+// page_table[e.pt_index] = e.pt_value for each of n entries with pt_index >= 0
+// (no copies): the second phase of a promotion.
+hipError_t launch_table_writes(const CopyEntry* entries, int32_t n, int32_t* page_table, hipStream_t s);
+
 struct SynthArgs {
     char* hot;
     char* cold;          // for rows naming spilled pages (KV_PAGE_COLD)

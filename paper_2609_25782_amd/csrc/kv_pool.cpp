@@ -334,6 +334,26 @@ struct kv_pool {
         return KV_OK;
     }
 
+    // Enqueue page-table element writes only (entries' pt_index / pt_value).
+    int submit_table_writes(const std::vector<hck::CopyEntry>& entries, hipStream_t s) {
+        for (size_t off = 0; off < entries.size(); off += kStagingEntries) {
+            const int32_t n = static_cast<int32_t>(std::min<size_t>(kStagingEntries, entries.size() - off));
+            StagingSlot* slot;
+            int rc = acquire_slot(&slot);
+            if (rc) return rc;
+            std::memcpy(slot->host, entries.data() + off, n * sizeof(hck::CopyEntry));
+            hipError_t e = hipMemcpyAsync(slot->dev, slot->host, n * sizeof(hck::CopyEntry),
+                                          hipMemcpyHostToDevice, s);
+            if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(table writes)");
+            e = hck::launch_table_writes(static_cast<const hck::CopyEntry*>(slot->dev), n, pt, s);
+            if (e != hipSuccess) return hip_fail(e, "table write launch");
+            e = hipEventRecord(slot->done, s);
+            if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
+            slot->pending = true;
+        }
+        return KV_OK;
+    }
+
     // Write `n` page ids into page-table row `sid` (entries 0..n-1).
     int submit_row(int32_t sid, const int32_t* vals, int32_t n, hipStream_t s) {
         if (n <= 0) return KV_OK;
@@ -933,15 +953,20 @@ int kv_promote_pages(kv_pool* pool, int32_t n, kv_stream_t stream, int32_t* prom
     if (!pool->meta && !a.pages.empty()) {
         DeviceGuard g(pool->d.device);
         hipStream_t st = pool->strm(stream);
-        std::vector<hck::CopyEntry> entries;
+        // Two phases: the copies, then (stream-ordered after them) the row
+        // entries.  A decode running meanwhile on another stream reads either
+        // the cold id (the cold copy stays valid) or a fully copied hot page.
+        std::vector<hck::CopyEntry> copies, writes;
         for (size_t k = 0; k < a.pages.size(); ++k) {
             const Victim& w = want[k];
-            entries.push_back(hck::CopyEntry{pool->sessions[w.sid].cold[w.page], a.pages[k],
-                                             w.sid * pool->d.max_pages_per_session + w.page, a.pages[k]});
+            copies.push_back(hck::CopyEntry{pool->sessions[w.sid].cold[w.page], a.pages[k], -1, 0});
+            writes.push_back(hck::CopyEntry{-1, -1, w.sid * pool->d.max_pages_per_session + w.page,
+                                            a.pages[k]});
         }
         rc = pool->order_after_frees(st);
         if (!rc) rc = pool->submit_victims(a, st);
-        if (!rc) rc = pool->submit_copies(pool->cold, pool->hot, entries, st, KV_KERNEL_PAGE_COPY);
+        if (!rc) rc = pool->submit_copies(pool->cold, pool->hot, copies, st, KV_KERNEL_PAGE_COPY);
+        if (!rc) rc = pool->submit_table_writes(writes, st);
         if (rc) return rc;
     }
     pool->commit_victims(a);

@@ -71,6 +71,15 @@ __global__ __launch_bounds__(kBlockThreads) void page_copy_kernel(
     }
 }
 
+__global__ __launch_bounds__(kBlockThreads) void table_writes_kernel(const CopyEntry* __restrict__ entries,
+                                                                     int32_t n, int32_t* page_table) {
+    for (int32_t i = static_cast<int32_t>(blockIdx.x * kBlockThreads + threadIdx.x); i < n;
+         i += static_cast<int32_t>(gridDim.x * kBlockThreads)) {
+        const CopyEntry e = entries[i];
+        if (e.pt_index >= 0) page_table[e.pt_index] = e.pt_value;
+    }
+}
+
 __global__ __launch_bounds__(kBlockThreads) void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; i < n;
          i += static_cast<int64_t>(gridDim.x) * kBlockThreads)
@@ -274,6 +283,13 @@ hipError_t launch_slice_copy(const char* src_base, int64_t src_stride, char* dst
         case 2: hipLaunchKernelGGL(page_copy_kernel<2>, grid, block, 0, s, src_base, src_stride, dst_base, dst_stride, entries, n, cpp, page_table); break;
         default: hipLaunchKernelGGL(page_copy_kernel<1>, grid, block, 0, s, src_base, src_stride, dst_base, dst_stride, entries, n, cpp, page_table); break;
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_table_writes(const CopyEntry* entries, int32_t n, int32_t* page_table, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(table_writes_kernel, dim3(grid_for(n, 1024)), dim3(kBlockThreads), 0, s, entries, n,
+                       page_table);
     return hipGetLastError();
 }
 

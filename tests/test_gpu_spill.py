@@ -364,3 +364,40 @@ def test_staging_error_paths(dev):
     tolerance_check(got, case.oracle_out())
     kv.kv_pool_set_staging(pool.handle, 0, 0)
     pool.close()
+
+
+def test_promotion_concurrent_with_decode(dev):
+    """Promotion on a second stream while the same sessions decode on the first:
+    rows are rewritten only after the copies, so every decode reads each page
+    either from its cold copy or from a finished hot copy, and its output is
+    bit-identical to the decode with every page cold (decode does not depend on
+    where a page lives)."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    lens = [400, 260, 333, 515]
+    n_pages = sum(synth.pages_for(L) for L in lens)
+    pool = _spilled_pool(dev, "device", lens, hot_pages=n_pages + 4)
+    sids = list(range(len(lens)))
+    pool.evict(sids)
+    pool.resume_lazy(sids)
+    sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+    sid_t = torch.tensor(sids, dtype=torch.int32, device=dev)
+    case = _oracle(lens, 1)
+    q = to_device(case.q, "bf16", dev)
+    ref = pool.decode(1, q, sl, page_table=pool.gather_table(sid_t)).clone()
+    torch.cuda.synchronize()
+    tolerance_check(to_host(ref), case.oracle_out())
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    outs, moved = [], 0
+    for it in range(40):
+        side.wait_stream(main)
+        n = pool.promote(3, stream=side)          # copies, then row entries, on `side`
+        table = pool.gather_table(sid_t)          # on `main`, concurrently
+        outs.append(pool.decode(1, q, sl, page_table=table).clone())
+        main.wait_stream(side)
+        moved += n
+    torch.cuda.synchronize()
+    assert moved == n_pages and pool.stats()["cold_active_pages"] == 0
+    for o in outs:
+        assert torch.equal(o, ref)
+    pool.close()
