@@ -520,6 +520,7 @@ def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
         pool.close()
         del pool
         torch.cuda.empty_cache()
+    out["graph_step48"] = measure_graph(seed)
     a = torch.empty(2 ** 31, dtype=torch.uint8, device=dev)
     b = torch.empty_like(a)
     times = []
@@ -536,6 +537,63 @@ def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
     del a, b
     torch.cuda.empty_cache()
     return out
+
+
+def measure_graph(seed: int, steps: int = 10, warmup: int = 3):
+    """A 48-layer decode step launched eagerly (96 launches from the host) and as
+    a captured HIP graph replayed, for a small batch (launch-bound) and a large
+    one (bandwidth-bound).  HIP events around each step; medians."""
+    import torch
+    import synth
+    from paper_2609_25782_amd.pool import HotColdPool
+    rows = []
+    for B, L in ((8, 2048), (8, 8192), (32, 8192)):
+        pages = B * synth.pages_for(L)
+        pool = HotColdPool(48, 4, 128, "bf16", pages, 0, B, synth.pages_for(L))
+        for b in range(B):
+            pool.create_session(L)
+            pool.fill_synthetic(b, b, seed, float(synth.value_multiplier(1.0 / math.sqrt(128))))
+        q = torch.randn(B, 32, 128, generator=torch.Generator().manual_seed(seed)).to(torch.bfloat16).cuda()
+        sl = torch.full((B,), L, dtype=torch.int32, device="cuda")
+        pt = pool.page_table[:B]
+        outs = [torch.empty_like(q) for _ in range(48)]
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+
+        def step():
+            for layer in range(48):
+                pool.decode(layer, q, sl, page_table=pt, out=outs[layer], stream=s)
+
+        with torch.cuda.stream(s):
+            step()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            step()
+        res = {}
+        for mode, fn in (("eager", step), ("graph", g.replay)):
+            times = []
+            for it in range(warmup + steps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                with torch.cuda.stream(s):
+                    e0.record(s)
+                    fn()
+                    e1.record(s)
+                torch.cuda.synchronize()
+                if it >= warmup:
+                    times.append(e0.elapsed_time(e1))
+            res[mode] = float(np.median(times))
+        nbytes = 48 * sum(decode_bytes([L] * B, 32, 4, 128, 2))
+        rows.append({"batch": B, "seq_len": L, "eager_ms": round(res["eager"], 3),
+                     "graph_ms": round(res["graph"], 3),
+                     "graph_GBps": round(nbytes / (res["graph"] / 1e3) / 1e9, 1),
+                     "speedup": round(res["eager"] / res["graph"], 3)})
+        log("graph: %s" % json.dumps(rows[-1]))
+        del g
+        pool.close()
+        del pool
+        torch.cuda.empty_cache()
+    return rows
 
 
 def measure_spill(seed: int, steps: int = 6, warmup: int = 2):

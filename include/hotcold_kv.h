@@ -473,7 +473,11 @@ size_t paged_decode_workspace_bytes(const kv_pool* pool, int32_t batch, int32_t 
  * Only tokens [0, L) are read: other slots of the tail page and pages past
  * ceil(L / 16) may hold anything, NaN included.
  * Decode calls of one pool are ordered with each other across streams (they
- * share the pool's small arrival-counter array).
+ * share the pool's small arrival-counter array).  A call made while `stream`
+ * is being captured into a HIP graph launches its two kernels and nothing
+ * else (no events, no profiling); capture needs the separate merge and no
+ * staged entries (KV_ERR_INVALID otherwise).  Replays read the pool as it is
+ * then: q, seq_lens and the page table may change between replays.
  * Numerics: bf16 or float32 inputs, float32 accumulation, scores and weights in
  * float32 (bf16 pools round the softmax weights to bf16 for the weighted sum of
  * V and use the same rounded weights in the normaliser).  The result does not

@@ -1279,8 +1279,16 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
         a.num_stage_slots = static_cast<int32_t>(pool->plan.size());
     }
     hipStream_t st = pool->strm(stream);
-    // decode calls of one pool share its counters: order them across streams
-    if (pool->decode_pending) {
+    // Under stream capture (a HIP graph of decode steps) the call launches its
+    // two kernels only: no pool events, which belong to eager cross-stream use.
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    hipError_t ce = hipStreamIsCapturing(st, &cap);
+    if (ce != hipSuccess) return hip_fail(ce, "hipStreamIsCapturing");
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    if (capturing && (a.fused || staged))
+        return fail(KV_ERR_INVALID, "graph capture supports the separate merge without staged pages");
+    // decode calls of one pool share its counters (fused merge): order them across streams
+    if (pool->decode_pending && !capturing) {
         hipError_t w = hipStreamWaitEvent(st, pool->decode_event, 0);
         if (w != hipSuccess) return hip_fail(w, "hipStreamWaitEvent(decode)");
     }
@@ -1288,16 +1296,17 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
         hipError_t w = hipStreamWaitEvent(st, pool->half_ready[half], 0);
         if (w != hipSuccess) return hip_fail(w, "hipStreamWaitEvent(staging)");
     }
-    hipEvent_t p = pool->prof_begin(st);
+    hipEvent_t p = capturing ? nullptr : pool->prof_begin(st);
     hipError_t e = hck::launch_decode_split(a, pool->d.head_dim, pool->d.dtype, st);
     pool->prof_end(KV_KERNEL_DECODE_SPLIT, p, st);
     if (e != hipSuccess) return hip_fail(e, "decode split launch");
     if (!a.fused) {
-        p = pool->prof_begin(st);
+        p = capturing ? nullptr : pool->prof_begin(st);
         e = hck::launch_decode_combine(a, pool->d.head_dim, pool->d.dtype, st);
         pool->prof_end(KV_KERNEL_DECODE_COMBINE, p, st);
         if (e != hipSuccess) return hip_fail(e, "decode combine launch");
     }
+    if (capturing) return KV_OK;
     e = hipEventRecord(pool->decode_event, st);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord(decode)");
     pool->decode_pending = true;
