@@ -532,9 +532,23 @@ def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
         torch.cuda.synchronize()
         if it >= 2:
             times.append(e0.elapsed_time(e1))
-    out["context"] = {"dtod_copy_GBps": round(2 * a.numel() / (float(np.median(times)) / 1e3) / 1e9, 1),
-                      "note": "2 GiB device-to-device copy (torch), read + write bytes"}
-    del a, b
+    dtod = 2 * a.numel() / (float(np.median(times)) / 1e3) / 1e9
+    del b
+    x = a.view(torch.bfloat16)
+    times = []
+    for it in range(8):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        torch.sum(x, dtype=torch.float32)
+        e1.record()
+        torch.cuda.synchronize()
+        if it >= 2:
+            times.append(e0.elapsed_time(e1))
+    out["context"] = {"dtod_copy_GBps": round(dtod, 1),
+                      "streaming_read_GBps": round(a.numel() / (float(np.median(times)) / 1e3) / 1e9, 1),
+                      "note": "2 GiB device-to-device copy (torch; read + write bytes) and a torch sum "
+                              "over the same 2 GiB (read bytes), same run"}
+    del a, x
     torch.cuda.empty_cache()
     return out
 
