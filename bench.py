@@ -710,8 +710,9 @@ def main():
         ap.error("unknown sections: %s" % ", ".join(sorted(unknown)))
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(each GPU would own its own sessions; see the design notes).", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(sharded by session, each GPU would own its own sessions and page tables).",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch

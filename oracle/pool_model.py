@@ -19,7 +19,7 @@ Policy being modelled (paper Sec. III):
   resident are not fetched, and the share found resident is the resume hit
   rate (Sec. III, "Eviction, resume and decode"; Sec. IV, Methodology).
 
-Readings where the paper is silent (each is stated in the design notes):
+Readings where the paper is silent:
 
 * Hot and cold pages are handed out lowest id first; pages needed by one call
   go to its sessions in argument order and logical page order; session ids are
