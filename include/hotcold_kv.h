@@ -4,8 +4,8 @@
  * The paper ("Hot-Cold Tiering of HBM and High Bandwidth Flash for Agentic LLM
  * Serving") splits the KV cache of agentic sessions into a hot set, the KV of
  * sessions that are decoding and that every decode step reads (Sec. I; Sec. II,
- * "Agentic AI Serving"), and a cold pool, the KV of paused sessions, read only
- * when a session resumes.  The hot set lives in the fast tier; the cold pool in
+ * "Agentic AI Serving"), and a cold pool holding what paused sessions have
+ * written, read only when a session resumes.  The hot set lives in the fast tier; the cold pool in
  * a capacity tier (Sec. III, first paragraph).  This library implements the
  * data-parallel part of that hierarchy on one GPU:
  *
@@ -229,8 +229,8 @@ int kv_evict_pages(kv_pool* pool, int32_t n, kv_stream_t stream, int32_t* evicte
 
 /*
  * Spill (enable = 1; off by default).  The paper does not pin active KV in HBM:
- * when the active set alone outgrows it, blocks spill to the capacity tier
- * instead of the call failing (Sec. III, "Eviction, resume and decode").  With
+ * if HBM cannot hold even the decoding sessions' KV, blocks move to the
+ * capacity tier instead of the call failing (Sec. III, "Eviction, resume and decode").  With
  * spill on, an allocating call that finds too few hot pages even after
  * evicting every resident page of paused sessions places the remaining new
  * pages in fresh cold pages (kv_session_create, kv_session_extend; hot pages

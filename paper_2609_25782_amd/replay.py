@@ -529,7 +529,7 @@ class Replay:
         write_bps = d["pages_to_cold"] * pb / secs
         fetch_bps = d["pages_to_hot"] * pb / secs
         produced_bps = self.produced_tokens * cfg.token_bytes / secs
-        hot_read_bps = active_pages * pb / cfg.step_s        # decode reads the hot set every step
+        hot_read_bps = active_pages * pb / cfg.step_s        # every step's decode reads all active KV
         per_session = live_pages * pb / live if live else 0.0
         miss_bytes = d["pages_to_hot"] * pb / d["resumes"] if d["resumes"] else 0.0
         e_hbm, e_fl = cfg.hbm_pj_per_bit, cfg.flash_pj_per_bit
