@@ -286,11 +286,12 @@ class PoolModel:
         if dirty > len(self.cold_free):
             raise ModelError(ERR_NO_COLD, "cold pool exhausted")
         copies = []
+        fresh = iter(self._lowest(self.cold_free, dirty))  # lowest first, in call and page order
         for sid in sids:
             s = self.sessions[sid]
             for i in range(len(s.hot)):
                 if s.cold[i] < 0:
-                    c = self._lowest(self.cold_free, 1)[0]
+                    c = next(fresh)
                     self.cold_free.remove(c)
                     self.cold_ref[c] = 1
                     s.cold[i] = c

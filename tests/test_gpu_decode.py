@@ -263,3 +263,26 @@ def test_repeated_calls_and_batch_changes_are_consistent(dev):
     torch.cuda.synchronize()
     tolerance_check(first, case.oracle_out())
     pool.close()
+
+
+def test_maximum_batch_and_full_rows(dev):
+    """The largest batch the decode kernels take (8,192 rows) with ragged
+    lengths of 1 to 48 tokens; the longest rows fill their page-table row (3
+    pages) exactly.  Every row against the oracle; one row more is refused."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    rng = np.random.default_rng(11)
+    lens = [int(x) for x in rng.integers(1, 49, size=8192)]
+    lens[0] = lens[-1] = 48
+    case = Case(1, 4, 1, 64, "bf16", lens, seed=11, extra_stride=0)
+    assert case.stride == 3
+    pool = build_gpu(case, dev)
+    q = to_device(case.q, "bf16", dev)
+    sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+    got = to_host(pool.decode(0, q, sl))
+    torch.cuda.synchronize()
+    tolerance_check(got, case.oracle_out())
+    with pytest.raises(kv.KVError) as e:
+        kv.paged_decode_attention(pool.handle, 0, q.data_ptr(), pool.page_table.data_ptr(), pool.stride,
+                                  sl.data_ptr(), 8193, 4, 0.125, q.data_ptr(), q.data_ptr(), 1 << 20, 0)
+    assert e.value.status == kv.KV_ERR_INVALID
+    pool.close()

@@ -390,3 +390,31 @@ def test_partial_residency_round_trip(dev, cold):
     assert np.array_equal(before, after)
     pool.destroy_session(filler)
     pool.close()
+
+
+def test_copy_lists_larger_than_one_staging_slot(dev):
+    """One eviction and one resume of 80,000 pages (two sessions of 40,000): the
+    copy list spans two staging slots and two launches.  Page tables follow the
+    model; every resumed page equals its cold copy."""
+    from paper_2609_25782_amd.pool import HotColdPool
+    n = 40000
+    pool = HotColdPool(1, 1, 64, "bf16", 2 * n + 100, 2 * n + 10, 3, n)
+    model = PoolModel(2 * n + 100, 2 * n + 10, 3, n)
+    for b in range(2):
+        assert pool.create_session(16 * n) == model.create(16 * n) == b
+        pool.fill_synthetic(b, b, 3, 1.0)
+    pool.evict([0, 1])
+    model.evict_many([0, 1])
+    blocker = pool.create_session(16 * 90)        # the resume lands on other hot pages
+    assert blocker == model.create(16 * 90)
+    pool.resume([1, 0])
+    model.resume([1, 0])
+    torch.cuda.synchronize()
+    _check_table(pool, model)
+    pb = pool.page_bytes
+    for sid in (0, 1):
+        st, L, hot, cold = pool.info(sid)
+        h = torch.tensor(hot, dtype=torch.long, device=dev)
+        c = torch.tensor(cold, dtype=torch.long, device=dev)
+        assert torch.equal(pool.hot.view(-1, pb).index_select(0, h), pool.cold.view(-1, pb).index_select(0, c))
+    pool.close()
