@@ -694,6 +694,9 @@ def main():
     ap.add_argument("--waves", type=int, default=0, help="override the decode wave count")
     ap.add_argument("--combine", choices=["fused", "separate"], default="separate",
                     help="merge split partials in the split kernel's last wave or in a second kernel")
+    ap.add_argument("--compute", choices=["matrix", "vector"], default="matrix",
+                    help="units the decode split kernel computes on: matrix cores, or bf16 dot2 on "
+                         "the vector ALU")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--no-check", action="store_true", help="skip the sampled oracle check")
@@ -752,6 +755,7 @@ def main():
     if args.waves:
         pool.set_waves(args.waves)
     pool.set_combine(args.combine == "fused")
+    pool.set_compute(args.compute == "vector")
 
     q = torch.from_numpy(synth.queries(w.seed + 1, w.batch, w.num_q_heads, w.head_dim,
                                        w.value_scale, "bf16").view(np.int16)).to(dev).view(torch.bfloat16)
@@ -828,6 +832,38 @@ def main():
         "resume copy %.1f us" % (args.steps, total_ms / args.steps, 1e3 * decode_ms, 1e3 * ms1 / n1,
                                  1e3 * ms2 / max(n2, 1), 1e3 * ms3 / n3))
 
+    # The same steps with the split's two products on the vector ALU instead of
+    # the matrix cores (same work split, loads and merge): the measured case for
+    # matrix cores.  Split-kernel time on the default grid and on 8 waves per CU
+    # (two per SIMD, which the vector form's registers allow and which suits it
+    # best); each output is compared with the matrix-core result of the same step.
+    other = None
+    if args.compute == "matrix" and args.combine == "separate" and not args.waves:
+        ref_out = out.float().clone()
+        cus = torch.cuda.get_device_properties(dev).multi_processor_count
+        pool.set_compute(True)
+        other = {"matrix_split_us": round(1e3 * ms1 / n1, 2), "matrix_waves": pool.waves()}
+        for tag, nw in (("same_grid", 0), ("two_waves_per_simd", 8 * cus)):
+            pool.set_waves(nw)
+            for i in range(args.warmup):
+                step()
+            kv.kv_pool_set_profiling(pool.handle, True)
+            for k in range(kv.KV_KERNEL_COUNT):
+                kv.kv_pool_profile_read(pool.handle, k)
+            for i in range(args.steps):
+                step()
+            torch.cuda.synchronize()
+            nv, msv = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_DECODE_SPLIT)
+            kv.kv_pool_set_profiling(pool.handle, False)
+            diff = float((out.float() - ref_out).abs().max() / ref_out.abs().max())
+            other[tag] = {"waves": pool.waves(), "split_us": round(1e3 * msv / nv, 2),
+                          "time_vs_matrix": round((msv / nv) / (ms1 / n1), 4),
+                          "max_normalised_diff_vs_matrix": diff}
+            log("vector-ALU split, %d waves: %.1f us (matrix cores %.1f us), normalised difference %.3g"
+                % (pool.waves(), 1e3 * msv / nv, 1e3 * ms1 / n1, diff))
+        pool.set_compute(False)
+        pool.set_waves(0)
+
     kvb, qo, ptb = decode_bytes(w.seq_lens, w.num_q_heads, w.num_kv_heads, w.head_dim, 2)
     dec_bytes = kvb + qo + ptb
     dec_s = (ms1 + ms2) / 1e3 / args.steps     # device time of the two decode kernels
@@ -861,6 +897,7 @@ def main():
             "batch": w.batch, "total_tokens": int(w.seq_lens.sum()), "num_q_heads": w.num_q_heads,
             "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "layers": 1, "page_tokens": 16,
             "hot_pages": num_hot, "decode_waves": pool.waves(), "combine": args.combine,
+            "compute": args.compute,
             "seed": args.seed,
         },
         "pct_of_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
@@ -884,11 +921,12 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(k1_gbs / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic() if args.combine == "separate" else None,
+            "traffic": measured_traffic() if args.combine == "separate" and args.compute == "matrix" else None,
             "bytes_per_launch": k1_bytes,
             "us_per_launch": round(1e6 * k1_s, 2),
         },
         "check": check,
+        "split_on_vector_alu": other,
     }
     pool.close()
     del pool

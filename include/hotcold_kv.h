@@ -395,6 +395,18 @@ enum kv_combine_mode {
  * bit; each mode on its own is deterministic. */
 int kv_pool_set_decode_combine(kv_pool* pool, int32_t mode);
 
+enum kv_decode_compute {
+    KV_DECODE_MATRIX = 0, /* both products on the matrix cores (default) */
+    KV_DECODE_VECTOR = 1  /* both products as bf16 dot2 on the vector ALU, with the same work
+                             split, page loads and partial format; bf16 pools, at most 8 query
+                             heads per KV head, separate merge only */
+};
+/* Which units the decode split kernel computes on.  The vector form exists to
+ * measure the matrix-core choice; the two sum in different orders, so their
+ * results agree to float32 rounding, not bit for bit.  Decode calls that the
+ * vector form cannot serve return KV_ERR_INVALID. */
+int kv_pool_set_decode_compute(kv_pool* pool, int32_t mode);
+
 /*
  * The page table of a decode batch: row i of `table` (device int32
  * [n][max_pages_per_session]) becomes the pool's row for session sids[i]

@@ -463,7 +463,258 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
     }
 }
 
-template <int D, bool BF16, int R, bool TIERED>
+// ---------------------------------------------------------------------------
+// Vector-ALU variant (bf16, at most 8 query heads per KV head).  Same work
+// split, page loads, partial format and combine as the matrix-core path; both
+// products run as v_dot2_f32_bf16 instead.  It exists to measure the choice of
+// matrix cores on the same memory schedule.
+//
+// Scores: lane (t = l % 16, qq = l / 16) holds a quarter of token t's dims (the
+// K loads are shared with the matrix-core path), so it forms partial dot
+// products for all 8 head slots from the group's queries in LDS, and a
+// reduce-scatter over the quarters leaves lane (t, qq) with the full scores of
+// heads 2 qq and 2 qq + 1.  The bf16 weights cross to the output layout through
+// 256 bytes of LDS.  Output: lane (dl, qg) holds dims 16 c + dl of tokens
+// 4 qg .. 4 qg + 3 for every chunk c (the V loads of the matrix-core path) and
+// accumulates all 8 head slots over its tokens; the four token quarters are
+// summed once per piece.
+constexpr int kValuMaxGroup = 8;
+
+template <int D>
+struct ValuLds {
+    u32x4 q[(D / 8) * kValuMaxGroup];  // [load i][head][quarter qq]: dims 8 (4 i + qq) .. + 7
+    unsigned p[kPageTokens * 4];       // [token][qq]: bf16 weights of heads 2 qq, 2 qq + 1
+};
+
+template <int D>
+struct ValuState {
+    float o[kValuMaxGroup][D / 16];  // lane (dl, qg): head h, dim 16 c + dl, over tokens 4 qg .. + 3
+    float m[2], l[2];                // lane (t, qq): heads 2 qq + e; l over token t only
+};
+
+// Order this wave's LDS accesses: earlier writes complete before later reads,
+// and the compiler moves no LDS access across it.
+__device__ __forceinline__ void wave_lds_sync() { __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ float dot2_bf16(unsigned a, unsigned b, float c) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c,
+                                           false);
+}
+
+__device__ __forceinline__ float readlane_f(float x, int lane) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
+}
+
+template <int D>
+__device__ __forceinline__ void compute_page_valu(ValuState<D>& st, PageRegs<D, true>& pg, int valid,
+                                                  float scale_log2, int lane, ValuLds<D>& sm) {
+    using S = Shape<D, true>;
+    const int t = lane & 15, qq = lane >> 4, qg = lane >> 4;
+    // partial scores of token t over this lane's dims, all 8 head slots
+    float s[kValuMaxGroup];
+#pragma unroll
+    for (int h = 0; h < kValuMaxGroup; ++h) s[h] = 0.f;
+#pragma unroll
+    for (int i = 0; i < S::kKLoads; ++i) {
+#pragma unroll
+        for (int h = 0; h < kValuMaxGroup; ++h) {
+            const u32x4 qv = sm.q[(i * kValuMaxGroup + h) * 4 + qq];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) s[h] = dot2_bf16(pg.k[i][j], qv[j], s[h]);
+        }
+    }
+    // reduce-scatter over the quarters: lanes l and l ^ 32 split heads 0-3 / 4-7,
+    // then lanes l and l ^ 16 split each half in pairs
+    const bool upper = lane >= 32, odd = (lane & 16) != 0;
+    float k4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const float send = upper ? s[j] : s[4 + j];
+        k4[j] = (upper ? s[4 + j] : s[j]) + __shfl_xor(send, 32);
+    }
+    float sh[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const float send = odd ? k4[e] : k4[2 + e];
+        sh[e] = (odd ? k4[2 + e] : k4[e]) + __shfl_xor(send, 16);
+    }
+    // online softmax for heads 2 qq + e at token t (same lazy rescale as above)
+#pragma unroll
+    for (int e = 0; e < 2; ++e) sh[e] = t < valid ? sh[e] * scale_log2 : -INFINITY;
+    if (__builtin_amdgcn_ballot_w64(sh[0] > st.m[0] || sh[1] > st.m[1])) {
+        float mx[2] = {sh[0], sh[1]};
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1)
+#pragma unroll
+            for (int e = 0; e < 2; ++e) mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], o));
+        float alpha[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const float mn = fmaxf(st.m[e], mx[e]);
+            alpha[e] = __builtin_amdgcn_exp2f(st.m[e] - mn);
+            st.l[e] *= alpha[e];
+            st.m[e] = mn;
+        }
+#pragma unroll
+        for (int h = 0; h < kValuMaxGroup; ++h) {
+            const float ah = readlane_f(alpha[h & 1], 16 * (h >> 1));
+#pragma unroll
+            for (int c = 0; c < S::kChunks; ++c) st.o[h][c] *= ah;
+        }
+    }
+    __bf16 pb[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        pb[e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(sh[e] - st.m[e]));
+        st.l[e] += static_cast<float>(pb[e]);
+    }
+    sm.p[t * 4 + qq] = static_cast<unsigned>(__builtin_bit_cast(unsigned short, pb[0])) |
+                       (static_cast<unsigned>(__builtin_bit_cast(unsigned short, pb[1])) << 16);
+    wave_lds_sync();
+    // w[j][hp] = weights of heads 2 hp, 2 hp + 1 at token 4 qg + j
+    u32x4 w[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w[j] = *reinterpret_cast<const u32x4*>(sm.p + 4 * (4 * qg + j));
+    unsigned p01[kValuMaxGroup], p23[kValuMaxGroup];
+#pragma unroll
+    for (int hp = 0; hp < 4; ++hp) {
+        p01[2 * hp] = (w[0][hp] & 0xFFFFu) | (w[1][hp] << 16);
+        p01[2 * hp + 1] = (w[0][hp] >> 16) | (w[1][hp] & 0xFFFF0000u);
+        p23[2 * hp] = (w[2][hp] & 0xFFFFu) | (w[3][hp] << 16);
+        p23[2 * hp + 1] = (w[2][hp] >> 16) | (w[3][hp] & 0xFFFF0000u);
+    }
+    if (valid < kPageTokens) mask_v<D, true>(pg, valid, qg);
+#pragma unroll
+    for (int c = 0; c < S::kChunks; ++c)
+#pragma unroll
+        for (int h = 0; h < kValuMaxGroup; ++h) {
+            st.o[h][c] = dot2_bf16(pg.v[c][0], p01[h], st.o[h][c]);
+            st.o[h][c] = dot2_bf16(pg.v[c][1], p23[h], st.o[h][c]);
+        }
+    __asm__ volatile("" ::: "memory");  // the next page's weight writes stay after these reads
+}
+
+template <int D, int R, bool TIERED>
+__device__ void run_piece_valu(const DecodeArgs& a, const Piece& pc, int nb, int seq_len, int lane,
+                               ValuLds<D>& sm) {
+    using S = Shape<D, true>;
+    constexpr int kGroups = D / 8;
+    // the group's queries (zero beyond `group` heads) into LDS
+    wave_lds_sync();  // the previous piece's reads are done
+    {
+        const __bf16* qrow = static_cast<const __bf16*>(a.q) +
+                             (static_cast<int64_t>(pc.b) * a.num_q_heads + pc.g * a.group) * D;
+        for (int e = lane; e < kGroups * kValuMaxGroup; e += kWave) {
+            const int h = e / kGroups, grp = e % kGroups;
+            const u32x4 v = h < a.group ? *reinterpret_cast<const u32x4*>(qrow + h * D + 8 * grp)
+                                        : u32x4{0u, 0u, 0u, 0u};
+            sm.q[((grp >> 2) * kValuMaxGroup + h) * 4 + (grp & 3)] = v;
+        }
+    }
+    wave_lds_sync();
+    ValuState<D> st;
+#pragma unroll
+    for (int h = 0; h < kValuMaxGroup; ++h)
+#pragma unroll
+        for (int c = 0; c < S::kChunks; ++c) st.o[h][c] = 0.f;
+    st.m[0] = st.m[1] = -INFINITY;
+    st.l[0] = st.l[1] = 0.f;
+    bool bad = false;
+
+    const int32_t* row = a.page_table + static_cast<int64_t>(pc.b) * a.pt_stride;
+    const int64_t head_off = static_cast<int64_t>(pc.g) * 2 * S::kTile;
+    PageSrc ps;
+    ps.hot = a.hot + a.layer_offset + head_off;
+    ps.page_bytes = a.page_bytes;
+    ps.num_hot = static_cast<unsigned>(a.num_pages);
+    if constexpr (TIERED) {
+        ps.cold = a.cold + a.layer_offset + head_off;
+        ps.stage = a.stage + head_off;
+        ps.slice_bytes = a.slice_bytes;
+        ps.num_cold = static_cast<unsigned>(a.num_cold_pages);
+        ps.num_stage = static_cast<unsigned>(a.num_stage_slots);
+    }
+    const int qg = lane >> 4;
+    const unsigned koff = 16u * lane;
+    const unsigned voff = 32u * (lane & 15) + 8u * qg;
+    const int tail_valid = seq_len - kPageTokens * (nb - 1);
+
+    int ids_cur = load_ids(row, pc.p0, pc.p1, lane);
+    int ids_nxt = load_ids(row, pc.p0 + kWave, pc.p1, lane);
+    int cur_chunk = 0;
+    auto pid_at = [&](int i) -> int {
+        const int rel = i - pc.p0;
+        const int cc = rel >> 6;
+        if (cc != cur_chunk) {
+            ids_cur = ids_nxt;
+            cur_chunk = cc;
+            ids_nxt = load_ids(row, pc.p0 + kWave * (cc + 1), pc.p1, lane);
+        }
+        return __builtin_amdgcn_readlane(ids_cur, rel & 63);
+    };
+
+    PageRegs<D, true> buf[R];
+#pragma unroll
+    for (int r = 0; r < R - 1; ++r)
+        if (pc.p0 + r < pc.p1) load_page<D, true, TIERED>(buf[r], ps, pid_at(pc.p0 + r), bad, koff, voff);
+    for (int i = pc.p0; i < pc.p1; i += R) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int ip = i + r;
+            if (ip < pc.p1) {
+                const int ahead = ip + R - 1;
+                if (ahead < pc.p1)
+                    load_page<D, true, TIERED>(buf[(r + R - 1) % R], ps, pid_at(ahead), bad, koff, voff);
+                compute_page_valu<D>(st, buf[r], ip == nb - 1 ? tail_valid : kPageTokens, a.scale_log2,
+                                     lane, sm);
+            }
+        }
+    }
+
+    // outputs: reduce-scatter over the token quarters (lane (dl, qg) keeps heads
+    // 2 qg, 2 qg + 1), then every lane writes its two heads' dims 16 c + dl
+    const bool upper = lane >= 32, odd = (lane & 16) != 0;
+    float o4[4][S::kChunks];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int c = 0; c < S::kChunks; ++c) {
+            const float send = upper ? st.o[j][c] : st.o[4 + j][c];
+            o4[j][c] = (upper ? st.o[4 + j][c] : st.o[j][c]) + __shfl_xor(send, 32);
+        }
+    float o2[2][S::kChunks];
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int c = 0; c < S::kChunks; ++c) {
+            const float send = odd ? o4[e][c] : o4[2 + e][c];
+            o2[e][c] = (odd ? o4[2 + e][c] : o4[e][c]) + __shfl_xor(send, 16);
+        }
+    // weight sums: lane (t, qq) holds token t's share of heads 2 qq + e
+    float l[2] = {st.l[0], st.l[1]};
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) l[e] += __shfl_xor(l[e], o);
+    const int dl = lane & 15;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const int h = 2 * qg + e;
+        if (h < a.group) {
+            float* po = a.part_o + (static_cast<int64_t>(pc.slot) * a.group + h) * D + dl;
+#pragma unroll
+            for (int c = 0; c < S::kChunks; ++c) po[16 * c] = o2[e][c];
+            if (dl == 0) {
+                float* pml = a.part_ml + static_cast<int64_t>(pc.slot) * 2 * a.group;
+                pml[h] = st.m[e];
+                pml[a.group + h] = bad ? __builtin_nanf("") : l[e];
+            }
+        }
+    }
+}
+
+template <int D, bool BF16, int R, bool TIERED, bool VALU>
 __global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs a) {
     extern __shared__ int32_t s_pref[];
     block_prefix_pages(a.seq_lens, a.batch, a.pt_stride, s_pref);
@@ -490,7 +741,12 @@ __global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs 
         const int seq_len = L < kPageTokens * nb ? L : kPageTokens * nb;
         const int64_t seg_first = static_cast<int64_t>(lds_uniform(s_pref + pc.b)) * a.num_kv_heads +
                                   static_cast<int64_t>(pc.g) * nb;
-        run_piece<D, BF16, R, TIERED>(a, pc, nb, seq_len, lane, seg_first, total);
+        if constexpr (VALU) {
+            __shared__ ValuLds<D> s_valu[kBlockWaves];
+            run_piece_valu<D, R, TIERED>(a, pc, nb, seq_len, lane, s_valu[threadIdx.x / kWave]);
+        } else {
+            run_piece<D, BF16, R, TIERED>(a, pc, nb, seq_len, lane, seg_first, total);
+        }
         u += pc.p1 - pc.p0;
     }
 }
@@ -626,19 +882,23 @@ constexpr int ring_depth() {
     return BF16 ? (D == 128 ? HCK_RING_BF16_D128 : 5) : (D == 128 ? 2 : 3);
 }
 
-template <int D, bool BF16>
+template <int D, bool BF16, bool VALU>
 const void* split_kernel_ptr(bool tiered) {
-    return tiered ? reinterpret_cast<const void*>(&decode_split_kernel<D, BF16, ring_depth<D, BF16>(), true>)
-                  : reinterpret_cast<const void*>(&decode_split_kernel<D, BF16, ring_depth<D, BF16>(), false>);
+    constexpr int R = ring_depth<D, BF16>();
+    return tiered ? reinterpret_cast<const void*>(&decode_split_kernel<D, BF16, R, true, VALU>)
+                  : reinterpret_cast<const void*>(&decode_split_kernel<D, BF16, R, false, VALU>);
 }
 
-const void* pick_split(int head_dim, int dtype, bool tiered) {
+// The vector-ALU variant exists for bf16 only.
+const void* pick_split(int head_dim, int dtype, bool tiered, bool valu) {
     if (dtype == kDtypeBf16) {
-        if (head_dim == 128) return split_kernel_ptr<128, true>(tiered);
-        if (head_dim == 64) return split_kernel_ptr<64, true>(tiered);
-    } else {
-        if (head_dim == 128) return split_kernel_ptr<128, false>(tiered);
-        if (head_dim == 64) return split_kernel_ptr<64, false>(tiered);
+        if (head_dim == 128)
+            return valu ? split_kernel_ptr<128, true, true>(tiered) : split_kernel_ptr<128, true, false>(tiered);
+        if (head_dim == 64)
+            return valu ? split_kernel_ptr<64, true, true>(tiered) : split_kernel_ptr<64, true, false>(tiered);
+    } else if (!valu) {
+        if (head_dim == 128) return split_kernel_ptr<128, false, false>(tiered);
+        if (head_dim == 64) return split_kernel_ptr<64, false, false>(tiered);
     }
     return nullptr;
 }
@@ -665,7 +925,8 @@ size_t prefix_lds_bytes(int batch) { return static_cast<size_t>(batch + 1) * siz
 }  // namespace
 
 hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s) {
-    const void* k = pick_split(head_dim, dtype, a.tiered != 0);
+    if (a.valu && (a.group > kValuMaxGroup || a.fused)) return hipErrorInvalidValue;
+    const void* k = pick_split(head_dim, dtype, a.tiered != 0, a.valu != 0);
     if (!k || a.waves <= 0) return hipErrorInvalidValue;
     const int blocks = (a.waves + kBlockWaves - 1) / kBlockWaves;
     void* args[] = {const_cast<DecodeArgs*>(&a)};
@@ -686,7 +947,7 @@ hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, h
 }
 
 int decode_split_blocks_per_cu(int head_dim, int dtype, int batch) {
-    const void* k = pick_split(head_dim, dtype, false);
+    const void* k = pick_split(head_dim, dtype, false, false);
     if (!k) return 0;
     int n = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kBlockThreads, prefix_lds_bytes(batch)) !=

@@ -48,6 +48,7 @@ struct DecodeArgs {
     const char* stage;        // staging buffer of this layer: [slot][kv_head][K tile, V tile]
     int32_t num_stage_slots;
     int64_t slice_bytes;      // bytes of one staging slot
+    int32_t valu;             // 1: the split runs its products on the vector ALU (bf16, group <= 8)
 };
 
 // Bytes of partial results for `slots` slots.

@@ -200,6 +200,7 @@ struct kv_pool {
     bool free_pending = false;
     bool profiling = false;
     int32_t combine_mode = KV_COMBINE_SEPARATE;
+    int32_t compute_mode = KV_DECODE_MATRIX;
     int32_t* counters = nullptr;  // decode arrival counters, zero between calls
     hipEvent_t decode_event = nullptr;
     bool decode_pending = false;
@@ -1202,6 +1203,13 @@ int kv_pool_set_decode_combine(kv_pool* pool, int32_t mode) {
     return KV_OK;
 }
 
+int kv_pool_set_decode_compute(kv_pool* pool, int32_t mode) {
+    if (!pool || (mode != KV_DECODE_MATRIX && mode != KV_DECODE_VECTOR))
+        return fail(KV_ERR_INVALID, "bad arguments");
+    pool->compute_mode = mode;
+    return KV_OK;
+}
+
 int kv_pool_set_decode_waves(kv_pool* pool, int32_t waves) {
     if (!pool || waves < 0) return fail(KV_ERR_INVALID, "bad arguments");
     pool->waves_override = waves;
@@ -1234,6 +1242,10 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
                     pool->d.num_kv_heads);
     const int32_t group = num_q_heads / pool->d.num_kv_heads;
     if (group > 16) return fail(KV_ERR_INVALID, "more than 16 query heads per KV head");
+    const bool valu = pool->compute_mode == KV_DECODE_VECTOR;
+    if (valu && (pool->d.dtype != KV_DTYPE_BF16 || group > 8 || pool->combine_mode != KV_COMBINE_SEPARATE))
+        return fail(KV_ERR_INVALID, "vector-ALU decode needs bf16, at most 8 query heads per KV head "
+                                    "and the separate merge");
     if (pt_stride < 1 || static_cast<int64_t>(batch) * pt_stride >= (int64_t(1) << 31))
         return fail(KV_ERR_INVALID, "bad page-table stride");
     if (reinterpret_cast<uintptr_t>(workspace) & 255)
@@ -1267,6 +1279,7 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
     a.counters = pool->counters;
     a.fused = pool->combine_mode == KV_COMBINE_FUSED ? 1 : 0;
     a.tiered = pool->tiered() ? 1 : 0;
+    a.valu = valu ? 1 : 0;
     a.cold = pool->cold;
     a.num_cold_pages = pool->cold ? pool->d.num_cold_pages : 0;
     a.slice_bytes = pool->slice_bytes;

@@ -28,6 +28,7 @@ KV_KERNEL_DECODE_SPLIT, KV_KERNEL_DECODE_COMBINE, KV_KERNEL_PAGE_COPY, KV_KERNEL
 KV_KERNEL_PREFETCH_COPY, KV_KERNEL_COUNT = 4, 5
 KV_PAGE_COLD, KV_PAGE_STAGED = 1 << 30, 1 << 29
 KV_COMBINE_SEPARATE, KV_COMBINE_FUSED = 0, 1
+KV_DECODE_MATRIX, KV_DECODE_VECTOR = 0, 1
 
 
 class KVError(RuntimeError):
@@ -96,6 +97,7 @@ _SIGS = {
     "paged_decode_waves": (_I32, [_P]),
     "kv_pool_set_decode_waves": (ctypes.c_int, [_P, _I32]),
     "kv_pool_set_decode_combine": (ctypes.c_int, [_P, _I32]),
+    "kv_pool_set_decode_compute": (ctypes.c_int, [_P, _I32]),
     "paged_decode_workspace_bytes": (_SZ, [_P, _I32, _I32]),
     "paged_decode_attention": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _I32, _I32,
                                               ctypes.c_float, _P, _P, _SZ, _P]),
@@ -290,6 +292,10 @@ def kv_pool_set_decode_waves(pool: int, waves: int) -> None:
 
 def kv_pool_set_decode_combine(pool: int, mode: int) -> None:
     _check(_lib.kv_pool_set_decode_combine(pool, mode), "kv_pool_set_decode_combine")
+
+
+def kv_pool_set_decode_compute(pool: int, mode: int) -> None:
+    _check(_lib.kv_pool_set_decode_compute(pool, mode), "kv_pool_set_decode_compute")
 
 
 def paged_decode_workspace_bytes(pool: int, batch: int, num_q_heads: int) -> int:
