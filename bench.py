@@ -692,6 +692,8 @@ def main():
     ap.add_argument("--batch", type=int, default=32, help="active sessions (the workload has 32)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--waves", type=int, default=0, help="override the decode wave count")
+    ap.add_argument("--copy-blocks", type=int, default=0,
+                    help="cap on the resume copy's persistent grid (0 = the library default)")
     ap.add_argument("--combine", choices=["fused", "separate"], default="separate",
                     help="merge split partials in the split kernel's last wave or in a second kernel")
     ap.add_argument("--compute", choices=["matrix", "vector"], default="matrix",
@@ -756,6 +758,8 @@ def main():
         pool.set_waves(args.waves)
     pool.set_combine(args.combine == "fused")
     pool.set_compute(args.compute == "vector")
+    if args.copy_blocks:
+        kv.kv_pool_set_copy_blocks(pool.handle, args.copy_blocks)
 
     q = torch.from_numpy(synth.queries(w.seed + 1, w.batch, w.num_q_heads, w.head_dim,
                                        w.value_scale, "bf16").view(np.int16)).to(dev).view(torch.bfloat16)
@@ -897,6 +901,7 @@ def main():
             "batch": w.batch, "total_tokens": int(w.seq_lens.sum()), "num_q_heads": w.num_q_heads,
             "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "layers": 1, "page_tokens": 16,
             "hot_pages": num_hot, "decode_waves": pool.waves(), "combine": args.combine,
+            "copy_blocks": args.copy_blocks,
             "compute": args.compute,
             "seed": args.seed,
         },
