@@ -418,3 +418,56 @@ def test_copy_lists_larger_than_one_staging_slot(dev):
         c = torch.tensor(cold, dtype=torch.long, device=dev)
         assert torch.equal(pool.hot.view(-1, pb).index_select(0, h), pool.cold.view(-1, pb).index_select(0, c))
     pool.close()
+
+
+def test_copy_launch_shapes_and_budget(dev):
+    """The page copy takes one of two launch shapes by size: up to 16 GiB of
+    4 KiB rows (10,922 pages of 1.5 MiB) one row per block on a large grid,
+    above it (10,923 pages) 32 KiB chunks on the persistent grid; a caller's
+    copy-block budget takes the persistent shape with the budget as the grid.
+    Each resume: page table as the model predicts, sampled pages bit-exact."""
+    from paper_2609_25782_amd.pool import HotColdPool
+    fine, coarse = 10922, 10923
+    assert fine * 384 <= 4 << 20 < coarse * 384
+    n_hot, n_cold, stride = coarse + 8, fine + coarse + 8, coarse
+    _say("copy launch shapes: %d and %d pages of 1.5 MiB" % (fine, coarse))
+    pool = HotColdPool(48, 4, 128, "bf16", n_hot, n_cold, 2, stride)
+    model = PoolModel(n_hot, n_cold, 2, stride)
+    g = torch.Generator(device=dev)
+    g.manual_seed(8)
+    view = pool.cold.view(n_cold, -1)
+    for i in range(0, n_cold, 1024):
+        view[i:i + 1024].copy_(torch.randint(0, 256, view[i:i + 1024].shape, dtype=torch.uint8,
+                                             device=dev, generator=g))
+    rng = np.random.default_rng(8)
+    perm = rng.permutation(n_cold)
+    lists = [[int(p) for p in perm[:fine]], [int(p) for p in perm[fine:fine + coarse]]]
+    for n, cold in zip((fine, coarse), lists):
+        assert pool.import_cold(16 * n, cold) == model.import_cold(16 * n, cold)
+    pb = pool.page_bytes
+    hot = pool.hot.view(-1, pb)
+
+    def resume_and_check(sid, what):
+        pool.resume([sid])
+        copied = sum(len(per) for per in model.resume([sid]))
+        torch.cuda.synchronize()
+        _check_table(pool, model)
+        _, _, h, c = pool.info(sid)
+        idx = sorted(set([0, len(h) - 1] + [int(x) for x in rng.choice(len(h), size=300, replace=False)]))
+        hh = torch.tensor([h[i] for i in idx], dtype=torch.long, device=dev)
+        cc = torch.tensor([c[i] for i in idx], dtype=torch.long, device=dev)
+        assert torch.equal(hot.index_select(0, hh), view.index_select(0, cc))
+        _say("%s: %d pages resumed, %d copied, %d sampled pages bit-exact" % (what, len(h), copied, len(idx)))
+        return copied
+
+    n1 = resume_and_check(0, "fine shape")
+    pool.evict([0])
+    model.evict_many([0])
+    n2 = resume_and_check(1, "persistent shape")  # takes session 0's former hot pages
+    pool.evict([1])
+    model.evict_many([1])
+    pool.set_copy_blocks(64)
+    n3 = resume_and_check(0, "budget of 64 blocks")
+    assert (n1, n2) == (fine, coarse) and n3 > fine - 16
+    assert pool.stats()["pages_to_hot"] == n1 + n2 + n3
+    pool.close()
