@@ -386,9 +386,9 @@ int kv_pool_set_decode_waves(kv_pool* pool, int32_t waves);
 
 enum kv_combine_mode {
     KV_COMBINE_SEPARATE = 0, /* partials merged by a second kernel (default) */
-    KV_COMBINE_FUSED = 1     /* the last wave of each (row, KV head) merges them; needs a
-                                device-scope release/acquire per partial, which on gfx950
-                                writes back and invalidates the L2 and is slower */
+    KV_COMBINE_FUSED = 1     /* the last wave of each (row, KV head) merges them; every
+                                wave's arrival is a device-scope release, which on gfx950
+                                writes back its L2, and this mode is slower */
 };
 /* How paged_decode_attention merges its split partials.  The two modes merge
  * in different orders, so their results agree to float32 rounding, not bit for

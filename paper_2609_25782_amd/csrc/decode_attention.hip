@@ -448,15 +448,16 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
         }
     }
     if (a.fused) {
-        // The wave that delivers the last partial of (b, g) merges them all.
+        // The wave that delivers the last partial of (b, g) merges them all.  The
+        // arrival count is a release (this wave's partial becomes visible to every
+        // XCD: on gfx950 an L2 write-back) and only the merging wave acquires.
         const SegWaves sw = seg_waves(seg_first_unit, nb, total_units, a.waves);
         int32_t* cnt = a.counters + pc.b * a.num_kv_heads + pc.g;
-        __threadfence();  // release this wave's partial
         int prev = 0;
-        if (lane == 0) prev = atomicAdd(cnt, 1);
+        if (lane == 0) prev = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
         prev = __builtin_amdgcn_readfirstlane(__shfl(prev, 0));
         if (prev + 1 == sw.pieces) {
-            __threadfence();  // acquire the other waves' partials
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             combine_segment<D, BF16>(a, pc.b, pc.g, sw, total_units, lane);
             if (lane == 0) atomicExch(cnt, 0);  // ready for the next call
         }
