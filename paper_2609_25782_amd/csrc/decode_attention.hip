@@ -49,6 +49,12 @@ constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9 
 #ifndef HCK_RING_BF16_D128
 #define HCK_RING_BF16_D128 3
 #endif
+// Waves per block of the split kernel.
+#ifndef HCK_SPLIT_BLOCK_WAVES
+#define HCK_SPLIT_BLOCK_WAVES 4
+#endif
+constexpr int kSplitBlockWaves = HCK_SPLIT_BLOCK_WAVES;
+constexpr int kSplitBlockThreads = kSplitBlockWaves * kWave;
 
 template <int D, bool BF16>
 struct Shape {
@@ -716,12 +722,12 @@ __device__ void run_piece_valu(const DecodeArgs& a, const Piece& pc, int nb, int
 }
 
 template <int D, bool BF16, int R, bool TIERED, bool VALU>
-__global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kSplitBlockThreads) void decode_split_kernel(DecodeArgs a) {
     extern __shared__ int32_t s_pref[];
-    block_prefix_pages(a.seq_lens, a.batch, a.pt_stride, s_pref);
+    block_prefix_pages<kSplitBlockThreads>(a.seq_lens, a.batch, a.pt_stride, s_pref);
     __syncthreads();
     const int lane = threadIdx.x & (kWave - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kBlockWaves + threadIdx.x / kWave);
+    const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kSplitBlockWaves + threadIdx.x / kWave);
     if (wave >= a.waves) return;
     if (a.fused) {
         // rows with no pages get no partials: write them here (0 for L = 0, NaN for L < 0)
@@ -743,7 +749,7 @@ __global__ __launch_bounds__(kBlockThreads) void decode_split_kernel(DecodeArgs 
         const int64_t seg_first = static_cast<int64_t>(lds_uniform(s_pref + pc.b)) * a.num_kv_heads +
                                   static_cast<int64_t>(pc.g) * nb;
         if constexpr (VALU) {
-            __shared__ ValuLds<D> s_valu[kBlockWaves];
+            __shared__ ValuLds<D> s_valu[kSplitBlockWaves];
             run_piece_valu<D, R, TIERED>(a, pc, nb, seq_len, lane, s_valu[threadIdx.x / kWave]);
         } else {
             run_piece<D, BF16, R, TIERED>(a, pc, nb, seq_len, lane, seg_first, total);
@@ -929,9 +935,9 @@ hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hip
     if (a.valu && (a.group > kValuMaxGroup || a.fused)) return hipErrorInvalidValue;
     const void* k = pick_split(head_dim, dtype, a.tiered != 0, a.valu != 0);
     if (!k || a.waves <= 0) return hipErrorInvalidValue;
-    const int blocks = (a.waves + kBlockWaves - 1) / kBlockWaves;
+    const int blocks = (a.waves + kSplitBlockWaves - 1) / kSplitBlockWaves;
     void* args[] = {const_cast<DecodeArgs*>(&a)};
-    return hipLaunchKernel(k, dim3(blocks), dim3(kBlockThreads), args, prefix_lds_bytes(a.batch), s);
+    return hipLaunchKernel(k, dim3(blocks), dim3(kSplitBlockThreads), args, prefix_lds_bytes(a.batch), s);
 }
 
 hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s) {
@@ -951,7 +957,7 @@ int decode_split_blocks_per_cu(int head_dim, int dtype, int batch) {
     const void* k = pick_split(head_dim, dtype, false, false);
     if (!k) return 0;
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kBlockThreads, prefix_lds_bytes(batch)) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kSplitBlockThreads, prefix_lds_bytes(batch)) !=
         hipSuccess)
         return 0;
     return n;

@@ -26,13 +26,14 @@ __device__ __forceinline__ int row_pages(int32_t seq_len, int64_t stride) {
 }
 
 // s_pref[b] = sum of row_pages over rows < b, for b = 0 .. batch (exclusive
-// prefix sum plus the total).  All 256 threads of the block must call it; the
-// caller synchronises before reading s_pref.
+// prefix sum plus the total).  All kThreads threads of the block must call it;
+// the caller synchronises before reading s_pref.
+template <int kThreads = kBlockThreads>
 __device__ inline void block_prefix_pages(const int32_t* __restrict__ seq_lens, int batch,
                                           int64_t stride, int32_t* s_pref) {
-    __shared__ int32_t s_wave_sum[kBlockWaves];
+    __shared__ int32_t s_wave_sum[kThreads / kWave];
     const int tid = threadIdx.x;
-    const int per = (batch + kBlockThreads - 1) / kBlockThreads;
+    const int per = (batch + kThreads - 1) / kThreads;
     const int lo = min(batch, tid * per);
     const int hi = min(batch, lo + per);
     int sum = 0;
@@ -52,7 +53,7 @@ __device__ inline void block_prefix_pages(const int32_t* __restrict__ seq_lens, 
         s_pref[b] = run;
         run += row_pages(seq_lens[b], stride);
     }
-    if (tid == kBlockThreads - 1) s_pref[batch] = run;
+    if (tid == kThreads - 1) s_pref[batch] = run;
 }
 
 // One piece of the decode work split: wave `wave` handles pages [p0, p1) of
