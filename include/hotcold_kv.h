@@ -523,10 +523,11 @@ const char* kv_strerror(int status);
 const char* kv_last_error(void);
 
 /*
- * Profiling hook.  When enabled, every kernel the pool launches is bracketed by
- * HIP events on the launch stream.  kv_pool_profile_read waits for the recorded
- * launches of one kernel id, returns their count and summed duration in
- * milliseconds, and forgets them.
+ * Profiling hook.  When enabled, every timed kernel the pool launches (the ids
+ * above) carries a pair of HIP events that its dispatch records at the kernel's
+ * start and end (hipExtLaunchKernel), so a duration covers the kernel alone.
+ * kv_pool_profile_read waits for the recorded launches of one kernel id,
+ * returns their count and summed duration in milliseconds, and forgets them.
  */
 int kv_pool_set_profiling(kv_pool* pool, int enable);
 int kv_pool_profile_read(kv_pool* pool, int32_t kernel_id, int32_t* launches, double* total_ms);

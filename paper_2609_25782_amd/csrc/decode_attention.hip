@@ -931,16 +931,18 @@ size_t prefix_lds_bytes(int batch) { return static_cast<size_t>(batch + 1) * siz
 
 }  // namespace
 
-hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s) {
+hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s,
+                               const LaunchEvents& ev) {
     if (a.valu && (a.group > kValuMaxGroup || a.fused)) return hipErrorInvalidValue;
     const void* k = pick_split(head_dim, dtype, a.tiered != 0, a.valu != 0);
     if (!k || a.waves <= 0) return hipErrorInvalidValue;
     const int blocks = (a.waves + kSplitBlockWaves - 1) / kSplitBlockWaves;
     void* args[] = {const_cast<DecodeArgs*>(&a)};
-    return hipLaunchKernel(k, dim3(blocks), dim3(kSplitBlockThreads), args, prefix_lds_bytes(a.batch), s);
+    return launch_kernel(k, dim3(blocks), dim3(kSplitBlockThreads), args, prefix_lds_bytes(a.batch), s, ev);
 }
 
-hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s) {
+hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s,
+                                 const LaunchEvents& ev) {
     const int segs = a.batch * a.num_kv_heads;
     if (segs == 0) return hipSuccess;
     // Many partials per segment (waves well above segments): four waves per head.
@@ -950,7 +952,7 @@ hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, h
     void* args[] = {const_cast<DecodeArgs*>(&a)};
     const unsigned y = wide ? static_cast<unsigned>(a.group)
                             : static_cast<unsigned>((a.group + kBlockWaves - 1) / kBlockWaves);
-    return hipLaunchKernel(k, dim3(segs, y), dim3(kBlockThreads), args, 0, s);
+    return launch_kernel(k, dim3(segs, y), dim3(kBlockThreads), args, 0, s, ev);
 }
 
 int decode_split_blocks_per_cu(int head_dim, int dtype, int batch) {

@@ -1,6 +1,7 @@
 // Host-side launchers for the library's HIP kernels (internal interface).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -51,13 +52,29 @@ struct DecodeArgs {
     int32_t valu;             // 1: the split runs its products on the vector ALU (bf16, group <= 8)
 };
 
+// Events a launch records at its kernel's start and end (the library's
+// profiling); both null for a plain launch.  The timestamps come from the
+// dispatch itself, so they bracket the kernel and nothing else.
+struct LaunchEvents {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
+
+inline hipError_t launch_kernel(const void* k, dim3 grid, dim3 block, void** args, size_t lds,
+                                hipStream_t s, const LaunchEvents& ev) {
+    if (ev.start && ev.stop) return hipExtLaunchKernel(k, grid, block, args, lds, s, ev.start, ev.stop, 0);
+    return hipLaunchKernel(k, grid, block, args, lds, s);
+}
+
 // Bytes of partial results for `slots` slots.
 inline size_t decode_partials_bytes(int64_t slots, int group, int head_dim) {
     return static_cast<size_t>(slots) * group * (head_dim + 2) * sizeof(float);
 }
 
-hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s);
-hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s);
+hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s,
+                               const LaunchEvents& ev = {});
+hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s,
+                                 const LaunchEvents& ev = {});
 // Largest batch the decode kernels accept (bounds the counter array).
 constexpr int kMaxDecodeBatch = 8192;
 // Resident 256-thread blocks per CU of the split kernel (0 if unsupported shape).
@@ -82,7 +99,7 @@ struct CopyEntry {
 // max_blocks caps the persistent grid (0: the default cap).
 hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_bytes,
                             const CopyEntry* entries, int32_t n, int32_t* page_table,
-                            int32_t max_blocks, hipStream_t s);
+                            int32_t max_blocks, hipStream_t s, const LaunchEvents& ev = {});
 
 // The general form: `bytes` (a multiple of 4 KiB) from src_base + e.src *
 // src_stride to dst_base + e.dst * dst_stride.  With src_base at a layer's
@@ -90,7 +107,8 @@ hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_b
 // slices of spilled pages.
 hipError_t launch_slice_copy(const char* src_base, int64_t src_stride, char* dst_base,
                              int64_t dst_stride, int64_t bytes, const CopyEntry* entries, int32_t n,
-                             int32_t* page_table, int32_t max_blocks, hipStream_t s);
+                             int32_t* page_table, int32_t max_blocks, hipStream_t s,
+                             const LaunchEvents& ev = {});
 
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t s);
 

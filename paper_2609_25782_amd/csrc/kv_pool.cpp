@@ -294,19 +294,29 @@ struct kv_pool {
         return e;
     }
 
-    // Bracket a launch with profiling events when profiling is on.
-    hipEvent_t prof_begin(hipStream_t s) {
-        if (!profiling) return nullptr;
-        hipEvent_t e = take_event();
-        if (e) (void)hipEventRecord(e, s);
-        return e;
+    // Events for one launch when profiling is on: the launch records them at
+    // its kernel's start and end.  prof_done files them under `kernel` if the
+    // launch went out, or returns them to the spares.
+    hck::LaunchEvents prof_events() {
+        hck::LaunchEvents ev;
+        if (!profiling) return ev;
+        ev.start = take_event();
+        ev.stop = take_event();
+        if (!ev.start || !ev.stop) {
+            if (ev.start) spare_events.push_back(ev.start);
+            if (ev.stop) spare_events.push_back(ev.stop);
+            return hck::LaunchEvents{};
+        }
+        return ev;
     }
-    void prof_end(int kernel, hipEvent_t start, hipStream_t s) {
-        if (!start) return;
-        hipEvent_t e = take_event();
-        if (!e) return;
-        (void)hipEventRecord(e, s);
-        prof[kernel].push_back(ProfRec{start, e});
+    void prof_done(int kernel, const hck::LaunchEvents& ev, hipError_t launched) {
+        if (!ev.start) return;
+        if (launched == hipSuccess) {
+            prof[kernel].push_back(ProfRec{ev.start, ev.stop});
+        } else {
+            spare_events.push_back(ev.start);
+            spare_events.push_back(ev.stop);
+        }
     }
 
     // Enqueue page copies (in chunks that fit a staging slot).
@@ -322,11 +332,11 @@ struct kv_pool {
             hipError_t e = hipMemcpyAsync(slot->dev, slot->host, n * sizeof(hck::CopyEntry),
                                           hipMemcpyHostToDevice, s);
             if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(copy list)");
-            hipEvent_t p = prof_begin(s);
+            const hck::LaunchEvents ev = prof_events();
             e = hck::launch_page_copy(src, dst, page_bytes,
                                       static_cast<const hck::CopyEntry*>(slot->dev), n, pt,
-                                      copy_blocks, s);
-            prof_end(kernel_id, p, s);
+                                      copy_blocks, s, ev);
+            prof_done(kernel_id, ev, e);
             if (e != hipSuccess) return hip_fail(e, "page copy launch");
             e = hipEventRecord(slot->done, s);
             if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
@@ -1309,14 +1319,14 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
         hipError_t w = hipStreamWaitEvent(st, pool->half_ready[half], 0);
         if (w != hipSuccess) return hip_fail(w, "hipStreamWaitEvent(staging)");
     }
-    hipEvent_t p = capturing ? nullptr : pool->prof_begin(st);
-    hipError_t e = hck::launch_decode_split(a, pool->d.head_dim, pool->d.dtype, st);
-    pool->prof_end(KV_KERNEL_DECODE_SPLIT, p, st);
+    hck::LaunchEvents ev = capturing ? hck::LaunchEvents{} : pool->prof_events();
+    hipError_t e = hck::launch_decode_split(a, pool->d.head_dim, pool->d.dtype, st, ev);
+    pool->prof_done(KV_KERNEL_DECODE_SPLIT, ev, e);
     if (e != hipSuccess) return hip_fail(e, "decode split launch");
     if (!a.fused) {
-        p = capturing ? nullptr : pool->prof_begin(st);
-        e = hck::launch_decode_combine(a, pool->d.head_dim, pool->d.dtype, st);
-        pool->prof_end(KV_KERNEL_DECODE_COMBINE, p, st);
+        ev = capturing ? hck::LaunchEvents{} : pool->prof_events();
+        e = hck::launch_decode_combine(a, pool->d.head_dim, pool->d.dtype, st, ev);
+        pool->prof_done(KV_KERNEL_DECODE_COMBINE, ev, e);
         if (e != hipSuccess) return hip_fail(e, "decode combine launch");
     }
     if (capturing) return KV_OK;
@@ -1446,11 +1456,11 @@ int paged_decode_prefetch(kv_pool* pool, int32_t layer, kv_stream_t copy_stream)
     if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(prefetch)");
     const int64_t layer_offset = static_cast<int64_t>(layer) * pool->slice_bytes;
     char* dst = pool->stage + static_cast<int64_t>(half) * pool->stage_slots * pool->slice_bytes;
-    hipEvent_t p = pool->prof_begin(cs);
+    const hck::LaunchEvents ev = pool->prof_events();
     e = hck::launch_slice_copy(pool->cold + layer_offset, pool->page_bytes, dst, pool->slice_bytes,
                                pool->slice_bytes, pool->plan_dev, static_cast<int32_t>(pool->plan.size()),
-                               nullptr, pool->copy_blocks, cs);
-    pool->prof_end(KV_KERNEL_PREFETCH_COPY, p, cs);
+                               nullptr, pool->copy_blocks, cs, ev);
+    pool->prof_done(KV_KERNEL_PREFETCH_COPY, ev, e);
     if (e != hipSuccess) return hip_fail(e, "prefetch launch");
     e = hipEventRecord(pool->half_ready[half], cs);
     if (e == hipSuccess) e = hipEventRecord(pool->prefetch_done, cs);

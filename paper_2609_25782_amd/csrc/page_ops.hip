@@ -276,14 +276,15 @@ int grid_for(int64_t work, int cap) {
 
 hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_bytes,
                             const CopyEntry* entries, int32_t n, int32_t* page_table,
-                            int32_t max_blocks, hipStream_t s) {
+                            int32_t max_blocks, hipStream_t s, const LaunchEvents& ev) {
     return launch_slice_copy(src_base, page_bytes, dst_base, page_bytes, page_bytes, entries, n,
-                             page_table, max_blocks, s);
+                             page_table, max_blocks, s, ev);
 }
 
 hipError_t launch_slice_copy(const char* src_base, int64_t src_stride, char* dst_base,
                              int64_t dst_stride, int64_t bytes, const CopyEntry* entries, int32_t n,
-                             int32_t* page_table, int32_t max_blocks, hipStream_t s) {
+                             int32_t* page_table, int32_t max_blocks, hipStream_t s,
+                             const LaunchEvents& ev) {
     if (n <= 0) return hipSuccess;
     constexpr int64_t kRow = static_cast<int64_t>(kBlockThreads) * 16;  // 4 KiB
     if (bytes % kRow || bytes <= 0) return hipErrorInvalidValue;
@@ -299,15 +300,14 @@ hipError_t launch_slice_copy(const char* src_base, int64_t src_stride, char* dst
     const int64_t work = chunks * n;
     const int64_t cap = max_blocks > 0 ? max_blocks : fine ? HCK_COPY_FINE_BLOCKS : HCK_COPY_MAX_BLOCKS;
     const int64_t blocks = work < cap ? work : cap;
-    const dim3 grid(static_cast<unsigned>(blocks)), block(kBlockThreads);
     const int cpp = static_cast<int>(chunks);
-    switch (u) {
-        case 8: hipLaunchKernelGGL(page_copy_kernel<8>, grid, block, 0, s, src_base, src_stride, dst_base, dst_stride, entries, n, cpp, page_table); break;
-        case 4: hipLaunchKernelGGL(page_copy_kernel<4>, grid, block, 0, s, src_base, src_stride, dst_base, dst_stride, entries, n, cpp, page_table); break;
-        case 2: hipLaunchKernelGGL(page_copy_kernel<2>, grid, block, 0, s, src_base, src_stride, dst_base, dst_stride, entries, n, cpp, page_table); break;
-        default: hipLaunchKernelGGL(page_copy_kernel<1>, grid, block, 0, s, src_base, src_stride, dst_base, dst_stride, entries, n, cpp, page_table); break;
-    }
-    return hipGetLastError();
+    const void* k = u == 8   ? reinterpret_cast<const void*>(&page_copy_kernel<8>)
+                    : u == 4 ? reinterpret_cast<const void*>(&page_copy_kernel<4>)
+                    : u == 2 ? reinterpret_cast<const void*>(&page_copy_kernel<2>)
+                             : reinterpret_cast<const void*>(&page_copy_kernel<1>);
+    void* args[] = {&src_base, &src_stride, &dst_base, &dst_stride, &entries, &n, const_cast<int*>(&cpp),
+                    &page_table};
+    return launch_kernel(k, dim3(static_cast<unsigned>(blocks)), dim3(kBlockThreads), args, 0, s, ev);
 }
 
 hipError_t launch_table_writes(const CopyEntry* entries, int32_t n, int32_t* page_table, hipStream_t s) {
