@@ -721,8 +721,15 @@ __device__ void run_piece_valu(const DecodeArgs& a, const Piece& pc, int nb, int
     }
 }
 
+// Register budget of the split kernel: with HCK_SPLIT_WAVES_PER_EU = n the
+// compiler keeps it within 512 / n registers so that n waves fit per SIMD.
+#ifndef HCK_SPLIT_WAVES_PER_EU
+#define HCK_SPLIT_WAVES_PER_EU 1
+#endif
+
 template <int D, bool BF16, int R, bool TIERED, bool VALU>
-__global__ __launch_bounds__(kSplitBlockThreads) void decode_split_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kSplitBlockThreads)
+__attribute__((amdgpu_waves_per_eu(HCK_SPLIT_WAVES_PER_EU))) void decode_split_kernel(DecodeArgs a) {
     extern __shared__ int32_t s_pref[];
     block_prefix_pages<kSplitBlockThreads>(a.seq_lens, a.batch, a.pt_stride, s_pref);
     __syncthreads();
