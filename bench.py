@@ -545,12 +545,44 @@ def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
         if it >= 2:
             times.append(e0.elapsed_time(e1))
     out["context"] = {"dtod_copy_GBps": round(dtod, 1),
-                      "streaming_read_GBps": round(a.numel() / (float(np.median(times)) / 1e3) / 1e9, 1),
+                      "torch_sum_read_GBps": round(a.numel() / (float(np.median(times)) / 1e3) / 1e9, 1),
                       "note": "2 GiB device-to-device copy (torch; read + write bytes) and a torch sum "
-                              "over the same 2 GiB (read bytes), same run"}
+                              "over the same 2 GiB (read bytes), same run; the library's own streaming-read "
+                              "ceiling is roofline.measured_read_ceiling"}
     del a, x
     torch.cuda.empty_cache()
     return out
+
+
+def measure_read_ceiling(nbytes: int = 16 * 2 ** 30):
+    """The streaming-read rate this GPU reaches: the library's read probe
+    (kv_read_probe, the decode kernel's 16-byte nontemporal loads, 8 in flight
+    per thread) over a 16 GiB buffer, best median over a few grid sizes."""
+    import torch
+    from paper_2609_25782_amd import hotcold_kv as kv
+    dev = torch.device("cuda", 0)
+    buf = torch.zeros(nbytes, dtype=torch.uint8, device=dev)
+    out = torch.empty(1 << 16, dtype=torch.int32, device=dev)
+    best = None
+    for blocks in (2048, 4096, 8192, 16384, 65536):
+        times = []
+        for it in range(7):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            kv.kv_read_probe(buf.data_ptr(), nbytes, out.data_ptr(), blocks,
+                             torch.cuda.current_stream().cuda_stream)
+            e1.record()
+            torch.cuda.synchronize()
+            if it >= 2:
+                times.append(e0.elapsed_time(e1))
+        gbps = nbytes / (float(np.median(times)) / 1e3) / 1e9
+        if best is None or gbps > best["GBps"]:
+            best = {"GBps": round(gbps, 1), "blocks": blocks}
+    del buf, out
+    torch.cuda.empty_cache()
+    best.update({"bytes": nbytes, "method": "kv_read_probe: sequential 16-byte nontemporal loads, "
+                                            "events around one launch, best median over grid sizes"})
+    return best
 
 
 def measure_graph(seed: int, steps: int = 10, warmup: int = 3):
@@ -936,6 +968,10 @@ def main():
     pool.close()
     del pool
     torch.cuda.empty_cache()
+    ceiling = measure_read_ceiling()
+    log("streaming-read ceiling (library read probe): %.0f GB/s" % ceiling["GBps"])
+    result["roofline"]["measured_read_ceiling"] = ceiling
+    result["roofline"]["frac_of_measured_read_ceiling"] = round(k1_gbs / ceiling["GBps"], 4)
     if "resume48" in sections:
         result["resume48"] = measure_resume_mix(args.seed, max(3, args.steps // 4), 1)
         log("resume mix: %s" % json.dumps(result["resume48"]))

@@ -523,6 +523,19 @@ const char* kv_strerror(int status);
 const char* kv_last_error(void);
 
 /*
+ * Measurement context, not part of the KV path: a streaming read of `bytes`
+ * (a multiple of 16) of device memory at `buf` (16-byte aligned), with the
+ * 16-byte nontemporal loads the decode kernel uses and 8 of them in flight
+ * per thread, on `blocks` (1 .. 2^20) blocks of 256 threads.  Each block
+ * writes the XOR of what it read to out[block] (device, `blocks` words), so
+ * the reads cannot be elided.  Asynchronous on `stream`; time it with events
+ * around the call.  It gives the sequential-read rate this GPU reaches, the
+ * practical ceiling that the decode's random page reads are compared with.
+ * KV_ERR_INVALID for bad arguments.
+ */
+int kv_read_probe(const void* buf, size_t bytes, uint32_t* out, int32_t blocks, kv_stream_t stream);
+
+/*
  * Profiling hook.  When enabled, every timed kernel the pool launches (the ids
  * above) carries a pair of HIP events that its dispatch records at the kernel's
  * start and end (hipExtLaunchKernel), so a duration covers the kernel alone.

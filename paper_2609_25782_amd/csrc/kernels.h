@@ -112,6 +112,10 @@ hipError_t launch_slice_copy(const char* src_base, int64_t src_stride, char* dst
 
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t s);
 
+// Streaming read of `bytes` (a multiple of 16) at buf by `blocks` blocks; one
+// XOR word per block to out[0 .. blocks).
+hipError_t launch_read_probe(const void* buf, int64_t bytes, uint32_t* out, int32_t blocks, hipStream_t s);
+
 // page_table[e.pt_index] = e.pt_value for each of n entries with pt_index >= 0
 // (no copies): the second phase of a promotion.
 hipError_t launch_table_writes(const CopyEntry* entries, int32_t n, int32_t* page_table, hipStream_t s);

@@ -1514,6 +1514,16 @@ const char* kv_strerror(int status) {
 
 const char* kv_last_error(void) { return g_err.c_str(); }
 
+int kv_read_probe(const void* buf, size_t bytes, uint32_t* out, int32_t blocks, kv_stream_t stream) {
+    if (!buf || !out || bytes == 0 || bytes % 16 || (reinterpret_cast<uintptr_t>(buf) & 15) || blocks < 1 ||
+        blocks > (1 << 20))
+        return fail(KV_ERR_INVALID, "bad arguments");
+    hipError_t e = hck::launch_read_probe(buf, static_cast<int64_t>(bytes), out, blocks,
+                                          static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "read probe launch");
+    return KV_OK;
+}
+
 int kv_pool_set_profiling(kv_pool* pool, int enable) {
     if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
     if (pool->meta && enable) return fail(KV_ERR_INVALID, "metadata-only pool launches nothing");

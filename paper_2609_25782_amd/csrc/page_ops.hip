@@ -98,6 +98,37 @@ __global__ __launch_bounds__(kBlockThreads) void table_writes_kernel(const CopyE
     }
 }
 
+// Streaming read of a whole buffer: every thread keeps 8 nontemporal 16-byte
+// loads in flight and folds them into an XOR, one word per block, so the
+// loads cannot be dropped.  It measures the read rate the GPU reaches on
+// plain sequential data with the loads the decode kernel uses.
+__global__ __launch_bounds__(kBlockThreads) void read_probe_kernel(const u32x4* __restrict__ p, int64_t n16,
+                                                                   uint32_t* __restrict__ out) {
+    constexpr int U = 8;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlockThreads;
+    int64_t i = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x;
+    u32x4 acc = {0u, 0u, 0u, 0u};
+    for (; i + (U - 1) * stride < n16; i += U * stride) {
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(p + i + u * stride);
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc ^= v[u];
+    }
+    for (; i < n16; i += stride) acc ^= __builtin_nontemporal_load(p + i);
+    unsigned x = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) x ^= __shfl_xor(x, o);
+    __shared__ unsigned s_x[kBlockWaves];
+    if ((threadIdx.x & (kWave - 1)) == 0) s_x[threadIdx.x / kWave] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned r = 0;
+        for (int w = 0; w < kBlockWaves; ++w) r ^= s_x[w];
+        out[blockIdx.x] = r;
+    }
+}
+
 __global__ __launch_bounds__(kBlockThreads) void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; i < n;
          i += static_cast<int64_t>(gridDim.x) * kBlockThreads)
@@ -314,6 +345,13 @@ hipError_t launch_table_writes(const CopyEntry* entries, int32_t n, int32_t* pag
     if (n <= 0) return hipSuccess;
     hipLaunchKernelGGL(table_writes_kernel, dim3(grid_for(n, 1024)), dim3(kBlockThreads), 0, s, entries, n,
                        page_table);
+    return hipGetLastError();
+}
+
+hipError_t launch_read_probe(const void* buf, int64_t bytes, uint32_t* out, int32_t blocks, hipStream_t s) {
+    if (blocks <= 0 || bytes <= 0 || bytes % 16) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(read_probe_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kBlockThreads), 0, s,
+                       static_cast<const u32x4*>(buf), bytes / 16, out);
     return hipGetLastError();
 }
 

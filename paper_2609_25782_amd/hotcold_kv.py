@@ -98,6 +98,7 @@ _SIGS = {
     "kv_pool_set_decode_waves": (ctypes.c_int, [_P, _I32]),
     "kv_pool_set_decode_combine": (ctypes.c_int, [_P, _I32]),
     "kv_pool_set_decode_compute": (ctypes.c_int, [_P, _I32]),
+    "kv_read_probe": (ctypes.c_int, [_P, ctypes.c_size_t, _P, _I32, _P]),
     "paged_decode_workspace_bytes": (_SZ, [_P, _I32, _I32]),
     "paged_decode_attention": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _I32, _I32,
                                               ctypes.c_float, _P, _P, _SZ, _P]),
@@ -296,6 +297,10 @@ def kv_pool_set_decode_combine(pool: int, mode: int) -> None:
 
 def kv_pool_set_decode_compute(pool: int, mode: int) -> None:
     _check(_lib.kv_pool_set_decode_compute(pool, mode), "kv_pool_set_decode_compute")
+
+
+def kv_read_probe(buf: int, nbytes: int, out: int, blocks: int, stream: int = 0) -> None:
+    _check(_lib.kv_read_probe(buf, nbytes, out, blocks, stream), "kv_read_probe")
 
 
 def paged_decode_workspace_bytes(pool: int, batch: int, num_q_heads: int) -> int:
