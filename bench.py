@@ -521,6 +521,8 @@ def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
         del pool
         torch.cuda.empty_cache()
     out["graph_step48"] = measure_graph(seed)
+    out["append"] = measure_append(seed)
+    log("append: %s" % json.dumps(out["append"]))
     a = torch.empty(2 ** 31, dtype=torch.uint8, device=dev)
     b = torch.empty_like(a)
     times = []
@@ -550,6 +552,78 @@ def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
                               "over the same 2 GiB (read bytes), same run; the library's own streaming-read "
                               "ceiling is roofline.measured_read_ceiling"}
     del a, x
+    torch.cuda.empty_cache()
+    return out
+
+
+def measure_append(seed: int, steps: int = 20, warmup: int = 3):
+    """Data path 3 at the paper's shape (48 layers, 4 KV heads, 128, bf16): a
+    decode step appends one token to each of 32 sessions in every layer.  Times
+    the batched append (kv_append_tokens, one call per layer) against one
+    kv_write_tokens call per session and layer, and an 8,192-token prompt
+    written into one session (kv_write_tokens, one call per layer)."""
+    import torch
+    from paper_2609_25782_amd.pool import HotColdPool
+    B, NL, L0 = 32, 48, 1024
+    prompt = 8192
+    pages = B * ((L0 + steps + warmup + 16) // 16 + 1) + (prompt // 16 + 2)
+    pool = HotColdPool(NL, 4, 128, "bf16", pages, 0, B + 1, (L0 + steps + warmup + prompt) // 16 + 4)
+    dev = pool.device
+    sids = [pool.create_session(L0) for _ in range(B)]
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    k = torch.randn((B, 4, 128), generator=g, device=dev).to(torch.bfloat16)
+    v = torch.randn((B, 4, 128), generator=g, device=dev).to(torch.bfloat16)
+    lens = [L0] * B
+
+    def step(batched):
+        for i, sid in enumerate(sids):
+            lens[i] += 1
+            pool.extend(sid, lens[i])
+        for layer in range(NL):
+            if batched:
+                pool.append_tokens(layer, sids, [n - 1 for n in lens], k, v)
+            else:
+                for i, sid in enumerate(sids):
+                    pool.write_tokens(sid, layer, lens[i] - 1, k[i:i + 1], v[i:i + 1])
+
+    out = {"sessions": B, "layers": NL}
+    for batched in (True, False):
+        for _ in range(warmup):
+            step(batched)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record()
+        for _ in range(steps):
+            step(batched)
+        e1.record()
+        host = time.perf_counter() - t0
+        torch.cuda.synchronize()
+        name = "batched_append" if batched else "per_session_write"
+        out[name] = {"ms_per_step": round(e0.elapsed_time(e1) / steps, 4),
+                     "host_ms_per_step": round(1e3 * host / steps, 4),
+                     "calls_per_step": NL if batched else NL * B}
+    # a prompt of 8,192 tokens into one session, every layer
+    sid = pool.create_session(prompt)
+    kp = torch.randn((prompt, 4, 128), generator=g, device=dev).to(torch.bfloat16)
+    vp = torch.randn((prompt, 4, 128), generator=g, device=dev).to(torch.bfloat16)
+    for _ in range(2):
+        for layer in range(NL):
+            pool.write_tokens(sid, layer, 0, kp, vp)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        for layer in range(NL):
+            pool.write_tokens(sid, layer, 0, kp, vp)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 5
+    nbytes = 2 * prompt * 4 * 128 * 2 * NL          # K and V written (the same again read)
+    out["prompt_write"] = {"tokens": prompt, "ms": round(ms, 4), "bytes_written": nbytes,
+                           "GBps_written": round(nbytes / (ms / 1e3) / 1e9, 1)}
+    pool.close()
     torch.cuda.empty_cache()
     return out
 

@@ -307,6 +307,22 @@ int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin
                     const void* k, const void* v, kv_stream_t stream);
 
 /*
+ * Batched append for a decode step (data path 3, Sec. III): for one layer, row
+ * i of k and v (device arrays [n][num_kv_heads][head_dim], pool dtype) is
+ * token positions[i] of ACTIVE session sids[i] (host arrays, n <= 8192).  One
+ * launch writes every row.  Call kv_session_extend first so the positions lie
+ * inside the sessions.  A token on a spilled page is written to its cold page
+ * in place; hot pages written to lose their cold copy, as with kv_write_tokens.
+ * All rows are checked before anything is written or launched.  On a
+ * KV_POOL_METADATA_ONLY pool only the bookkeeping happens.
+ * Errors: KV_ERR_INVALID (bad layer, a position outside its session, the same
+ * token twice), KV_ERR_STATE (a session not ACTIVE, a spilled page shared with
+ * another session).
+ */
+int kv_append_tokens(kv_pool* pool, int32_t layer, const int32_t* sids, const int32_t* positions, int32_t n,
+                     const void* k, const void* v, kv_stream_t stream);
+
+/*
  * Test and benchmark input: fill every slot of an ACTIVE session's pages, all
  * layers, with counter-based pseudo-normal values.  Element (kind, layer, head,
  * token, dim) of logical session gen_sid gets value(seed, coordinate) computed

@@ -146,4 +146,28 @@ struct WriteArgs {
 };
 hipError_t launch_write_tokens(const WriteArgs& a, hipStream_t s);
 
+// Where one appended token goes: its page (a hot id, or KV_PAGE_COLD | cold id
+// for a spilled page) and its slot in the page.
+struct AppendEntry {
+    int32_t page;
+    int32_t slot;
+};
+
+// Batches up to this many rows carry their entries in the kernel arguments
+// (2 KiB), so a decode-step append needs no copy list and no staging slot.
+constexpr int kAppendInline = 256;
+
+struct AppendArgs {
+    char* hot;
+    char* cold;
+    int64_t page_bytes;
+    const AppendEntry* entries;  // device [n] when n > kAppendInline
+    int32_t n;
+    int32_t num_kv_heads, head_dim, dtype, layer;
+    const void* k;               // [n][num_kv_heads][head_dim]
+    const void* v;
+    AppendEntry inline_entries[kAppendInline];  // the entries when n <= kAppendInline
+};
+hipError_t launch_append_tokens(const AppendArgs& a, hipStream_t s);
+
 }  // namespace hck

@@ -847,6 +847,84 @@ int kv_session_info(const kv_pool* pool, int32_t sid, int32_t* state, int32_t* s
     return KV_OK;
 }
 
+int kv_append_tokens(kv_pool* pool, int32_t layer, const int32_t* sids, const int32_t* positions, int32_t n,
+                     const void* k, const void* v, kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    if (layer < 0 || layer >= pool->d.num_layers) return fail(KV_ERR_INVALID, "bad layer %d", layer);
+    if (n < 0 || n > kMaxDecodeBatch || (n > 0 && (!sids || !positions)))
+        return fail(KV_ERR_INVALID, "bad arguments");
+    if (n == 0) return KV_OK;
+    std::vector<std::pair<int32_t, int32_t>> seen(static_cast<size_t>(n));
+    for (int32_t i = 0; i < n; ++i) {
+        const Session* s = pool->session(sids[i]);
+        if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sids[i]);
+        if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sids[i]);
+        if (positions[i] < 0 || positions[i] >= s->seq_len)
+            return fail(KV_ERR_INVALID, "token %d outside session %d", positions[i], sids[i]);
+        const int32_t p = positions[i] / KV_PAGE_TOKENS;
+        if (s->hot[p] < 0 && pool->cold_ref[s->cold[p]] > 1)
+            return fail(KV_ERR_STATE, "page %d is spilled to a cold page shared with another session", p);
+        seen[i] = {sids[i], positions[i]};
+    }
+    std::sort(seen.begin(), seen.end());
+    for (int32_t i = 1; i < n; ++i)
+        if (seen[i] == seen[i - 1]) return fail(KV_ERR_INVALID, "token %d of session %d given twice",
+                                                seen[i].second, seen[i].first);
+    if (!pool->meta) {
+        if (!k || !v) return fail(KV_ERR_INVALID, "NULL k or v");
+        DeviceGuard g(pool->d.device);
+        hipStream_t st = pool->strm(stream);
+        // short lists travel in the kernel arguments, longer ones through a staging slot
+        hck::AppendArgs a;
+        StagingSlot* slot = nullptr;
+        hck::AppendEntry* ent = a.inline_entries;
+        if (n > hck::kAppendInline) {
+            int rc = pool->acquire_slot(&slot);
+            if (rc) return rc;
+            ent = static_cast<hck::AppendEntry*>(slot->host);
+        }
+        for (int32_t i = 0; i < n; ++i) {
+            const Session& s = pool->sessions[sids[i]];
+            const int32_t p = positions[i] / KV_PAGE_TOKENS;
+            ent[i].page = s.hot[p] >= 0 ? s.hot[p] : (s.cold[p] | KV_PAGE_COLD);
+            ent[i].slot = positions[i] % KV_PAGE_TOKENS;
+        }
+        a.entries = nullptr;
+        if (slot) {
+            hipError_t e = hipMemcpyAsync(slot->dev, slot->host, static_cast<size_t>(n) * sizeof(hck::AppendEntry),
+                                          hipMemcpyHostToDevice, st);
+            if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(append list)");
+            a.entries = static_cast<const hck::AppendEntry*>(slot->dev);
+        }
+        a.hot = pool->hot;
+        a.cold = pool->cold;
+        a.page_bytes = pool->page_bytes;
+        a.n = n;
+        a.num_kv_heads = pool->d.num_kv_heads;
+        a.head_dim = pool->d.head_dim;
+        a.dtype = pool->d.dtype;
+        a.layer = layer;
+        a.k = k;
+        a.v = v;
+        hipError_t e = hck::launch_append_tokens(a, st);
+        if (e != hipSuccess) return hip_fail(e, "append_tokens launch");
+        if (slot) {
+            e = hipEventRecord(slot->done, st);
+            if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
+            slot->pending = true;
+        }
+    }
+    for (int32_t i = 0; i < n; ++i) {      // a written hot page loses its cold copy
+        Session& s = pool->sessions[sids[i]];
+        const int32_t p = positions[i] / KV_PAGE_TOKENS;
+        if (s.hot[p] >= 0 && s.cold[p] >= 0) {
+            pool->release_cold(s.cold[p]);
+            s.cold[p] = -1;
+        }
+    }
+    return KV_OK;
+}
+
 int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin, int32_t n_tok,
                     const void* k, const void* v, kv_stream_t stream) {
     if (!pool) return fail(KV_ERR_INVALID, "NULL pool");

@@ -222,36 +222,104 @@ __global__ __launch_bounds__(kBlockThreads) void fill_synthetic_kernel(SynthArgs
 }
 
 // One thread per (token, KV head, 16-byte group of dims).
+// One 16-byte group of dims (x elements) of one token's K and V into the
+// (layer, KV head) slice `lh` of its page, token slot `slot`: K is a 16-byte
+// store (the group is contiguous in the K tile); V, dims-major and
+// token-minor, takes one element store per dim.
+__device__ __forceinline__ void write_token_group(char* lh, int64_t tile, int slot, int cd, int x, int elt,
+                                                  const char* ksrc, const char* vsrc) {
+    *reinterpret_cast<u32x4*>(lh + (static_cast<int64_t>(cd) * kPageTokens + slot) * x * elt) =
+        *reinterpret_cast<const u32x4*>(ksrc);
+    char* vt = lh + tile;
+    for (int j = 0; j < x; ++j) {
+        const int64_t e = static_cast<int64_t>(cd * x + j) * kPageTokens + slot;
+        if (elt == 2)
+            *reinterpret_cast<unsigned short*>(vt + e * 2) = reinterpret_cast<const unsigned short*>(vsrc)[j];
+        else
+            *reinterpret_cast<unsigned*>(vt + e * 4) = reinterpret_cast<const unsigned*>(vsrc)[j];
+    }
+}
+
+// Tokens [tok_begin, tok_begin + n_tok) of one layer: one block per (page,
+// KV head).  The page's tokens in the range are read from the source rows
+// ([token][kv_head][head_dim], each token's dims contiguous) into LDS with
+// 16-byte loads, then written out in the tile layouts with 16-byte stores: K
+// as groups of x dims, consecutive threads on consecutive tokens; V transposed
+// to dims-major rows of 16 tokens.  Slots of the page outside the range keep
+// their bytes: a V store that would cover one of them is done element by
+// element instead.
+template <typename T>
 __global__ __launch_bounds__(kBlockThreads) void write_tokens_kernel(WriteArgs a) {
+    constexpr int x = 16 / sizeof(T);            // elements per 16 bytes
+    constexpr int kMaxD = 128;
+    __shared__ __align__(16) T s_k[kPageTokens][kMaxD + x];
+    __shared__ __align__(16) T s_v[kPageTokens][kMaxD + x];
+    const int D = a.head_dim;
+    const int groups = D / x;
+    const int64_t tile = static_cast<int64_t>(kPageTokens) * D * sizeof(T);
+    const int p0 = a.tok_begin / kPageTokens;
+    const int page = p0 + static_cast<int>(blockIdx.x);
+    const int head = static_cast<int>(blockIdx.y);
+    const int t_base = page * kPageTokens;
+    const int s0 = max(a.tok_begin, t_base) - t_base;                       // first slot written
+    const int s1 = min(a.tok_begin + a.n_tok, t_base + kPageTokens) - t_base;  // one past the last
+    const int tid = threadIdx.x;
+    for (int e = tid; e < kPageTokens * groups; e += kBlockThreads) {
+        const int t = e / groups, cd = e % groups;
+        if (t < s0 || t >= s1) continue;
+        const int64_t src = (static_cast<int64_t>(t_base + t - a.tok_begin) * a.num_kv_heads + head) * D + cd * x;
+        *reinterpret_cast<u32x4*>(&s_k[t][cd * x]) = *reinterpret_cast<const u32x4*>(static_cast<const T*>(a.k) + src);
+        *reinterpret_cast<u32x4*>(&s_v[t][cd * x]) = *reinterpret_cast<const u32x4*>(static_cast<const T*>(a.v) + src);
+    }
+    __syncthreads();
+    char* lh = page_address(a.hot, a.cold, a.row[page], a.page_bytes) +
+               (static_cast<int64_t>(a.layer) * a.num_kv_heads + head) * 2 * tile;
+    // K tile: [group][token][x]
+    for (int e = tid; e < groups * kPageTokens; e += kBlockThreads) {
+        const int cd = e / kPageTokens, t = e % kPageTokens;
+        if (t < s0 || t >= s1) continue;
+        *reinterpret_cast<u32x4*>(lh + (static_cast<int64_t>(cd) * kPageTokens + t) * 16) =
+            *reinterpret_cast<const u32x4*>(&s_k[t][cd * x]);
+    }
+    // V tile: [dim][token]; one 16-byte store covers x consecutive tokens of a dim
+    constexpr int kChunks = kPageTokens / x;
+    T* vt = reinterpret_cast<T*>(lh + tile);
+    for (int e = tid; e < D * kChunks; e += kBlockThreads) {
+        const int d = e / kChunks, c = e % kChunks;
+        const int t0 = c * x;
+        if (t0 + x <= s0 || t0 >= s1) continue;
+        if (t0 >= s0 && t0 + x <= s1) {
+            T w[x];
+#pragma unroll
+            for (int j = 0; j < x; ++j) w[j] = s_v[t0 + j][d];
+            *reinterpret_cast<u32x4*>(vt + static_cast<int64_t>(d) * kPageTokens + t0) =
+                *reinterpret_cast<const u32x4*>(w);
+        } else {
+            for (int j = 0; j < x; ++j)
+                if (t0 + j >= s0 && t0 + j < s1) vt[static_cast<int64_t>(d) * kPageTokens + t0 + j] = s_v[t0 + j][d];
+        }
+    }
+}
+
+// Row r of the batch: one token into page e[r].page (a hot id, or a cold id
+// tagged KV_PAGE_COLD) at slot e[r].slot; K and V rows [n][kv_heads][head_dim].
+__global__ __launch_bounds__(kBlockThreads) void append_tokens_kernel(const AppendArgs a) {
     const int elt = a.dtype == kDtypeBf16 ? 2 : 4;
     const int x = 16 / elt;
     const int groups = a.head_dim / x;
     const int64_t tile = static_cast<int64_t>(kPageTokens) * a.head_dim * elt;
-    const int64_t total = static_cast<int64_t>(a.n_tok) * a.num_kv_heads * groups;
+    const int64_t total = static_cast<int64_t>(a.n) * a.num_kv_heads * groups;
     for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; gi < total;
          gi += static_cast<int64_t>(gridDim.x) * kBlockThreads) {
         const int cd = static_cast<int>(gi % groups);
         const int head = static_cast<int>((gi / groups) % a.num_kv_heads);
-        const int tok = static_cast<int>(gi / (static_cast<int64_t>(groups) * a.num_kv_heads));
-        const int t = a.tok_begin + tok;
-        const int32_t pid = a.row[t / kPageTokens];
-        const int slot = t % kPageTokens;
-        char* lh = page_address(a.hot, a.cold, pid, a.page_bytes) +
+        const int r = static_cast<int>(gi / (static_cast<int64_t>(groups) * a.num_kv_heads));
+        const AppendEntry e = a.n <= kAppendInline ? a.inline_entries[r] : a.entries[r];
+        char* lh = page_address(a.hot, a.cold, e.page, a.page_bytes) +
                    (static_cast<int64_t>(a.layer) * a.num_kv_heads + head) * 2 * tile;
-        const int64_t src_elem = (static_cast<int64_t>(tok) * a.num_kv_heads + head) * a.head_dim + cd * x;
-        // K: the group's x dims are contiguous in the tile
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.k) + src_elem * elt);
-        *reinterpret_cast<u32x4*>(lh + (static_cast<int64_t>(cd) * kPageTokens + slot) * x * elt) = kv;
-        // V: dims-major, token-minor
-        const char* vs = static_cast<const char*>(a.v) + src_elem * elt;
-        char* vt = lh + tile;
-        for (int j = 0; j < x; ++j) {
-            const int64_t e = static_cast<int64_t>(cd * x + j) * kPageTokens + slot;
-            if (elt == 2)
-                *reinterpret_cast<unsigned short*>(vt + e * 2) = reinterpret_cast<const unsigned short*>(vs)[j];
-            else
-                *reinterpret_cast<unsigned*>(vt + e * 4) = reinterpret_cast<const unsigned*>(vs)[j];
-        }
+        const int64_t src = ((static_cast<int64_t>(r) * a.num_kv_heads + head) * a.head_dim + cd * x) * elt;
+        write_token_group(lh, tile, e.slot, cd, x, elt, static_cast<const char*>(a.k) + src,
+                          static_cast<const char*>(a.v) + src);
     }
 }
 
@@ -369,10 +437,22 @@ hipError_t launch_fill_synthetic(const SynthArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_write_tokens(const WriteArgs& a, hipStream_t s) {
+    if (a.n_tok <= 0) return hipSuccess;
+    if (a.head_dim > 128 || a.head_dim % 16) return hipErrorInvalidValue;
+    const int pages = (a.tok_begin + a.n_tok - 1) / kPageTokens - a.tok_begin / kPageTokens + 1;
+    const dim3 grid(static_cast<unsigned>(pages), static_cast<unsigned>(a.num_kv_heads));
+    if (a.dtype == kDtypeBf16)
+        hipLaunchKernelGGL(write_tokens_kernel<unsigned short>, grid, dim3(kBlockThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(write_tokens_kernel<unsigned>, grid, dim3(kBlockThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_append_tokens(const AppendArgs& a, hipStream_t s) {
     const int x = a.dtype == kDtypeBf16 ? 8 : 4;
-    const int64_t work = static_cast<int64_t>(a.n_tok) * a.num_kv_heads * (a.head_dim / x);
+    const int64_t work = static_cast<int64_t>(a.n) * a.num_kv_heads * (a.head_dim / x);
     if (work <= 0) return hipSuccess;
-    hipLaunchKernelGGL(write_tokens_kernel, dim3(grid_for(work, 16384)), dim3(kBlockThreads), 0, s, a);
+    hipLaunchKernelGGL(append_tokens_kernel, dim3(grid_for(work, 16384)), dim3(kBlockThreads), 0, s, a);
     return hipGetLastError();
 }
 

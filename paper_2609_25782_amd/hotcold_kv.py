@@ -81,6 +81,7 @@ _SIGS = {
     "kv_session_destroy": (ctypes.c_int, [_P, _I32, _P]),
     "kv_session_info": (ctypes.c_int, [_P, _I32, _PI32, _PI32, _PI32, _PI32, _I32]),
     "kv_write_tokens": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P]),
+    "kv_append_tokens": (ctypes.c_int, [_P, _I32, _P, _P, _I32, _P, _P, _P]),
     "kv_fill_synthetic": (ctypes.c_int, [_P, _I32, _I32, _U64, ctypes.c_float, _P]),
     "kv_fill_synthetic_pages": (ctypes.c_int, [_P, _I32, _I32, _U64, ctypes.c_float, _I32, _I32, _P]),
     "kv_evict_session": (ctypes.c_int, [_P, _I32, _P]),
@@ -212,6 +213,18 @@ def kv_write_tokens(pool: int, sid: int, layer: int, tok_begin: int, n_tok: int,
                     v_ptr: int, stream: int = 0) -> None:
     _check(_lib.kv_write_tokens(pool, sid, layer, tok_begin, n_tok, k_ptr or None, v_ptr or None,
                                 stream or None), "kv_write_tokens")
+
+
+def kv_append_tokens(pool: int, layer: int, sids, positions, k: int, v: int, stream: int = 0) -> None:
+    sids = [int(x) for x in sids]
+    positions = [int(x) for x in positions]
+    if len(sids) != len(positions):
+        raise ValueError("sids and positions differ in length")
+    n = len(sids)
+    sa = (ctypes.c_int32 * max(n, 1))(*sids)
+    pa = (ctypes.c_int32 * max(n, 1))(*positions)
+    _check(_lib.kv_append_tokens(pool, layer, sa, pa, n, k or None, v or None, stream or None),
+           "kv_append_tokens")
 
 
 def kv_fill_synthetic(pool: int, sid: int, gen_sid: int, seed: int, value_mult: float,

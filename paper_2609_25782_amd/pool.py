@@ -95,6 +95,12 @@ class HotColdPool:
         kv.kv_write_tokens(self.handle, sid, layer, tok_begin, k.shape[0], k.data_ptr(), v.data_ptr(),
                            _stream(stream))
 
+    def append_tokens(self, layer: int, sids, positions, k: torch.Tensor, v: torch.Tensor, stream=None) -> None:
+        """One token per row: row i of k and v is token positions[i] of session sids[i]."""
+        assert k.is_contiguous() and v.is_contiguous() and k.shape == v.shape and k.shape[0] == len(sids)
+        assert k.dtype == self.torch_dtype and k.device == self.device
+        kv.kv_append_tokens(self.handle, layer, sids, positions, k.data_ptr(), v.data_ptr(), _stream(stream))
+
     def fill_synthetic(self, sid: int, gen_sid: int, seed: int, value_mult: float, stream=None) -> None:
         kv.kv_fill_synthetic(self.handle, sid, gen_sid, seed, float(value_mult), _stream(stream))
 

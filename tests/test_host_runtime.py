@@ -5,7 +5,7 @@ random call sequences, and no state change on any failing call (CPU only)."""
 import numpy as np
 import pytest
 
-from oracle.pool_model import ACTIVE, ModelError, PoolModel
+from oracle.pool_model import ACTIVE, ERR_INVALID, ERR_STATE, PAGE_TOKENS, ModelError, PoolModel
 
 
 def _lib():
@@ -44,9 +44,36 @@ def _same(kv, pool, model, ms):
     assert st["cold_active_pages"] == model.cold_active()
 
 
+def _model_append(m, sids, positions):
+    """kv_append_tokens on the model: every row is checked first, in order
+    (session id, state, position, shared spilled page), then duplicates; then
+    each row is a one-token write."""
+    for sid, pos in zip(sids, positions):
+        s = m._session(sid)
+        if s.state != ACTIVE:
+            raise ModelError(ERR_STATE, "not active")
+        if not 0 <= pos < s.seq_len:
+            raise ModelError(ERR_INVALID, "token outside the session")
+        p = pos // PAGE_TOKENS
+        if s.hot[p] < 0 and m.cold_ref[s.cold[p]] > 1:
+            raise ModelError(ERR_STATE, "spilled page shared with another session")
+    if len(set(zip(sids, positions))) != len(sids):
+        raise ModelError(ERR_INVALID, "token given twice")
+    for sid, pos in zip(sids, positions):
+        m.write_tokens(sid, pos, 1)
+
+
 def _random_call(kv, pool, rng, nh, nc, ms, stride):
     """One random call as a (model call, library call) pair."""
-    op = int(rng.integers(0, 12))
+    op = int(rng.integers(0, 13))
+    if op == 12:
+        n = int(rng.integers(1, 6))
+        sids = [int(x) for x in rng.integers(-1, ms + 1, size=n)]
+        positions = [int(x) for x in rng.integers(-1, 16 * stride + 2, size=n)]
+        if rng.random() < 0.1:
+            sids, positions = sids + sids[:1], positions + positions[:1]
+        return (lambda m: _model_append(m, sids, positions)), \
+            (lambda: kv.kv_append_tokens(pool, 0, sids, positions, 0, 0))
     sid = int(rng.integers(-1, ms + 1))
     if op == 0:
         L = int(rng.integers(-2, 16 * stride + 20))
@@ -151,6 +178,38 @@ def test_metadata_write_drops_cold_copies():
     kv.kv_evict_session(pool, a)
     st = kv.kv_pool_stats_get(pool)
     assert st["pages_to_cold"] == 5 and kv.kv_session_info(pool, a)[3] == [0, 1, 2]
+    kv.kv_pool_destroy(pool)
+
+
+def test_metadata_append_drops_cold_copies_and_checks_every_row():
+    """A batched append is bookkeeping on a metadata-only pool: each row's page
+    loses its cold copy.  A bad row anywhere refuses the whole call and changes
+    nothing."""
+    kv = _lib()
+    pool = _meta_pool(kv, 12, 12, 3, 4)
+    a = kv.kv_session_create(pool, 40)
+    b = kv.kv_session_create(pool, 20)
+    kv.kv_evict_sessions(pool, [a, b])
+    kv.kv_resume_sessions(pool, [a, b])
+    cold_a, cold_b = kv.kv_session_info(pool, a)[3], kv.kv_session_info(pool, b)[3]
+    assert -1 not in cold_a + cold_b
+    for sids, pos, code in (([a, b], [39, 20], kv.KV_ERR_INVALID),     # past b's length
+                            ([a, a], [5, 5], kv.KV_ERR_INVALID),       # the same token twice
+                            ([a, 2], [5, 0], kv.KV_ERR_STATE),         # row 2 not in use
+                            ([a, 9], [5, 0], kv.KV_ERR_INVALID)):      # bad session id
+        with pytest.raises(kv.KVError) as e:
+            kv.kv_append_tokens(pool, 0, sids, pos, 0, 0)
+        assert e.value.status == code
+    assert kv.kv_session_info(pool, a)[3] == cold_a and kv.kv_session_info(pool, b)[3] == cold_b
+    kv.kv_append_tokens(pool, 0, [a, b, a], [39, 0, 31], 0, 0)  # a: page 2 and page 1; b: page 0
+    assert kv.kv_session_info(pool, a)[3] == [cold_a[0], -1, -1]
+    assert kv.kv_session_info(pool, b)[3] == [-1, cold_b[1]]
+    before = kv.kv_pool_stats_get(pool)["pages_to_cold"]
+    kv.kv_evict_sessions(pool, [a, b])
+    assert kv.kv_pool_stats_get(pool)["pages_to_cold"] - before == 3
+    with pytest.raises(kv.KVError) as e:                       # paused now
+        kv.kv_append_tokens(pool, 0, [a], [0], 0, 0)
+    assert e.value.status == kv.KV_ERR_STATE
     kv.kv_pool_destroy(pool)
 
 
