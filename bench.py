@@ -556,6 +556,56 @@ def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
     return out
 
 
+def measure_evict(seed: int, reps: int = 3):
+    """Write-on-evict at 48 layers (data path 4): 8 sessions of 8K-32K tokens
+    whose pages have no cold copy are evicted in one call (every page copied hot
+    -> cold), resumed, refilled (which drops the cold copies again), and so on.
+    Also the eviction of the same sessions right after a resume, when every
+    page still has its cold copy: no page is written."""
+    import torch
+    import synth
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+    rng = np.random.Generator(np.random.PCG64([seed, 13]))
+    lens = [int(x) for x in rng.integers(8192, 32768, size=8, endpoint=True)]
+    n_pages = sum(synth.pages_for(L) for L in lens)
+    pool = HotColdPool(48, 4, 128, "bf16", n_pages + 8, n_pages + 8, 8, synth.pages_for(32768))
+    mult = float(synth.value_multiplier(1.0 / math.sqrt(128)))
+    sids = [pool.create_session(L) for L in lens]
+    payload = n_pages * pool.page_bytes
+    dirty, clean = [], []
+    for r in range(reps + 1):
+        for j, sid in enumerate(sids):
+            pool.fill_synthetic(sid, j, seed, mult)
+        torch.cuda.synchronize()
+        kv.kv_pool_set_profiling(pool.handle, True)
+        kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_EVICT_COPY)
+        pool.evict(sids)
+        n, ms = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_EVICT_COPY)
+        pool.resume(sids)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        pool.evict(sids)                    # clean: the cold copies are still valid
+        e1.record()
+        torch.cuda.synchronize()
+        kv.kv_pool_set_profiling(pool.handle, False)
+        pool.resume(sids)
+        if r > 0:                           # the first round warms up
+            dirty.append(ms)
+            clean.append(e0.elapsed_time(e1))
+    st = pool.stats()
+    pool.close()
+    torch.cuda.empty_cache()
+    d = float(np.median(dirty))
+    return {"sessions": 8, "layers": 48, "payload_bytes": payload,
+            "dirty_evict_ms": round(d, 3), "dirty_ms_per_session": round(d / 8, 4),
+            "copy_GBps": round(2 * payload / (d / 1e3) / 1e9, 1),
+            "frac_of_copy_roofline": round(2 * payload / (d / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+            "clean_evict_ms": round(float(np.median(clean)), 4),
+            "cold_writes_total": st["pages_to_cold"]}
+
+
 def measure_append(seed: int, steps: int = 20, warmup: int = 3):
     """Data path 3 at the paper's shape (48 layers, 4 KV heads, 128, bf16): a
     decode step appends one token to each of 32 sessions in every layer.  Times
@@ -1049,6 +1099,8 @@ def main():
     if "resume48" in sections:
         result["resume48"] = measure_resume_mix(args.seed, max(3, args.steps // 4), 1)
         log("resume mix: %s" % json.dumps(result["resume48"]))
+        result["evict48"] = measure_evict(args.seed)
+        log("write-on-evict: %s" % json.dumps(result["evict48"]))
     if "host" in sections:
         result["resume_host_tier"] = measure_host_tier(args.seed)
         log("host tier: %s" % json.dumps(result["resume_host_tier"]))

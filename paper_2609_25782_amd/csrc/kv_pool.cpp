@@ -319,9 +319,24 @@ struct kv_pool {
         }
     }
 
-    // Enqueue page copies (in chunks that fit a staging slot).
-    int submit_copies(const char* src, char* dst, const std::vector<hck::CopyEntry>& entries,
+    // Enqueue page copies (in chunks that fit a staging slot).  Entries that
+    // only write the page table (rows cleared on eviction, resident pages
+    // remapped on resume) go to the table-write kernel instead, so the copy
+    // grid only walks pages that move.
+    int submit_copies(const char* src, char* dst, const std::vector<hck::CopyEntry>& all,
                       hipStream_t s, int kernel_id) {
+        std::vector<hck::CopyEntry> entries, writes;
+        entries.reserve(all.size());
+        for (const hck::CopyEntry& e : all) {
+            if (e.src >= 0)
+                entries.push_back(e);
+            else if (e.pt_index >= 0)
+                writes.push_back(e);
+        }
+        if (!writes.empty()) {
+            int rc = submit_table_writes(writes, s);
+            if (rc) return rc;
+        }
         for (size_t off = 0; off < entries.size(); off += kStagingEntries) {
             const int32_t n = static_cast<int32_t>(
                 std::min<size_t>(kStagingEntries, entries.size() - off));
