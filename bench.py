@@ -379,7 +379,76 @@ def measure_host_tier(seed: int):
         pool.close()
         del pool
         torch.cuda.empty_cache()
+    out["beside_decode"] = measure_host_overlap(seed)
     return out
+
+
+def measure_host_overlap(seed: int):
+    """A 48-layer session of 32K tokens (3.2 GB) resumed from the pinned-host
+    tier on one stream while another stream decodes 32 active sessions of 8K
+    tokens (48 layers, three steps), with the host-tier copies on the DMA
+    engines (the default) and in the copy kernel."""
+    import torch
+    from paper_2609_25782_amd.pool import HotColdPool
+    B, L, LR = 32, 8192, 32768
+    pool = HotColdPool(48, 4, 128, "bf16", B * (L // 16) + LR // 16 + 64, LR // 16 + 8, B + 1, LR // 16,
+                       cold_location="host")
+    dev = pool.device
+    for b in range(B):
+        pool.create_session(L)
+        pool.fill_synthetic(b, b, seed, 0.01)
+    r = pool.create_session(LR)
+    pool.evict([r])
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    q = torch.randn((B, 32, 128), generator=g, device=dev).to(torch.bfloat16)
+    sl = torch.full((B,), L, dtype=torch.int32, device=dev)
+    pt = pool.page_table[:B]
+    out_t = torch.empty_like(q)
+    dec_s, res_s = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    def decode_steps(n):
+        for _ in range(n):
+            for layer in range(48):
+                pool.decode(layer, q, sl, page_table=pt, out=out_t, stream=dec_s)
+
+    decode_steps(2)
+    torch.cuda.synchronize()
+    e0, e1 = ev(), ev()
+    e0.record(dec_s)
+    decode_steps(3)
+    e1.record(dec_s)
+    torch.cuda.synchronize()
+    res = {"decode48_ms_alone": round(e0.elapsed_time(e1) / 3, 3), "resume_bytes": (LR // 16) * pool.page_bytes}
+    for name, kernel in (("dma", False), ("kernel", True)):
+        pool.set_host_copy(kernel)
+        r0, r1 = ev(), ev()
+        r0.record(res_s)
+        pool.resume([r], stream=res_s)
+        r1.record(res_s)
+        torch.cuda.synchronize()
+        alone = r0.elapsed_time(r1)
+        pool.evict([r], stream=res_s)
+        torch.cuda.synchronize()
+        r0, r1, d0, d1 = ev(), ev(), ev(), ev()
+        r0.record(res_s)
+        pool.resume([r], stream=res_s)
+        r1.record(res_s)
+        d0.record(dec_s)
+        decode_steps(3)
+        d1.record(dec_s)
+        torch.cuda.synchronize()
+        res[name] = {"resume_ms_alone": round(alone, 2), "resume_ms_beside": round(r0.elapsed_time(r1), 2),
+                     "decode48_ms_beside": round(d0.elapsed_time(d1) / 3, 3)}
+        pool.evict([r], stream=res_s)
+        torch.cuda.synchronize()
+    pool.set_host_copy(False)
+    pool.close()
+    torch.cuda.empty_cache()
+    return res
 
 
 def measure_agentic_replay(seed: int, plateau_s: float = 20.0):

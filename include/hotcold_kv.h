@@ -387,6 +387,22 @@ int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_
  */
 int kv_pool_set_copy_blocks(kv_pool* pool, int32_t blocks);
 
+enum kv_host_copy {
+    KV_HOST_COPY_DMA = 0,    /* the GPU's DMA engines, one copy per run of consecutive pages
+                                (default) */
+    KV_HOST_COPY_KERNEL = 1  /* the page-copy kernel reading or writing host memory over PCIe */
+};
+/*
+ * How whole-page copies between a pinned-host cold pool and the hot pool
+ * (resume, eviction, promotion) are done.  Both reach PCIe bandwidth alone
+ * (the kernel somewhat more when pages are scattered), but copy waves waiting
+ * on PCIe hold the CUs' memory pipelines and slow a decode running meanwhile
+ * on another stream many times over, while the DMA engines use no CU.  The
+ * one-layer gathers of paged_decode_prefetch always use the kernel.  No effect
+ * on a device-memory cold pool.  KV_ERR_INVALID for other modes.
+ */
+int kv_pool_set_host_copy(kv_pool* pool, int32_t mode);
+
 /* ----------------------------------------------------------------------- */
 /* Decode attention (data path 1)                                           */
 /* ----------------------------------------------------------------------- */

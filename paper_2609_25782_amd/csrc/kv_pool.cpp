@@ -200,6 +200,8 @@ struct kv_pool {
     bool free_pending = false;
     bool profiling = false;
     int32_t combine_mode = KV_COMBINE_SEPARATE;
+    char* cold_host = nullptr;      // host address of a pinned-host cold pool (null otherwise)
+    int32_t host_copy = KV_HOST_COPY_DMA;
     int32_t compute_mode = KV_DECODE_MATRIX;
     int32_t* counters = nullptr;  // decode arrival counters, zero between calls
     hipEvent_t decode_event = nullptr;
@@ -337,6 +339,8 @@ struct kv_pool {
             int rc = submit_table_writes(writes, s);
             if (rc) return rc;
         }
+        if (cold_host && host_copy == KV_HOST_COPY_DMA && (src == cold || dst == cold))
+            return submit_dma_copies(src, dst, entries, s, kernel_id);
         for (size_t off = 0; off < entries.size(); off += kStagingEntries) {
             const int32_t n = static_cast<int32_t>(
                 std::min<size_t>(kStagingEntries, entries.size() - off));
@@ -361,6 +365,40 @@ struct kv_pool {
     }
 
     // Enqueue page-table element writes only (entries' pt_index / pt_value).
+    // Page copies to or from a pinned-host cold pool on the DMA engines: one
+    // hipMemcpyAsync per run of pages consecutive on both sides, then the
+    // page-table entries (stream-ordered after the copies).  A copy kernel
+    // reading or writing host memory keeps its waves waiting on PCIe in the
+    // CUs' memory pipelines, which slows a decode running on another stream
+    // many times over; the DMA engines use no CU.
+    int submit_dma_copies(const char* src, char* dst, const std::vector<hck::CopyEntry>& entries,
+                          hipStream_t s, int kernel_id) {
+        if (entries.empty()) return KV_OK;
+        const bool to_host = dst == cold;
+        const char* src_base = to_host ? src : cold_host;
+        char* dst_base = to_host ? cold_host : dst;
+        const hipMemcpyKind kind = to_host ? hipMemcpyDeviceToHost : hipMemcpyHostToDevice;
+        const hck::LaunchEvents ev = prof_events();
+        hipError_t e = ev.start ? hipEventRecord(ev.start, s) : hipSuccess;
+        for (size_t i = 0; i < entries.size() && e == hipSuccess;) {
+            size_t j = i + 1;
+            while (j < entries.size() && entries[j].src == entries[j - 1].src + 1 &&
+                   entries[j].dst == entries[j - 1].dst + 1)
+                ++j;
+            e = hipMemcpyAsync(dst_base + static_cast<int64_t>(entries[i].dst) * page_bytes,
+                               src_base + static_cast<int64_t>(entries[i].src) * page_bytes,
+                               static_cast<size_t>(j - i) * page_bytes, kind, s);
+            i = j;
+        }
+        if (e == hipSuccess && ev.stop) e = hipEventRecord(ev.stop, s);
+        prof_done(kernel_id, ev, e);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(host-tier pages)");
+        std::vector<hck::CopyEntry> writes;
+        for (const hck::CopyEntry& c : entries)
+            if (c.pt_index >= 0) writes.push_back(hck::CopyEntry{-1, -1, c.pt_index, c.pt_value});
+        return writes.empty() ? KV_OK : submit_table_writes(writes, s);
+    }
+
     int submit_table_writes(const std::vector<hck::CopyEntry>& entries, hipStream_t s) {
         for (size_t off = 0; off < entries.size(); off += kStagingEntries) {
             const int32_t n = static_cast<int32_t>(std::min<size_t>(kStagingEntries, entries.size() - off));
@@ -617,6 +655,7 @@ int kv_pool_create(const kv_pool_desc* desc, void* hot_base, size_t hot_bytes, v
                 return hip_fail(e, "hipHostGetDevicePointer(cold pool)");
             }
             p->cold = static_cast<char*>(dp);
+            p->cold_host = static_cast<char*>(cold_base);
         } else {
             p->cold = static_cast<char*>(cold_base);
         }
@@ -1303,6 +1342,13 @@ int kv_pool_set_decode_combine(kv_pool* pool, int32_t mode) {
     if (!pool || (mode != KV_COMBINE_SEPARATE && mode != KV_COMBINE_FUSED))
         return fail(KV_ERR_INVALID, "bad arguments");
     pool->combine_mode = mode;
+    return KV_OK;
+}
+
+int kv_pool_set_host_copy(kv_pool* pool, int32_t mode) {
+    if (!pool || (mode != KV_HOST_COPY_DMA && mode != KV_HOST_COPY_KERNEL))
+        return fail(KV_ERR_INVALID, "bad arguments");
+    pool->host_copy = mode;
     return KV_OK;
 }
 

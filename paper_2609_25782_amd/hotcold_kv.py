@@ -29,6 +29,7 @@ KV_KERNEL_PREFETCH_COPY, KV_KERNEL_COUNT = 4, 5
 KV_PAGE_COLD, KV_PAGE_STAGED = 1 << 30, 1 << 29
 KV_COMBINE_SEPARATE, KV_COMBINE_FUSED = 0, 1
 KV_DECODE_MATRIX, KV_DECODE_VECTOR = 0, 1
+KV_HOST_COPY_DMA, KV_HOST_COPY_KERNEL = 0, 1
 
 
 class KVError(RuntimeError):
@@ -99,6 +100,7 @@ _SIGS = {
     "kv_pool_set_decode_waves": (ctypes.c_int, [_P, _I32]),
     "kv_pool_set_decode_combine": (ctypes.c_int, [_P, _I32]),
     "kv_pool_set_decode_compute": (ctypes.c_int, [_P, _I32]),
+    "kv_pool_set_host_copy": (ctypes.c_int, [_P, _I32]),
     "kv_read_probe": (ctypes.c_int, [_P, ctypes.c_size_t, _P, _I32, _P]),
     "paged_decode_workspace_bytes": (_SZ, [_P, _I32, _I32]),
     "paged_decode_attention": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _I32, _I32,
@@ -310,6 +312,10 @@ def kv_pool_set_decode_combine(pool: int, mode: int) -> None:
 
 def kv_pool_set_decode_compute(pool: int, mode: int) -> None:
     _check(_lib.kv_pool_set_decode_compute(pool, mode), "kv_pool_set_decode_compute")
+
+
+def kv_pool_set_host_copy(pool: int, mode: int) -> None:
+    _check(_lib.kv_pool_set_host_copy(pool, mode), "kv_pool_set_host_copy")
 
 
 def kv_read_probe(buf: int, nbytes: int, out: int, blocks: int, stream: int = 0) -> None:

@@ -185,5 +185,8 @@ class HotColdPool:
     def set_combine(self, fused: bool) -> None:
         kv.kv_pool_set_decode_combine(self.handle, kv.KV_COMBINE_FUSED if fused else kv.KV_COMBINE_SEPARATE)
 
+    def set_host_copy(self, kernel: bool) -> None:
+        kv.kv_pool_set_host_copy(self.handle, kv.KV_HOST_COPY_KERNEL if kernel else kv.KV_HOST_COPY_DMA)
+
     def set_compute(self, vector: bool) -> None:
         kv.kv_pool_set_decode_compute(self.handle, kv.KV_DECODE_VECTOR if vector else kv.KV_DECODE_MATRIX)

@@ -178,15 +178,18 @@ def test_aliased_cold_pages_resume(dev):
     pool.close()
 
 
-@pytest.mark.parametrize("cold", COLD_TIERS)
-def test_random_sequences_match_model(dev, cold):
+@pytest.mark.parametrize("cold,host_kernel", [("device", False), ("host", False), ("host", True)])
+def test_random_sequences_match_model(dev, cold, host_kernel):
     """Random create / write / evict / pause / LRU-evict / extend / resume /
     destroy sequences: page tables, statistics and the bytes of every resident
-    page and every valid cold copy follow the model exactly."""
+    page and every valid cold copy follow the model exactly.  The pinned-host
+    tier runs with its copies on the DMA engines (default) and in the copy
+    kernel."""
     from paper_2609_25782_amd import hotcold_kv as kv
     from paper_2609_25782_amd.pool import HotColdPool
     nh, nc, ms, stride = 48, 40, 6, 8
     pool = HotColdPool(2, 2, 64, "bf16", nh, nc, ms, stride, cold_location=cold)
+    pool.set_host_copy(host_kernel)
     model = PoolModel(nh, nc, ms, stride)
     _random_fill(pool, 3)
     torch.cuda.synchronize()

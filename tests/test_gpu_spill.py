@@ -44,8 +44,8 @@ def _random_fill(pool, seed):
     pool.cold.copy_(torch.randint(0, 256, pool.cold.shape, dtype=torch.uint8, device=pool.device, generator=g))
 
 
-@pytest.mark.parametrize("cold", COLD_TIERS)
-def test_spill_sequences_match_model(dev, cold):
+@pytest.mark.parametrize("cold,host_kernel", [("device", False), ("host", False), ("host", True)])
+def test_spill_sequences_match_model(dev, cold, host_kernel):
     """Random create / extend / pause / resume / promote / evict / LRU-evict /
     destroy in spill mode: the device page table (cold-tagged entries
     included), the statistics and the bytes of every resident page and valid
@@ -55,6 +55,7 @@ def test_spill_sequences_match_model(dev, cold):
     _say("spill sequences, cold tier in %s memory" % cold)
     nh, nc, ms, stride = 14, 70, 6, 8
     pool = HotColdPool(2, 2, 64, "bf16", nh, nc, ms, stride, cold_location=cold)
+    pool.set_host_copy(host_kernel)
     kv.kv_pool_set_spill(pool.handle, True)
     model = PoolModel(nh, nc, ms, stride, spill=True)
     _random_fill(pool, 5)

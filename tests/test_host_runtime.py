@@ -213,6 +213,19 @@ def test_metadata_append_drops_cold_copies_and_checks_every_row():
     kv.kv_pool_destroy(pool)
 
 
+def test_mode_setters_refuse_unknown_modes():
+    kv = _lib()
+    pool = _meta_pool(kv, 4, 4, 2, 4)
+    for setter, good in ((kv._lib.kv_pool_set_host_copy, (kv.KV_HOST_COPY_DMA, kv.KV_HOST_COPY_KERNEL)),
+                         (kv._lib.kv_pool_set_decode_compute, (kv.KV_DECODE_MATRIX, kv.KV_DECODE_VECTOR)),
+                         (kv._lib.kv_pool_set_decode_combine, (kv.KV_COMBINE_SEPARATE, kv.KV_COMBINE_FUSED))):
+        for mode in good:
+            assert setter(pool, mode) == kv.KV_OK
+        for mode in (-1, 2, 7):
+            assert setter(pool, mode) == kv.KV_ERR_INVALID
+    kv.kv_pool_destroy(pool)
+
+
 def test_spill_entry_points_error_codes():
     """Errors of the spill entry points on a metadata-only pool, each leaving the
     pool unchanged."""
