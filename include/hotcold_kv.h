@@ -380,6 +380,8 @@ int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_
 /*
  * Bandwidth budget of the page copies (resume, eviction): at most `blocks`
  * 256-thread blocks copy at once (0: the default, enough to fill the GPU).
+ * It applies to the copy kernel only: pinned-host tier copies made by the DMA
+ * engines (kv_pool_set_host_copy) do not use it.
  * The paper overlaps eviction and resume with decode (Sec. III, "Architecture
  * and data paths"); with a device-memory cold tier both share HBM, so a smaller
  * budget leaves decode more bandwidth and CU slots at the cost of a slower
