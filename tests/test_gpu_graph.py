@@ -24,11 +24,14 @@ def dev():
     return torch.device("cuda", 0)
 
 
-def test_decode_step_graph_replays_match_eager(dev):
+@pytest.mark.parametrize("vector", [False, True])
+def test_decode_step_graph_replays_match_eager(dev, vector):
+    """Both forms of the split kernel: matrix cores and the vector ALU."""
     from paper_2609_25782_amd.pool import HotColdPool
     layers, lens = 4, [300, 1000, 57, 2000, 16, 777]
     n_pages = sum(synth.pages_for(L) for L in lens)
     pool = HotColdPool(layers, 2, 128, "bf16", n_pages + 10, 0, len(lens), synth.pages_for(2100))
+    pool.set_compute(vector)
     for b, L in enumerate(lens):
         pool.create_session(L)
         pool.fill_synthetic(b, b, SEED, float(synth.value_multiplier(1.0)))
