@@ -451,25 +451,41 @@ def measure_host_overlap(seed: int):
     return res
 
 
-def measure_agentic_replay(seed: int, plateau_s: float = 20.0):
+def measure_agentic_replay(seed: int, plateau_s: float = 20.0, paper_node: bool = False):
     """The replay driver over a device pool of the paper's shape (48 layers, 4 KV
-    heads, 128, bf16, 1.5 MiB pages; 32 query heads), N_a = 32 sessions decoding:
-    40 GiB of hot pages and 160 GiB of device-memory cold pages, so LRU eviction,
-    write-back and partial resumes run on real pages.  The warm-up only moves
-    pages; the plateau also decodes all 48 layers of the running sessions every
-    step.  Times, per step on the GPU: the decode, and the whole step (its
-    admissions, resumes, evictions and page fills plus the decode)."""
+    heads, 128, bf16, 1.5 MiB pages; 32 query heads), so LRU eviction,
+    write-back and partial resumes run on real pages.  Default: N_a = 32
+    sessions decoding over 40 GiB of hot pages and 160 GiB of device-memory cold
+    pages (heavy LRU pressure).  paper_node: the paper's node, N_a = 48 over 192
+    GiB of HBM less 56.8 GiB of weights (135 GiB of hot pages), with 90 GiB of
+    device-memory cold pages.  The warm-up only moves pages; the plateau also
+    decodes all 48 layers of the running sessions every step.  Times, per step
+    on the GPU: the decode, and the whole step (its admissions, resumes,
+    evictions and page fills plus the decode)."""
     import torch
     import synth
     from paper_2609_25782_amd import hotcold_kv as kv
     from paper_2609_25782_amd import replay as rp
     from paper_2609_25782_amd.pool import HotColdPool
 
-    cfg = rp.ReplayConfig(n_active=32, weight_bytes=0.0, warmup_s=420.0, plateau_s=plateau_s,
-                          sample_s=0.5, max_sessions=320, seed=seed)
+    n_active = 48 if paper_node else 32
+    cfg = rp.ReplayConfig(n_active=n_active, weight_bytes=0.0, warmup_s=420.0, plateau_s=plateau_s,
+                          sample_s=0.5, max_sessions=512 if paper_node else 320, seed=seed)
     page = cfg.page_bytes
-    cfg.hbm_bytes = float(40 * 2 ** 30 // page * page)
-    cfg.cold_bytes = float(160 * 2 ** 30 // page * page)
+    if paper_node:
+        # the cold tier must take every page evicted during the warm-up (about
+        # 115 GiB at this load); it gets what HBM has left, up to 125 GiB
+        cfg.hbm_bytes, cfg.weight_bytes = 192.0 * 2 ** 30, 56.8 * 2 ** 30
+        free = torch.cuda.mem_get_info()[0]
+        cold = min(125 * 2 ** 30, free - cfg.num_hot_pages * page - 6 * 2 ** 30)
+        if cold < 115 * 2 ** 30:
+            return {"skipped": "needs %.0f GiB of free HBM for 135 GiB of hot and 115 GiB of cold pages, "
+                               "%.0f GiB free" % ((cfg.num_hot_pages * page + 121 * 2 ** 30) / 2 ** 30,
+                                                  free / 2 ** 30)}
+        cfg.cold_bytes = float(cold // page * page)
+    else:
+        cfg.hbm_bytes = float(40 * 2 ** 30 // page * page)
+        cfg.cold_bytes = float(160 * 2 ** 30 // page * page)
     hp = HotColdPool(48, 4, 128, "bf16", cfg.num_hot_pages, cfg.num_cold_pages, cfg.max_sessions,
                      cfg.stride)
     dp = rp.DevicePool(cfg, hp, seed, float(synth.value_multiplier(1.0)))
@@ -505,7 +521,13 @@ def measure_agentic_replay(seed: int, plateau_s: float = 20.0):
     token_bytes = cfg.token_bytes
     kv_bytes = t["tokens"].astype(np.float64) * token_bytes
     out = {
-        "config": "48 layers x 4 KV heads x 128 bf16 (1.5 MiB pages), 32 query heads, N_a=32, "
+        "config": ("48 layers x 4 KV heads x 128 bf16 (1.5 MiB pages), 32 query heads, N_a=48, the paper's "
+                   "node: 192 GiB HBM less 56.8 GiB weights = %.1f GiB hot, cold %.0f GiB device memory, "
+                   "synthetic trajectories, TBT model %.1f ms" % (cfg.num_hot_pages * page / 2 ** 30,
+                                                                   cfg.num_cold_pages * page / 2 ** 30,
+                                                                   1e3 * cfg.step_s))
+        if paper_node else
+                  "48 layers x 4 KV heads x 128 bf16 (1.5 MiB pages), 32 query heads, N_a=32, "
                   "hot 40 GiB, cold 160 GiB device memory, synthetic trajectories",
         "plateau_steps": int(len(t["step_ms"]) + profiled),
         "timed_steps": int(len(t["step_ms"])),
@@ -1176,6 +1198,8 @@ def main():
     if "replay" in sections:
         result["agentic_replay"] = measure_agentic_replay(args.seed)
         log("agentic replay: %s" % json.dumps(result["agentic_replay"]))
+        result["agentic_replay_paper_node"] = measure_agentic_replay(args.seed, paper_node=True)
+        log("agentic replay, paper's node: %s" % json.dumps(result["agentic_replay_paper_node"]))
     if "spill" in sections:
         result["spill_decode"] = measure_spill(args.seed)
     if "configs" in sections:

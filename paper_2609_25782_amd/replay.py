@@ -93,6 +93,7 @@ class ReplayConfig:
                                                    ("nvlink_c2c", 450e9, 0.0),
                                                    ("pcie5", 64e9, 0.0))
     seed: int = 0
+    stall_steps: int = 2000               # steps with nothing decoding before the replay gives up
 
     @property
     def step_s(self) -> float:
@@ -117,6 +118,10 @@ class ReplayConfig:
     @property
     def stride(self) -> int:
         return _pages(self.peak[1] + self.turn_prompt[1] + self.turn_decode[1])
+
+
+class ReplayStalled(RuntimeError):
+    """The replay cannot make progress: every tier is full."""
 
 
 class LibraryPool:
@@ -499,12 +504,22 @@ class Replay:
         self.plateau_start = warm
         base = None
         samples = []
+        stalled = 0
         for self.step in range(total):
             if self.step == warm:
                 base = self.pool.stats()
             if self.step >= warm and hasattr(decode_fn, "step_begin"):
                 decode_fn.step_begin()
             self._advance(decode_fn if self.step >= warm else None)
+            # Nothing decoding while sessions wait: both tiers are full (a page
+            # for the next token needs an eviction, which needs a free cold page),
+            # and preempting and re-admitting would go on forever.
+            stalled = stalled + 1 if self.active == 0 and (self.preempted or self.ready) else 0
+            if stalled > cfg.stall_steps:
+                st = self.pool.stats()
+                raise ReplayStalled("no session has decoded for %d steps at step %d: %d free hot and %d free "
+                                    "cold pages; the cold tier is too small for this load" % (
+                                        stalled, self.step, st["free_hot_pages"], st["free_cold_pages"]))
             if cfg.spill and self.step % promote_every == 0:
                 self.pool.promote(1 << 30)
             if self.step >= warm and (self.step - warm) % every == 0:

@@ -154,6 +154,27 @@ def test_preemption_keeps_an_overfull_active_set_moving():
     lib.close()
 
 
+def test_full_tiers_stop_the_replay_instead_of_spinning():
+    """A cold tier too small to take the evictions: the active set can neither
+    grow nor make room, so after stall_steps steps with nothing decoding the
+    replay raises, for the library pool and for the oracle's model alike (the
+    same configuration with a large cold tier runs to the end)."""
+    cfg = _tiny(n_active=4, prompt0=(30, 40), turn_prompt=(10, 20), turn_decode=(60, 80),
+                peak=(150, 200), gap_median_s=2.0, gap_mean_s=4.0, warmup_s=50, plateau_s=800)
+    cfg.hbm_bytes = _pages_bytes(cfg, 18)
+    cfg.cold_bytes = _pages_bytes(cfg, 6)
+    cfg.stall_steps = 500
+    for pool in (None, ModelPool(cfg)):
+        r = rp.Replay(cfg, pool)
+        with pytest.raises(rp.ReplayStalled, match="cold tier is too small"):
+            r.run()
+        r.close()
+    cfg.cold_bytes = _pages_bytes(cfg, 400)
+    r = rp.Replay(cfg)
+    assert r.run()["sessions_finished"] > 5
+    r.close()
+
+
 def test_replay_is_deterministic():
     cfg = _tiny(n_active=6, prompt0=(10, 40), turn_prompt=(5, 30), turn_decode=(5, 40),
                 peak=(60, 160), gap_median_s=6.0, gap_mean_s=15.0, warmup_s=100, plateau_s=300)
