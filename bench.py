@@ -476,6 +476,9 @@ def measure_agentic_replay(seed: int, plateau_s: float = 20.0, paper_node: bool 
         # the cold tier must take every page evicted during the warm-up (about
         # 115 GiB at this load); it gets what HBM has left, up to 125 GiB
         cfg.hbm_bytes, cfg.weight_bytes = 192.0 * 2 ** 30, 56.8 * 2 ** 30
+        import gc
+        gc.collect()
+        torch.cuda.empty_cache()
         free = torch.cuda.mem_get_info()[0]
         cold = min(125 * 2 ** 30, free - cfg.num_hot_pages * page - 6 * 2 ** 30)
         if cold < 115 * 2 ** 30:
@@ -548,7 +551,7 @@ def measure_agentic_replay(seed: int, plateau_s: float = 20.0, paper_node: bool 
     }
     r.close()
     hp.close()
-    del hp, dp, dec
+    del r, hp, dp, dec, Decode             # the replay holds the device pool's buffers
     torch.cuda.empty_cache()
     return out
 
