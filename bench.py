@@ -259,6 +259,42 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
         budget.append({"copy_blocks": blocks, "resume_ms_per_session": round(ms_b / len(sids), 3),
                        "decode48_ms_with_concurrent_resume": round(ev[0].elapsed_time(ev[1]), 3)})
     pool.set_copy_blocks(0)
+    # the same pair on streams confined to disjoint CUs: the copy stream gets
+    # `copy_slots` CUs of every XCD, the decode stream the others
+    from paper_2609_25782_amd.pool import split_streams
+    cu_split = []
+    for copy_slots in (8, 4, 2):
+        dec_s, cpy_s = split_streams(copy_slots)
+        torch.cuda.synchronize()
+        decode48(dec_s.stream)
+        torch.cuda.synchronize()
+        dec_alone = timed(lambda i: decode48(dec_s.stream), dec_s.stream, 2)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        sids = picks[k % len(picks)]
+        k += 1
+        ev[0].record(cpy_s.stream)
+        resume_batch(sids, cpy_s.stream)
+        ev[1].record(cpy_s.stream)
+        torch.cuda.synchronize()
+        sids = picks[k % len(picks)]
+        k += 1
+        ev[2].record(cpy_s.stream)
+        resume_batch(sids, cpy_s.stream)
+        ev[3].record(cpy_s.stream)
+        ev[4].record(dec_s.stream)
+        decode48(dec_s.stream)
+        ev[5].record(dec_s.stream)
+        torch.cuda.synchronize()
+        both_split = ev[4].elapsed_time(ev[5])
+        cu_split.append({"copy_cus": cpy_s.cus, "decode_cus": dec_s.cus,
+                         "decode48_ms_alone": round(dec_alone, 3),
+                         "resume_evict_ms_per_session_alone": round(ev[0].elapsed_time(ev[1]) / len(sids), 3),
+                         "decode48_ms_with_concurrent_resume": round(both_split, 3),
+                         "resume_evict_ms_per_session_beside": round(ev[2].elapsed_time(ev[3]) / len(sids), 3),
+                         "tbt_impact": round(both_split / decode_ms, 3)})
+        log("CU-split streams: %s" % json.dumps(cu_split[-1]))
+        dec_s.close()
+        cpy_s.close()
     # lazy resume: no copy when the sessions resume (their pages are read in
     # place from the cold tier), then promotion under a per-step page budget on a
     # second stream while the 48 layers decode; versus the eager resume above
@@ -339,6 +375,7 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
         "decode48_GBps": round(48 * sum(decode_bytes(w.seq_lens, 32, 4, 128, 2)) / (decode_ms / 1e3) / 1e9, 1),
         "partial_residency": partial,
         "copy_budget": budget,
+        "cu_split_streams": cu_split,
         "lazy_resume": lazy,
     }
 

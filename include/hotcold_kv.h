@@ -406,6 +406,39 @@ enum kv_host_copy {
 int kv_pool_set_host_copy(kv_pool* pool, int32_t mode);
 
 /* ----------------------------------------------------------------------- */
+/* Streams on a share of the compute units                                  */
+/* ----------------------------------------------------------------------- */
+
+/*
+ * The paper keeps fetches from the cold tier off the decode's path, running
+ * beside it (Sec. III, "Architecture and data paths").  On one GPU a resume
+ * copy and a decode launched on two plain streams share every CU: copy waves
+ * then sit beside split waves, and the split, whose static partition waits
+ * for its slowest wave, slows about threefold even when the copy's grid is
+ * capped (kv_pool_set_copy_blocks).  Streams confined to disjoint sets of CUs
+ * keep the two apart, so that only HBM bandwidth is shared.
+ *
+ * A "slot" is one CU of every XCD: the device has `xcds` XCDs of `slots` CUs
+ * each, and slot j of XCD x is bit x + xcds * j of the HIP stream CU mask (the
+ * driver spreads consecutive mask bits over the XCDs first, then over each
+ * XCD's shader engines).  A range of slots therefore gives every XCD, and so
+ * every L2, the same number of CUs.
+ *
+ * kv_device_cu_slots: the device's XCD count and CUs per XCD.
+ * kv_stream_create_cu_slots: a new stream on `device` whose kernels run only
+ *   on slots [slot_begin, slot_end) (0 <= begin < end <= slots).  The caller
+ *   owns the stream and releases it with kv_stream_destroy after its work is
+ *   done.  The decode's default grid (paged_decode_waves) has one block per CU
+ *   on 192 CUs; on a stream with fewer CUs, set at most four waves per CU
+ *   (kv_pool_set_decode_waves), or the split runs in two rounds.
+ * KV_ERR_INVALID for a bad device, range or output pointer; KV_ERR_HIP when
+ * the runtime refuses.
+ */
+int kv_device_cu_slots(int32_t device, int32_t* xcds, int32_t* slots);
+int kv_stream_create_cu_slots(int32_t device, int32_t slot_begin, int32_t slot_end, kv_stream_t* stream_out);
+int kv_stream_destroy(kv_stream_t stream);
+
+/* ----------------------------------------------------------------------- */
 /* Decode attention (data path 1)                                           */
 /* ----------------------------------------------------------------------- */
 

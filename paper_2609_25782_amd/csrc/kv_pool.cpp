@@ -1663,6 +1663,51 @@ int kv_read_probe(const void* buf, size_t bytes, uint32_t* out, int32_t blocks, 
     return KV_OK;
 }
 
+int kv_device_cu_slots(int32_t device, int32_t* xcds, int32_t* slots) {
+    if (!xcds || !slots) return fail(KV_ERR_INVALID, "NULL output");
+    int n = 0;
+    hipError_t e = hipGetDeviceCount(&n);
+    if (e != hipSuccess) return hip_fail(e, "device count");
+    if (device < 0 || device >= n) return fail(KV_ERR_INVALID, "no such device");
+    int cus = 0, x = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&x, hipDeviceAttributeNumberOfXccs, device);
+    if (e != hipSuccess) return hip_fail(e, "device attributes");
+    if (x < 1 || cus < x || cus % x != 0) return fail(KV_ERR_INVALID, "CUs do not divide evenly over the XCDs");
+    *xcds = x;
+    *slots = cus / x;
+    return KV_OK;
+}
+
+int kv_stream_create_cu_slots(int32_t device, int32_t slot_begin, int32_t slot_end, kv_stream_t* stream_out) {
+    if (!stream_out) return fail(KV_ERR_INVALID, "NULL output");
+    int32_t xcds = 0, slots = 0;
+    const int rc = kv_device_cu_slots(device, &xcds, &slots);
+    if (rc != KV_OK) return rc;
+    if (slot_begin < 0 || slot_end > slots || slot_begin >= slot_end)
+        return fail(KV_ERR_INVALID, "slot range outside [0, CUs per XCD)");
+    // slot j of XCD x is mask bit x + xcds * j
+    std::vector<uint32_t> mask((static_cast<size_t>(xcds) * slots + 31) / 32, 0u);
+    for (int32_t j = slot_begin; j < slot_end; ++j)
+        for (int32_t x = 0; x < xcds; ++x) {
+            const int64_t bit = x + static_cast<int64_t>(xcds) * j;
+            mask[bit / 32] |= 1u << (bit % 32);
+        }
+    DeviceGuard g(device);
+    hipStream_t s = nullptr;
+    const hipError_t e = hipExtStreamCreateWithCUMask(&s, static_cast<uint32_t>(mask.size()), mask.data());
+    if (e != hipSuccess) return hip_fail(e, "CU-masked stream");
+    *stream_out = s;
+    return KV_OK;
+}
+
+int kv_stream_destroy(kv_stream_t stream) {
+    if (!stream) return fail(KV_ERR_INVALID, "NULL stream");
+    const hipError_t e = hipStreamDestroy(static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "stream destroy");
+    return KV_OK;
+}
+
 int kv_pool_set_profiling(kv_pool* pool, int enable) {
     if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
     if (pool->meta && enable) return fail(KV_ERR_INVALID, "metadata-only pool launches nothing");

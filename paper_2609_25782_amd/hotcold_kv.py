@@ -102,6 +102,9 @@ _SIGS = {
     "kv_pool_set_decode_compute": (ctypes.c_int, [_P, _I32]),
     "kv_pool_set_host_copy": (ctypes.c_int, [_P, _I32]),
     "kv_read_probe": (ctypes.c_int, [_P, ctypes.c_size_t, _P, _I32, _P]),
+    "kv_device_cu_slots": (ctypes.c_int, [_I32, _PI32, _PI32]),
+    "kv_stream_create_cu_slots": (ctypes.c_int, [_I32, _I32, _I32, ctypes.POINTER(_P)]),
+    "kv_stream_destroy": (ctypes.c_int, [_P]),
     "paged_decode_workspace_bytes": (_SZ, [_P, _I32, _I32]),
     "paged_decode_attention": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _I32, _I32,
                                               ctypes.c_float, _P, _P, _SZ, _P]),
@@ -320,6 +323,25 @@ def kv_pool_set_host_copy(pool: int, mode: int) -> None:
 
 def kv_read_probe(buf: int, nbytes: int, out: int, blocks: int, stream: int = 0) -> None:
     _check(_lib.kv_read_probe(buf, nbytes, out, blocks, stream), "kv_read_probe")
+
+
+def kv_device_cu_slots(device: int = 0):
+    """(XCDs, CUs per XCD) of the device."""
+    x, n = ctypes.c_int32(), ctypes.c_int32()
+    _check(_lib.kv_device_cu_slots(device, ctypes.byref(x), ctypes.byref(n)), "kv_device_cu_slots")
+    return x.value, n.value
+
+
+def kv_stream_create_cu_slots(device: int, slot_begin: int, slot_end: int) -> int:
+    """A new stream whose kernels run on CU slots [slot_begin, slot_end) of every XCD."""
+    s = _P()
+    _check(_lib.kv_stream_create_cu_slots(device, slot_begin, slot_end, ctypes.byref(s)),
+           "kv_stream_create_cu_slots")
+    return s.value
+
+
+def kv_stream_destroy(stream: int) -> None:
+    _check(_lib.kv_stream_destroy(stream), "kv_stream_destroy")
 
 
 def paged_decode_workspace_bytes(pool: int, batch: int, num_q_heads: int) -> int:

@@ -190,3 +190,37 @@ class HotColdPool:
 
     def set_compute(self, vector: bool) -> None:
         kv.kv_pool_set_decode_compute(self.handle, kv.KV_DECODE_VECTOR if vector else kv.KV_DECODE_MATRIX)
+
+
+class CUStream:
+    """A torch stream whose kernels run only on CU slots [begin, end) of every
+    XCD (one slot = one CU per XCD).  The library creates the HIP stream; close()
+    waits for the device and destroys it."""
+
+    def __init__(self, begin: int, end: int, device: int = 0):
+        xcds, _ = kv.kv_device_cu_slots(device)
+        self.device = torch.device("cuda", device)
+        self.handle = kv.kv_stream_create_cu_slots(device, begin, end)
+        self.stream = torch.cuda.ExternalStream(self.handle, device=self.device)
+        self.cus = xcds * (end - begin)
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            torch.cuda.synchronize(self.device)
+            kv.kv_stream_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def split_streams(copy_slots: int, device: int = 0):
+    """A decode stream and a copy stream on disjoint CUs: the copy stream gets
+    `copy_slots` CUs of every XCD, the decode stream the rest."""
+    _, slots = kv.kv_device_cu_slots(device)
+    if not 0 < copy_slots < slots:
+        raise ValueError("copy_slots must be in [1, %d)" % slots)
+    return CUStream(copy_slots, slots, device), CUStream(0, copy_slots, device)
