@@ -196,8 +196,13 @@ struct kv_pool {
     int32_t half_layer[2] = {-1, -1};     // layer gathered into each half for the current plan
     StagingSlot ring[kStagingSlots];
     int ring_next = 0;
-    hipEvent_t free_event = nullptr;
-    bool free_pending = false;
+    // One event per stream on which calls freed hot pages: recorded after the
+    // last such call's device work on that stream.
+    struct FreeMark {
+        hipStream_t stream;
+        hipEvent_t event;
+    };
+    std::vector<FreeMark> free_marks;
     bool profiling = false;
     int32_t combine_mode = KV_COMBINE_SEPARATE;
     char* cold_host = nullptr;      // host address of a pinned-host cold pool (null otherwise)
@@ -218,7 +223,7 @@ struct kv_pool {
             if (s.dev) (void)hipFree(s.dev);
             if (s.done) (void)hipEventDestroy(s.done);
         }
-        if (free_event) (void)hipEventDestroy(free_event);
+        for (const FreeMark& m : free_marks) (void)hipEventDestroy(m.event);
         if (decode_event) {
             (void)hipEventSynchronize(decode_event);
             (void)hipEventDestroy(decode_event);
@@ -258,18 +263,42 @@ struct kv_pool {
 
     hipStream_t strm(kv_stream_t s) const { return static_cast<hipStream_t>(s); }
 
-    // Make `stream` wait for device work of calls that freed hot pages.
+    // Make `stream` wait for the device work of every call that freed hot pages,
+    // on whichever stream it ran.
     int order_after_frees(hipStream_t s) {
-        if (!free_pending) return KV_OK;
-        hipError_t e = hipStreamWaitEvent(s, free_event, 0);
-        if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        for (const FreeMark& m : free_marks) {
+            hipError_t e = hipStreamWaitEvent(s, m.event, 0);
+            if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        }
         return KV_OK;
     }
 
+    // After a call that freed hot pages enqueued its work on `s`.  Marks of other
+    // streams whose work has finished are dropped; a single shared event would
+    // lose the work of the previous freeing call whenever streams alternate.
     int note_frees(hipStream_t s) {
-        hipError_t e = hipEventRecord(free_event, s);
+        size_t keep = 0;
+        for (size_t i = 0; i < free_marks.size(); ++i) {
+            const FreeMark m = free_marks[i];
+            if (m.stream != s && hipEventQuery(m.event) == hipSuccess) {
+                (void)hipEventDestroy(m.event);
+                continue;
+            }
+            free_marks[keep++] = m;
+        }
+        free_marks.resize(keep);
+        FreeMark* mine = nullptr;
+        for (FreeMark& m : free_marks)
+            if (m.stream == s) mine = &m;
+        if (!mine) {
+            hipEvent_t ev = nullptr;
+            hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+            if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
+            free_marks.push_back(FreeMark{s, ev});
+            mine = &free_marks.back();
+        }
+        hipError_t e = hipEventRecord(mine->event, s);
         if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-        free_pending = true;
         return KV_OK;
     }
 
@@ -672,8 +701,7 @@ int kv_pool_create(const kv_pool_desc* desc, void* hot_base, size_t hot_bytes, v
                 return fail(KV_ERR_OOM, "staging allocation failed");
             }
         }
-        if (hipEventCreateWithFlags(&p->free_event, hipEventDisableTiming) != hipSuccess ||
-            hipEventCreateWithFlags(&p->decode_event, hipEventDisableTiming) != hipSuccess) {
+        if (hipEventCreateWithFlags(&p->decode_event, hipEventDisableTiming) != hipSuccess) {
             delete p;
             return fail(KV_ERR_OOM, "event creation failed");
         }

@@ -474,3 +474,36 @@ def test_copy_launch_shapes_and_budget(dev):
     assert (n1, n2) == (fine, coarse) and n3 > fine - 16
     assert pool.stats()["pages_to_hot"] == n1 + n2 + n3
     pool.close()
+
+
+def test_frees_on_alternating_streams_are_all_waited_for(dev):
+    """A 1 GiB eviction on stream A frees hot pages, a destroy on stream B frees
+    one more, and a session created on stream C takes A's freed pages and is
+    filled at once.  C must wait for A's copy as well as B's work: the evicted
+    session's cold copy equals its hot pages before the eviction."""
+    from paper_2609_25782_amd.pool import HotColdPool
+    NL = 8
+    n = 4096
+    pool = HotColdPool(NL, 4, 128, "bf16", n + 64, n + 64, 8, n)
+    pb = pool.page_bytes
+    big = pool.create_session(16 * n)
+    small = pool.create_session(16)
+    pool.fill_synthetic(big, 0, 5, 1.0)
+    pool.fill_synthetic(small, 1, 5, 1.0)
+    hot_big = pool.info(big)[2]
+    torch.cuda.synchronize()
+    idx = torch.tensor(hot_big, dtype=torch.long, device=dev)
+    before = pool.hot.view(-1, pb).index_select(0, idx)
+    sa, sb, sc = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    _say("evict %d pages of %d KiB on stream A, destroy on B, refill on C" % (n, pb // 1024))
+    pool.evict(big, stream=sa)
+    pool.destroy_session(small, stream=sb)
+    other = pool.create_session(16 * n, stream=sc)
+    assert sorted(pool.info(other)[2])[:n] == sorted(hot_big)  # the evicted session's pages
+    pool.fill_synthetic(other, 2, 6, 1.0, stream=sc)
+    torch.cuda.synchronize()
+    cold_big = pool.info(big)[3]
+    cidx = torch.tensor(cold_big, dtype=torch.long, device=dev)
+    assert torch.equal(pool.cold.view(-1, pb).index_select(0, cidx), before)
+    pool.close()
