@@ -59,7 +59,10 @@
  *    stream is ordered; across streams the caller orders it with events, with
  *    one exception the pool handles itself: hot pages freed by an eviction or
  *    a destroy are not handed out to a call on another stream before the
- *    freeing call's device work has finished.
+ *    freeing call's device work has finished, on whichever streams the
+ *    freeing calls ran.  Other readers of a session's pages (a decode, a
+ *    resume still copying, on another stream) are the caller's to order
+ *    before the call that frees those pages, hot or cold.
  */
 #ifndef HOTCOLD_KV_H
 #define HOTCOLD_KV_H
