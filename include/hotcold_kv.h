@@ -258,7 +258,10 @@ int kv_pool_set_spill(kv_pool* pool, int32_t enable);
  * of the same sessions on another stream may run meanwhile: it reads each page
  * either from its (unchanged) cold copy or from the finished hot copy.  The
  * LRU victims evicted to make room are pages of paused sessions, which decode
- * does not read.
+ * does not read.  Writes to those sessions on another stream
+ * (kv_append_tokens, kv_write_tokens) are another matter: the caller orders
+ * them around this call's work, since the copy could miss a write enqueued
+ * before it and overwrite one enqueued after it.
  * Errors: KV_ERR_INVALID, KV_ERR_NO_COLD_PAGES (evicted pages need cold copies;
  * nothing changes).
  */
