@@ -812,7 +812,8 @@ def measure_append(seed: int, steps: int = 20, warmup: int = 3):
 def measure_read_ceiling(nbytes: int = 16 * 2 ** 30):
     """The streaming-read rate this GPU reaches: the library's read probe
     (kv_read_probe, the decode kernel's 16-byte nontemporal loads, 8 in flight
-    per thread) over a 16 GiB buffer, best median over a few grid sizes."""
+    per thread, 32 KiB contiguous per block and step) over a 16 GiB buffer,
+    best median over a few grid sizes."""
     import torch
     from paper_2609_25782_amd import hotcold_kv as kv
     dev = torch.device("cuda", 0)
@@ -835,8 +836,9 @@ def measure_read_ceiling(nbytes: int = 16 * 2 ** 30):
             best = {"GBps": round(gbps, 1), "blocks": blocks}
     del buf, out
     torch.cuda.empty_cache()
-    best.update({"bytes": nbytes, "method": "kv_read_probe: sequential 16-byte nontemporal loads, "
-                                            "events around one launch, best median over grid sizes"})
+    best.update({"bytes": nbytes, "method": "kv_read_probe: 16-byte nontemporal loads, contiguous 32 KiB "
+                                            "chunks per block, events around one launch, best median over "
+                                            "grid sizes"})
     return best
 
 

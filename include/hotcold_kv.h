@@ -577,13 +577,18 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
 
 /*
  * The work split of paged_decode_attention, written out (device int32
- * [waves + batch * num_kv_heads][4]).  A unit is one page of one (row b, KV
- * head g); units are ordered by (b, g, page); wave k of `waves` takes units
- * [floor(k T / waves), floor((k + 1) T / waves)) of the T units; where a wave
- * meets the units of (b, g) it makes one partial result, stored in slot
- * k + b * num_kv_heads + g as (b, g, first page, end page).  Unused slots hold
- * (-1, -1, 0, 0).  The split is not the paper's: it is how this library
- * balances sessions of different lengths over the GPU.
+ * [waves + batch * num_kv_heads][4]).  Waves form workers of L waves: L = 4
+ * when num_kv_heads and `waves` are multiples of 4, else 1.  A unit is one
+ * page of one (row b, head group hg) with Hkv / L groups per row; units are
+ * ordered by (b, hg, page); worker k of waves / L takes units
+ * [floor(k T L / waves), floor((k + 1) T L / waves)) of the T units.  Where a
+ * worker meets the units of (b, hg), its wave w makes one partial result for
+ * KV head g = L hg + w, stored in slot (k + b Hkv / L + hg) L + w as
+ * (b, g, first page, end page).  Unused slots hold (-1, -1, 0, 0).  With
+ * L = 4 a worker's four waves read the four heads' tiles of the same pages,
+ * which HBM serves faster than unrelated pages.  The split is not the
+ * paper's: it is how this library balances sessions of different lengths
+ * over the GPU.
  */
 int paged_decode_partition(kv_pool* pool, const int32_t* seq_lens, int32_t batch, int32_t waves,
                            int32_t* slots_out, kv_stream_t stream);
@@ -599,7 +604,8 @@ const char* kv_last_error(void);
  * Measurement context, not part of the KV path: a streaming read of `bytes`
  * (a multiple of 16) of device memory at `buf` (16-byte aligned), with the
  * 16-byte nontemporal loads the decode kernel uses and 8 of them in flight
- * per thread, on `blocks` (1 .. 2^20) blocks of 256 threads.  Each block
+ * per thread, on `blocks` (1 .. 2^20) blocks of 256 threads that take
+ * contiguous 32 KiB chunks in turn.  Each block
  * writes the XOR of what it read to out[block] (device, `blocks` words), so
  * the reads cannot be elided.  Asynchronous on `stream`; time it with events
  * around the call.  It gives the sequential-read rate this GPU reaches, the

@@ -1,15 +1,19 @@
 // Split-K paged grouped-query decode attention for gfx950 (data path 1 of the
 // hot-cold hierarchy: every decode step reads the whole hot set).
 //
-// Work split.  A unit is one page (16 tokens) of one (row b, KV head g).  The
-// units of all rows are laid end to end and cut into `waves` equal ranges, one
-// per wave of a persistent grid, so long and short contexts balance exactly.
-// Where a wave's range meets the units of one (b, g) it produces a partial
-// result (running max m, weight sum l, unnormalised output o) for the group of
-// query heads sharing KV head g; the combine kernel merges the partials of each
-// (b, g) with the usual log-sum-exp rescaling.  Reduction order depends only on
-// seq_lens, never on page placement, so results are bitwise independent of
-// where pages sit in the pool.
+// Work split.  A unit is one page (16 tokens) of one (row b, group of L KV
+// heads); the units of all rows are laid end to end and cut into equal ranges,
+// one per worker of a persistent grid, so long and short contexts balance
+// exactly.  A worker is L consecutive waves, wave w taking KV head L hg + w of
+// head group hg: with L = 4 the four waves of a worker read the four heads'
+// tiles of each page side by side, which HBM serves faster than as many
+// unrelated pages (DRAM row locality); L = 1 when the KV heads do not come in
+// fours.  Where a worker's range meets the units of one (b, hg), each of its
+// waves produces a partial result (running max m, weight sum l, unnormalised
+// output o) for the query heads sharing its KV head; the combine kernel merges
+// the partials of each (b, g) with the usual log-sum-exp rescaling.  Reduction
+// order depends only on seq_lens, never on page placement, so results are
+// bitwise independent of where pages sit in the pool.
 //
 // One wave processes one page of one KV head per step with matrix cores:
 //   scores  S^T[t][h] = K[t][:] . Q[h][:]   v_mfma_f32_16x16x32_bf16 (f32: 16x16x4)
@@ -314,8 +318,10 @@ __device__ void combine_segment(const DecodeArgs& a, int b, int g, const SegWave
     constexpr int kQuads = D / 4;
     constexpr int kMaxItems = (16 * kQuads + kWave - 1) / kWave;
     const int items = a.group * kQuads;
-    const int seg = b * a.num_kv_heads + g;
-    const int N = a.waves;
+    const int gw = a.group_waves;
+    const int64_t sseg = static_cast<int64_t>(b) * (a.num_kv_heads / gw) + g / gw;
+    const int w = g % gw;
+    const int N = a.waves / gw;
     float M[kMaxItems], den[kMaxItems];
     f32x4 acc[kMaxItems];
 #pragma unroll
@@ -326,7 +332,7 @@ __device__ void combine_segment(const DecodeArgs& a, int b, int g, const SegWave
     }
     for (int k = sw.k_first; k <= sw.k_last; ++k) {
         if (static_cast<int64_t>(k) * T / N == static_cast<int64_t>(k + 1) * T / N) continue;
-        const int64_t slot = static_cast<int64_t>(k) + seg;
+        const int64_t slot = (static_cast<int64_t>(k) + sseg) * gw + w;
         const float* pml = a.part_ml + slot * 2 * a.group;
         float mk[kMaxItems], lk[kMaxItems];
         f32x4 ok[kMaxItems];
@@ -344,8 +350,8 @@ __device__ void combine_segment(const DecodeArgs& a, int b, int g, const SegWave
         for (int it = 0; it < kMaxItems; ++it)
             if (it * kWave + lane < items) lse_merge(M[it], den[it], acc[it], mk[it], lk[it], ok[it]);
     }
-    const int32_t L = a.seq_lens[b];
-    const bool invalid = static_cast<int64_t>(L) > kPageTokens * a.pt_stride;
+    const int32_t len = a.seq_lens[b];
+    const bool invalid = static_cast<int64_t>(len) > kPageTokens * a.pt_stride;
     const float nan = __builtin_nanf("");
 #pragma unroll
     for (int it = 0; it < kMaxItems; ++it) {
@@ -457,7 +463,7 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
         // The wave that delivers the last partial of (b, g) merges them all.  The
         // arrival count is a release (this wave's partial becomes visible to every
         // XCD: on gfx950 an L2 write-back) and only the merging wave acquires.
-        const SegWaves sw = seg_waves(seg_first_unit, nb, total_units, a.waves);
+        const SegWaves sw = seg_waves(seg_first_unit, nb, total_units, a.waves / a.group_waves);
         int32_t* cnt = a.counters + pc.b * a.num_kv_heads + pc.g;
         int prev = 0;
         if (lane == 0) prev = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
@@ -736,32 +742,40 @@ __attribute__((amdgpu_waves_per_eu(HCK_SPLIT_WAVES_PER_EU))) void decode_split_k
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kSplitBlockWaves + threadIdx.x / kWave);
     if (wave >= a.waves) return;
+    // the worker this wave belongs to, and its KV head within the worker's head group
+    const int gw = a.group_waves;
+    const int heads = a.num_kv_heads / gw;
+    const int worker = wave / gw, w_in = wave % gw;
     if (a.fused) {
         // rows with no pages get no partials: write them here (0 for L = 0, NaN for L < 0)
         for (int seg = wave; seg < a.batch * a.num_kv_heads; seg += a.waves) {
             const int b = seg / a.num_kv_heads;
-            const int32_t L = a.seq_lens[b];
-            if (L <= 0) fill_segment<D, BF16>(a, b, seg % a.num_kv_heads, L == 0 ? 0.f : __builtin_nanf(""), lane);
+            const int32_t len = a.seq_lens[b];
+            if (len <= 0)
+                fill_segment<D, BF16>(a, b, seg % a.num_kv_heads, len == 0 ? 0.f : __builtin_nanf(""), lane);
         }
     }
-    const int64_t total = static_cast<int64_t>(lds_uniform(s_pref + a.batch)) * a.num_kv_heads;
+    const int64_t total = static_cast<int64_t>(lds_uniform(s_pref + a.batch)) * heads;
     int64_t u, u1;
-    wave_units(total, wave, a.waves, u, u1);
+    wave_units(total, worker, a.waves / gw, u, u1);
     while (u < u1) {
-        const Piece pc = piece_at<true>(s_pref, a.batch, a.num_kv_heads, wave, u, u1);
+        Piece pc = piece_at<true>(s_pref, a.batch, heads, worker, u, u1);
         if (pc.p1 <= pc.p0) break;  // cannot happen for a consistent prefix; never spin
         const int nb = lds_uniform(s_pref + pc.b + 1) - lds_uniform(s_pref + pc.b);
-        const int32_t L = a.seq_lens[pc.b];
-        const int seq_len = L < kPageTokens * nb ? L : kPageTokens * nb;
-        const int64_t seg_first = static_cast<int64_t>(lds_uniform(s_pref + pc.b)) * a.num_kv_heads +
+        const int32_t len = a.seq_lens[pc.b];
+        const int seq_len = len < kPageTokens * nb ? len : kPageTokens * nb;
+        const int64_t seg_first = static_cast<int64_t>(lds_uniform(s_pref + pc.b)) * heads +
                                   static_cast<int64_t>(pc.g) * nb;
+        const int span = pc.p1 - pc.p0;
+        pc.g = pc.g * gw + w_in;
+        pc.slot = pc.slot * gw + w_in;
         if constexpr (VALU) {
             __shared__ ValuLds<D> s_valu[kSplitBlockWaves];
             run_piece_valu<D, R, TIERED>(a, pc, nb, seq_len, lane, s_valu[threadIdx.x / kWave]);
         } else {
             run_piece<D, BF16, R, TIERED>(a, pc, nb, seq_len, lane, seg_first, total);
         }
-        u += pc.p1 - pc.p0;
+        u += span;
     }
 }
 
@@ -771,8 +785,8 @@ __attribute__((amdgpu_waves_per_eu(HCK_SPLIT_WAVES_PER_EU))) void decode_split_k
 // them is merged.  Narrow: one wave per (b, g, h), four heads per block.  Wide
 // (many partials per segment, i.e. small batches): the block's four waves share
 // one (b, g, h) and merge their results through LDS.  The partials of a segment
-// are those of waves k_first..k_last when there are fewer waves than units, and
-// one per unit (the wave that owns it) otherwise.
+// are those of workers k_first..k_last when there are fewer workers than units,
+// and one per unit (the worker that owns it) otherwise.
 #ifndef HCK_WIDE_COMBINE_PIECES
 #define HCK_WIDE_COMBINE_PIECES 12
 #endif
@@ -805,16 +819,22 @@ __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArg
         before += __shfl_xor(before, o);
         total += __shfl_xor(total, o);
     }
-    const int32_t L = a.seq_lens[b];
-    const bool invalid = L < 0 || static_cast<int64_t>(L) > kPageTokens * a.pt_stride;
-    const int nb = row_pages(L, a.pt_stride);
+    const int32_t len = a.seq_lens[b];
+    const bool invalid = len < 0 || static_cast<int64_t>(len) > kPageTokens * a.pt_stride;
+    const int nb = row_pages(len, a.pt_stride);
+    // units of head group g / Lw over the workers' ranges; this head's partials
+    // are slot (worker + b * heads + g / Lw) * Lw + g % Lw
+    const int Lw = a.group_waves;
+    const int heads = a.num_kv_heads / Lw;
+    const int64_t sseg = static_cast<int64_t>(b) * heads + g / Lw;
+    const int w_in = g % Lw;
     f32x4 res;
     float M = -INFINITY, den = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     if (!invalid && nb > 0) {
-        const int64_t T = total * a.num_kv_heads;
-        const int64_t u_a = before * a.num_kv_heads + static_cast<int64_t>(g) * nb;
-        const int N = a.waves;
+        const int64_t T = total * heads;
+        const int64_t u_a = before * heads + static_cast<int64_t>(g / Lw) * nb;
+        const int N = a.waves / Lw;
         const int k_first = static_cast<int>(((u_a + 1) * N - 1) / T);
         const int k_last = static_cast<int>(((u_a + nb) * N - 1) / T);
         const bool per_unit = N > T;  // every non-empty wave holds exactly one unit
@@ -829,7 +849,7 @@ __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArg
                 // waves whose own unit range is empty wrote nothing to their slot
                 const bool use = i < count &&
                                  (per_unit || static_cast<int64_t>(k) * T / N != static_cast<int64_t>(k + 1) * T / N);
-                const int64_t slot = static_cast<int64_t>(use ? k : 0) + seg;
+                const int64_t slot = (static_cast<int64_t>(use ? k : 0) + sseg) * Lw + w_in;
                 const float* pml = a.part_ml + slot * 2 * a.group;
                 const float m_raw = pml[h], l_raw = pml[a.group + h];
                 const f32x4 o_raw =
@@ -941,6 +961,10 @@ size_t prefix_lds_bytes(int batch) { return static_cast<size_t>(batch + 1) * siz
 hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s,
                                const LaunchEvents& ev) {
     if (a.valu && (a.group > kValuMaxGroup || a.fused)) return hipErrorInvalidValue;
+    // a worker's waves must share a block and split the KV heads and waves evenly
+    if (a.group_waves < 1 || kSplitBlockWaves % a.group_waves || a.num_kv_heads % a.group_waves ||
+        a.waves % a.group_waves)
+        return hipErrorInvalidValue;
     const void* k = pick_split(head_dim, dtype, a.tiered != 0, a.valu != 0);
     if (!k || a.waves <= 0) return hipErrorInvalidValue;
     const int blocks = (a.waves + kSplitBlockWaves - 1) / kSplitBlockWaves;
@@ -952,6 +976,8 @@ hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, h
                                  const LaunchEvents& ev) {
     const int segs = a.batch * a.num_kv_heads;
     if (segs == 0) return hipSuccess;
+    if (a.group_waves < 1 || a.num_kv_heads % a.group_waves || a.waves % a.group_waves)
+        return hipErrorInvalidValue;
     // Many partials per segment (waves well above segments): four waves per head.
     const bool wide = static_cast<int64_t>(a.waves) >= static_cast<int64_t>(kWideCombinePieces) * segs;
     const void* k = pick_combine(head_dim, dtype, wide);

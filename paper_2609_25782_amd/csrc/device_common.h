@@ -56,8 +56,9 @@ __device__ inline void block_prefix_pages(const int32_t* __restrict__ seq_lens, 
     if (tid == kThreads - 1) s_pref[batch] = run;
 }
 
-// One piece of the decode work split: wave `wave` handles pages [p0, p1) of
-// row b, KV head g; its partial result goes to slot wave + b * Hkv + g.
+// One piece of the decode work split: worker `k` handles pages [p0, p1) of
+// row b, head group g (of `heads` per row); its partial results go to slot
+// k + b * heads + g (scaled by the waves of a worker, see the decode kernel).
 struct Piece {
     int b, g, p0, p1, slot;
 };
@@ -68,12 +69,13 @@ __device__ __forceinline__ int32_t lds_uniform(const int32_t* p) {
     return __builtin_amdgcn_readfirstlane(*p);
 }
 
-// Units are (row, KV head, page) triples ordered by row, then head, then page;
-// wave k of `waves` owns units [floor(k T / waves), floor((k + 1) T / waves)).
-__device__ __forceinline__ void wave_units(int64_t total_units, int wave, int waves, int64_t& u0,
+// Units are (row, head group, page) triples ordered by row, then head group,
+// then page; worker k of `workers` owns units
+// [floor(k T / workers), floor((k + 1) T / workers)).
+__device__ __forceinline__ void wave_units(int64_t total_units, int worker, int workers, int64_t& u0,
                                            int64_t& u1) {
-    u0 = static_cast<int64_t>(wave) * total_units / waves;
-    u1 = static_cast<int64_t>(wave + 1) * total_units / waves;
+    u0 = static_cast<int64_t>(worker) * total_units / workers;
+    u1 = static_cast<int64_t>(worker + 1) * total_units / workers;
 }
 
 // LDS read used by piece_at: readfirstlane when every lane of the wave asks
@@ -84,12 +86,13 @@ __device__ __forceinline__ int32_t lds_read(const int32_t* p) {
     return *p;
 }
 
-// The piece that starts at unit u (< total), ending no later than u_end.
+// The piece of worker `worker` that starts at unit u (< total), ending no later
+// than u_end; rows have `heads` head groups.
 template <bool kWaveUniform>
-__device__ __forceinline__ Piece piece_at(const int32_t* s_pref, int batch, int num_kv_heads,
-                                          int wave, int64_t u, int64_t u_end) {
-    // largest row b with Hkv * s_pref[b] <= u; it has at least one page
-    const int64_t target = u / num_kv_heads;
+__device__ __forceinline__ Piece piece_at(const int32_t* s_pref, int batch, int heads,
+                                          int worker, int64_t u, int64_t u_end) {
+    // largest row b with heads * s_pref[b] <= u; it has at least one page
+    const int64_t target = u / heads;
     int lo = 0, hi = batch - 1;
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
@@ -99,13 +102,13 @@ __device__ __forceinline__ Piece piece_at(const int32_t* s_pref, int batch, int 
     pc.b = lo;
     const int32_t first = lds_read<kWaveUniform>(s_pref + lo);
     const int nb = lds_read<kWaveUniform>(s_pref + lo + 1) - first;
-    const int64_t rel = u - static_cast<int64_t>(first) * num_kv_heads;
+    const int64_t rel = u - static_cast<int64_t>(first) * heads;
     pc.g = static_cast<int>(rel / nb);
     pc.p0 = static_cast<int>(rel % nb);
     const int64_t seg_end = u + (nb - pc.p0);
     const int64_t e = seg_end < u_end ? seg_end : u_end;
     pc.p1 = pc.p0 + static_cast<int>(e - u);
-    pc.slot = wave + lo * num_kv_heads + pc.g;
+    pc.slot = worker + lo * heads + pc.g;
     return pc;
 }
 

@@ -35,6 +35,7 @@ struct DecodeArgs {
     const int32_t* seq_lens;  // [batch]
     int32_t batch;
     int32_t waves;            // number of waves the work is split over
+    int32_t group_waves;      // waves sharing one work unit, one KV head each (1, or 4 = a block)
     float scale_log2;         // softmax scale * log2(e)
     float* part_o;            // [slots][group][head_dim] unnormalised partial outputs
     float* part_ml;           // [slots][2][group] running max (log2 domain) and weight sum
@@ -66,6 +67,20 @@ inline hipError_t launch_kernel(const void* k, dim3 grid, dim3 block, void** arg
     return hipLaunchKernel(k, grid, block, args, lds, s);
 }
 
+// Waves that share one work unit of the decode split, one KV head each.  With
+// four, a unit is one page of four KV heads and the four waves of a group read
+// their heads' tiles of the same page side by side, which HBM serves faster
+// than four unrelated pages (DRAM row locality).  Four when the KV heads come
+// in fours and the waves in whole groups, else one (a unit is one page of one
+// KV head).  The decode and its partition table follow the same rule.
+#ifndef HCK_GROUP_WAVES
+#define HCK_GROUP_WAVES 4
+#endif
+constexpr int kGroupWaves = HCK_GROUP_WAVES;
+inline int decode_group_waves(int num_kv_heads, int waves) {
+    return (num_kv_heads % kGroupWaves == 0 && waves % kGroupWaves == 0) ? kGroupWaves : 1;
+}
+
 // Bytes of partial results for `slots` slots.
 inline size_t decode_partials_bytes(int64_t slots, int group, int head_dim) {
     return static_cast<size_t>(slots) * group * (head_dim + 2) * sizeof(float);
@@ -84,7 +99,7 @@ int decode_split_blocks_per_cu(int head_dim, int dtype, int batch);
 hipError_t launch_gather_rows(const int32_t* pt, int64_t stride, int32_t max_sessions,
                               const int32_t* sids, int32_t n, int32_t* out, hipStream_t s);
 hipError_t launch_partition(const int32_t* seq_lens, int batch, int num_kv_heads, int waves,
-                            int64_t pt_stride, int32_t* slots, hipStream_t s);
+                            int group_waves, int64_t pt_stride, int32_t* slots, hipStream_t s);
 
 struct CopyEntry {
     int32_t src;       // source page id, or -1: no copy

@@ -1449,6 +1449,7 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
     a.seq_lens = seq_lens;
     a.batch = batch;
     a.waves = waves;
+    a.group_waves = hck::decode_group_waves(pool->d.num_kv_heads, waves);
     a.scale_log2 = scale * 1.4426950408889634f;
     a.part_o = static_cast<float*>(workspace);
     a.part_ml = a.part_o + slots * group * pool->d.head_dim;
@@ -1660,6 +1661,7 @@ int paged_decode_partition(kv_pool* pool, const int32_t* seq_lens, int32_t batch
         return fail(KV_ERR_INVALID, "bad arguments");
     DeviceGuard g(pool->d.device);
     hipError_t e = hck::launch_partition(seq_lens, batch, pool->d.num_kv_heads, waves,
+                                         hck::decode_group_waves(pool->d.num_kv_heads, waves),
                                          pool->d.max_pages_per_session, slots_out,
                                          pool->strm(stream));
     if (e != hipSuccess) return hip_fail(e, "partition launch");

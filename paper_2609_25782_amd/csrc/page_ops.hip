@@ -98,24 +98,31 @@ __global__ __launch_bounds__(kBlockThreads) void table_writes_kernel(const CopyE
     }
 }
 
-// Streaming read of a whole buffer: every thread keeps 8 nontemporal 16-byte
-// loads in flight and folds them into an XOR, one word per block, so the
-// loads cannot be dropped.  It measures the read rate the GPU reaches on
-// plain sequential data with the loads the decode kernel uses.
+// Streaming read of a whole buffer: each block reads whole chunks of 32 KiB
+// (256 threads x 8 nontemporal 16-byte loads, all in flight together), chunks
+// dealt to the blocks in turn, and folds them into an XOR, one word per block,
+// so the loads cannot be dropped.  Contiguous chunks per block read faster
+// than the same loads strided over the whole grid (DRAM row locality).  It
+// measures the read rate the GPU reaches on plain sequential data with the
+// loads the decode kernel uses.
 __global__ __launch_bounds__(kBlockThreads) void read_probe_kernel(const u32x4* __restrict__ p, int64_t n16,
                                                                    uint32_t* __restrict__ out) {
     constexpr int U = 8;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlockThreads;
-    int64_t i = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x;
+    constexpr int64_t kChunk = static_cast<int64_t>(kBlockThreads) * U;  // 16-byte elements
+    const int64_t nchunks = n16 / kChunk;
     u32x4 acc = {0u, 0u, 0u, 0u};
-    for (; i + (U - 1) * stride < n16; i += U * stride) {
+    for (int64_t c = blockIdx.x; c < nchunks; c += gridDim.x) {
+        const u32x4* q = p + c * kChunk + threadIdx.x;
         u32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(p + i + u * stride);
+        for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(q + u * kBlockThreads);
 #pragma unroll
         for (int u = 0; u < U; ++u) acc ^= v[u];
     }
-    for (; i < n16; i += stride) acc ^= __builtin_nontemporal_load(p + i);
+    // elements past the last whole chunk
+    for (int64_t i = nchunks * kChunk + static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; i < n16;
+         i += static_cast<int64_t>(gridDim.x) * kBlockThreads)
+        acc ^= __builtin_nontemporal_load(p + i);
     unsigned x = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
 #pragma unroll
     for (int o = kWave / 2; o > 0; o >>= 1) x ^= __shfl_xor(x, o);
@@ -345,22 +352,28 @@ __global__ __launch_bounds__(kBlockThreads) void gather_rows_kernel(const int32_
     }
 }
 
-// One thread per wave: enumerate its pieces exactly as the decode kernel does
-// (here the lanes of a hardware wave work on different decode waves).
+// One thread per worker: enumerate its pieces exactly as the decode kernel
+// does (here the lanes of a hardware wave work on different decode workers),
+// and write the record of each of its `group_waves` waves.
 __global__ __launch_bounds__(kBlockThreads) void partition_kernel(const int32_t* seq_lens, int batch,
                                                                   int num_kv_heads, int waves,
-                                                                  int64_t stride, int32_t* slots) {
+                                                                  int group_waves, int64_t stride,
+                                                                  int32_t* slots) {
     extern __shared__ int32_t s_pref[];
     block_prefix_pages(seq_lens, batch, stride, s_pref);
     __syncthreads();
-    const int64_t total = static_cast<int64_t>(lds_uniform(s_pref + batch)) * num_kv_heads;
-    for (int k = blockIdx.x * kBlockThreads + threadIdx.x; k < waves; k += gridDim.x * kBlockThreads) {
+    const int heads = num_kv_heads / group_waves;
+    const int workers = waves / group_waves;
+    const int64_t total = static_cast<int64_t>(lds_uniform(s_pref + batch)) * heads;
+    for (int k = blockIdx.x * kBlockThreads + threadIdx.x; k < workers; k += gridDim.x * kBlockThreads) {
         int64_t u, u1;
-        wave_units(total, k, waves, u, u1);
+        wave_units(total, k, workers, u, u1);
         while (u < u1) {
-            const Piece pc = piece_at<false>(s_pref, batch, num_kv_heads, k, u, u1);
+            const Piece pc = piece_at<false>(s_pref, batch, heads, k, u, u1);
             if (pc.p1 <= pc.p0) break;  // cannot happen for a consistent prefix; never spin
-            reinterpret_cast<int4*>(slots)[pc.slot] = make_int4(pc.b, pc.g, pc.p0, pc.p1);
+            for (int w = 0; w < group_waves; ++w)
+                reinterpret_cast<int4*>(slots)[static_cast<int64_t>(pc.slot) * group_waves + w] =
+                    make_int4(pc.b, pc.g * group_waves + w, pc.p0, pc.p1);
             u += pc.p1 - pc.p0;
         }
     }
@@ -466,14 +479,15 @@ hipError_t launch_gather_rows(const int32_t* pt, int64_t stride, int32_t max_ses
 }
 
 hipError_t launch_partition(const int32_t* seq_lens, int batch, int num_kv_heads, int waves,
-                            int64_t pt_stride, int32_t* slots, hipStream_t s) {
+                            int group_waves, int64_t pt_stride, int32_t* slots, hipStream_t s) {
+    if (group_waves < 1 || num_kv_heads % group_waves || waves % group_waves) return hipErrorInvalidValue;
     const int64_t n = static_cast<int64_t>(waves) + static_cast<int64_t>(batch) * num_kv_heads;
     hipLaunchKernelGGL(partition_holes_kernel, dim3(grid_for(n, 4096)), dim3(kBlockThreads), 0, s, slots, n);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || batch == 0) return e;
     const size_t lds = static_cast<size_t>(batch + 1) * sizeof(int32_t);
-    hipLaunchKernelGGL(partition_kernel, dim3(grid_for(waves, 1024)), dim3(kBlockThreads), lds, s,
-                       seq_lens, batch, num_kv_heads, waves, pt_stride, slots);
+    hipLaunchKernelGGL(partition_kernel, dim3(grid_for(waves / group_waves, 1024)), dim3(kBlockThreads), lds, s,
+                       seq_lens, batch, num_kv_heads, waves, group_waves, pt_stride, slots);
     return hipGetLastError();
 }
 
