@@ -60,7 +60,8 @@ def split_kernel_bytes(seq_lens, hq, hkv, d, elt):
 
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "decode_split_layer_b32_pmc.md")
 SPLIT_SOURCES = ("paper_2609_25782_amd/csrc/decode_attention.hip",
-                 "paper_2609_25782_amd/csrc/device_common.h")
+                 "paper_2609_25782_amd/csrc/device_common.h",
+                 "paper_2609_25782_amd/csrc/kernels.h")
 
 
 def measured_traffic():
