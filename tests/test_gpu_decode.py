@@ -191,6 +191,48 @@ def test_constant_v_gives_constant_output(dev):
     assert np.all(got == 1.0)
 
 
+def test_identical_keys_give_mean_of_values(dev):
+    """All keys of a (row, KV head) equal: every weight is 1/L and the output is
+    the mean of V (P3).  The scores are then bitwise equal, every exp2 is exactly
+    1, the weight sums are exact integers and every merge factor is 1, so the
+    only roundings are the float32 sums of V and the bf16 output: within one
+    bf16 half-unit (2^-9 relative, bounded here by 2^-8) of the fp64 mean."""
+    lens = [1000, 37, 5000, 16, 1]
+    case = Case(1, 32, 4, 128, "bf16", lens, seed=16)
+    for b in range(case.batch):
+        k, v = case.kv[b]
+        case.kv[b] = (np.ascontiguousarray(np.broadcast_to(k[:1], k.shape)), v)
+    got = _run(case, dev, fused=False)
+    for b in range(case.batch):
+        mean = synth.bf16_bits_to_f32(case.kv[b][1]).astype(np.float64).mean(axis=0)  # [Hkv, D]
+        for h in range(32):
+            want = mean[h // 8]
+            assert np.all(np.abs(got[b, h] - want) <= 2 ** -8 * np.abs(want) + 1e-6)
+
+
+def test_key_shift_leaves_output_unchanged(dev):
+    """Adding the same vector c to every key of a (row, KV head) adds q.c to
+    every score of a query head, which the softmax removes (P9).  float32 pool;
+    keys and c on a 2^-8 grid, so k + c is exact and only the scores' float32
+    rounding differs (about 1e-5 absolute at |q.c| ~ 24, 1e-6 relative in the
+    weights): the outputs agree within 1e-5 of the largest output."""
+    lens = [700, 33, 2500]
+    a = Case(1, 8, 2, 64, "f32", lens, seed=17)
+    b = Case(1, 8, 2, 64, "f32", lens, seed=17)
+    rng = np.random.default_rng(18)
+    shift = (np.round(rng.standard_normal((2, 64)) * 3 * 256) / 256).astype(np.float32)
+    for i in range(len(lens)):
+        k, v = a.kv[i]
+        kq = (np.round(k.astype(np.float64) * 256) / 256).astype(np.float32)
+        a.kv[i] = (kq, v)
+        b.kv[i] = ((kq + shift[None]).astype(np.float32), v)
+    ga, gb = _run(a, dev), _run(b, dev)
+    tolerance_check(ga, a.oracle_out())
+    diff = float(np.max(np.abs(ga - gb)))
+    _say("key shift: max difference %.3g, max |out| %.3g" % (diff, float(np.max(np.abs(ga)))))
+    assert diff <= 1e-5 * float(np.max(np.abs(ga)))
+
+
 def test_gqa_rows_identical_for_equal_queries(dev):
     """Equal queries within a group give bitwise identical output rows (P11)."""
     case = Case(1, 32, 4, 128, "bf16", [2500, 60], seed=13)

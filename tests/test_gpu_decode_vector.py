@@ -121,6 +121,22 @@ def test_single_token_and_constant_v(dev):
     assert np.all(_run(case, dev) == 1.0)
 
 
+def test_identical_keys_give_mean_of_values(dev):
+    """All keys of a (row, KV head) equal: the output is the mean of V within a
+    bf16 half-unit (P3); see the matrix-core test for the rounding argument."""
+    lens = [1000, 37, 5000, 16, 1]
+    case = Case(1, 32, 4, 128, "bf16", lens, seed=42)
+    for b in range(case.batch):
+        k, v = case.kv[b]
+        case.kv[b] = (np.ascontiguousarray(np.broadcast_to(k[:1], k.shape)), v)
+    got = _run(case, dev)
+    for b in range(case.batch):
+        mean = synth.bf16_bits_to_f32(case.kv[b][1]).astype(np.float64).mean(axis=0)
+        for h in range(32):
+            want = mean[h // 8]
+            assert np.all(np.abs(got[b, h] - want) <= 2 ** -8 * np.abs(want) + 1e-6)
+
+
 def test_gqa_rows_identical_for_equal_queries(dev):
     case = Case(1, 32, 4, 128, "bf16", [2500, 60], seed=39)
     for b in range(case.batch):
