@@ -128,7 +128,7 @@ def test_identical_keys_give_mean_of_values(dev):
     case = Case(1, 32, 4, 128, "bf16", lens, seed=42)
     for b in range(case.batch):
         k, v = case.kv[b]
-        case.kv[b] = (np.ascontiguousarray(np.broadcast_to(k[:1], k.shape)), v)
+        case.kv[b] = (np.broadcast_to(k[:1], k.shape).copy(), v)
     got = _run(case, dev)
     for b in range(case.batch):
         mean = synth.bf16_bits_to_f32(case.kv[b][1]).astype(np.float64).mean(axis=0)
