@@ -329,6 +329,35 @@ def measure_resume_mix(seed: int, steps: int, warmup: int):
                                 "steps_to_promote": steps_needed, "pages_promoted": moved})
         log("lazy resume: %s" % json.dumps(lazy["budgets"][-1]))
         pool.evict(sids, stream=main_s)
+    # the largest budget again with the promotion confined to 16 CUs and the
+    # decode on the other 240 (disjoint CU sets, as for the eager resume)
+    dec_s, cpy_s = split_streams(2)
+    sids = picks[k % len(picks)]
+    k += 1
+    torch.cuda.synchronize()
+    pool.resume_lazy(sids, stream=dec_s.stream)
+    steps_needed, dec_ms, moved = 0, [], 0
+    while True:
+        cpy_s.stream.wait_stream(dec_s.stream)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        n = pool.promote(4096, stream=cpy_s.stream)
+        ev[0].record(dec_s.stream)
+        decode48(dec_s.stream)
+        ev[1].record(dec_s.stream)
+        dec_s.stream.wait_stream(cpy_s.stream)
+        torch.cuda.synchronize()
+        moved += n
+        if n == 0:
+            break
+        steps_needed += 1
+        dec_ms.append(ev[0].elapsed_time(ev[1]))
+    lazy["cu_split_16_copy_cus"] = {"pages_per_step": 4096, "decode48_ms_while_promoting": round(float(np.mean(dec_ms)), 3),
+                                    "steps_to_promote": steps_needed, "pages_promoted": moved}
+    log("lazy resume, promotion on 16 CUs: %s" % json.dumps(lazy["cu_split_16_copy_cus"]))
+    pool.evict(sids, stream=dec_s.stream)
+    torch.cuda.synchronize()
+    dec_s.close()
+    cpy_s.close()
     pool.set_spill(False)
     torch.cuda.synchronize()
     # partial residency: sessions paused with all pages resident, a fraction of
