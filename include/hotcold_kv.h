@@ -454,7 +454,12 @@ int kv_stream_destroy(kv_stream_t stream);
  */
 int32_t paged_decode_waves(const kv_pool* pool);
 
-/* Override the number of decode waves (>= 1); 0 restores the automatic choice. */
+/*
+ * Override the number of decode waves (>= 1); 0 restores the automatic choice.
+ * A count that is not a multiple of 4 (or a pool whose KV heads are not) makes
+ * every wave its own worker instead of four waves sharing each page (see
+ * paged_decode_partition).
+ */
 int kv_pool_set_decode_waves(kv_pool* pool, int32_t waves);
 
 enum kv_combine_mode {
