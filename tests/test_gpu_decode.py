@@ -63,7 +63,9 @@ def test_tiny_config_f32(dev):
 
 @pytest.mark.parametrize("dtype,D,hq,hkv", [("bf16", 128, 32, 4), ("bf16", 64, 8, 2),
                                            ("bf16", 128, 16, 1), ("bf16", 64, 4, 4),
-                                           ("f32", 128, 8, 1), ("f32", 64, 6, 2)])
+                                           ("f32", 128, 8, 1), ("f32", 64, 6, 2),
+                                           ("bf16", 128, 32, 8), ("bf16", 64, 16, 16),
+                                           ("f32", 64, 16, 8)])
 def test_ragged_lengths(dev, dtype, D, hq, hkv):
     lens = [1, 15, 16, 17, 31, 33, 100, 1000, 4097, 250]
     case = Case(1, hq, hkv, D, dtype, lens, seed=3)
@@ -85,6 +87,15 @@ def test_split_invariance(dev, waves, fused):
     """Any number of waves, either merge of the partials: the oracle's answer
     within tolerance (P10)."""
     case = Case(1, 32, 4, 128, "bf16", [5000, 16, 1, 777, 3000, 48], seed=5)
+    got = _run(case, dev, waves=waves, fused=fused)
+    tolerance_check(got, case.oracle_out())
+
+
+@pytest.mark.parametrize("fused", [True, False])
+@pytest.mark.parametrize("waves", [8, 64, 1000, 4096])
+def test_split_invariance_two_head_groups(dev, waves, fused):
+    """Eight KV heads: workers of four waves take two head groups per row."""
+    case = Case(1, 32, 8, 128, "bf16", [5000, 16, 1, 777, 3000, 48], seed=19)
     got = _run(case, dev, waves=waves, fused=fused)
     tolerance_check(got, case.oracle_out())
 
@@ -273,18 +284,19 @@ def test_needle(dev, where):
 def test_partition_table_matches_reference(dev):
     from oracle import partition
     from paper_2609_25782_amd.pool import HotColdPool
-    pool = HotColdPool(1, 4, 64, "bf16", 8, 0, 1, 4096)
     rng = np.random.default_rng(15)
-    for trial in range(8):
-        B = int(rng.integers(1, 40))
-        lens = [int(x) for x in rng.integers(0, 20000, size=B)]
-        waves = int(rng.choice([1, 5, 64, 300, 2048]))
-        _say("partition trial %d: B=%d waves=%d" % (trial, B, waves))
-        sl = torch.tensor(lens, dtype=torch.int32, device=dev)
-        got = pool.partition(sl, waves).cpu().numpy()
-        want = np.array(partition.slot_table(lens, 4, waves), dtype=np.int32)
-        assert np.array_equal(got, want)
-    pool.close()
+    for hkv in (4, 8, 16, 2):
+        pool = HotColdPool(1, hkv, 64, "bf16", 8, 0, 1, 4096)
+        for trial in range(6):
+            B = int(rng.integers(1, 40))
+            lens = [int(x) for x in rng.integers(0, 20000, size=B)]
+            waves = int(rng.choice([1, 5, 64, 300, 2048]))
+            _say("partition trial %d: Hkv=%d B=%d waves=%d" % (trial, hkv, B, waves))
+            sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+            got = pool.partition(sl, waves).cpu().numpy()
+            want = np.array(partition.slot_table(lens, hkv, waves), dtype=np.int32)
+            assert np.array_equal(got, want)
+        pool.close()
 
 
 def test_repeated_calls_and_batch_changes_are_consistent(dev):

@@ -50,7 +50,8 @@ def _run(case: Case, dev, poison=False, waves=None, vector=True):
     return res
 
 
-@pytest.mark.parametrize("D,hq,hkv", [(128, 32, 4), (64, 8, 2), (128, 4, 4), (64, 6, 2), (128, 7, 1)])
+@pytest.mark.parametrize("D,hq,hkv", [(128, 32, 4), (64, 8, 2), (128, 4, 4), (64, 6, 2), (128, 7, 1),
+                                      (128, 32, 8), (64, 16, 16)])
 def test_ragged_lengths(dev, D, hq, hkv):
     """Groups of 8, 4, 1, 3 and 7 query heads; lengths across page boundaries."""
     case = Case(1, hq, hkv, D, "bf16", [1, 15, 16, 17, 31, 33, 100, 1000, 4097, 250], seed=31)
