@@ -61,24 +61,29 @@ def build(force: bool = False) -> str:
     return _LIB_PATH
 
 
+def load_library(path: str):
+    """A ctypes handle on a compiled copy of the C oracle, its functions typed."""
+    lib = ctypes.CDLL(path)
+    lib.oracle_paged_attention.restype = ctypes.c_int
+    lib.oracle_paged_attention.argtypes = [
+        ctypes.c_void_p, ctypes.c_long, ctypes.POINTER(_Layout), ctypes.c_int,
+        ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_long,
+        ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_long, ctypes.c_int]
+    lib.oracle_page_bytes.restype = ctypes.c_long
+    lib.oracle_page_bytes.argtypes = [ctypes.POINTER(_Layout)]
+    lib.oracle_elem_offset.restype = ctypes.c_long
+    lib.oracle_elem_offset.argtypes = [ctypes.POINTER(_Layout), ctypes.c_long, ctypes.c_int,
+                                       ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    return lib
+
+
 def _load():
     global _lib
     with _lock:
         if _lib is None:
             build()
-            lib = ctypes.CDLL(_LIB_PATH)
-            lib.oracle_paged_attention.restype = ctypes.c_int
-            lib.oracle_paged_attention.argtypes = [
-                ctypes.c_void_p, ctypes.c_long, ctypes.POINTER(_Layout), ctypes.c_int,
-                ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_long,
-                ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p,
-                ctypes.c_long, ctypes.c_int]
-            lib.oracle_page_bytes.restype = ctypes.c_long
-            lib.oracle_page_bytes.argtypes = [ctypes.POINTER(_Layout)]
-            lib.oracle_elem_offset.restype = ctypes.c_long
-            lib.oracle_elem_offset.argtypes = [ctypes.POINTER(_Layout), ctypes.c_long, ctypes.c_int,
-                                               ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]
-            _lib = lib
+            _lib = load_library(_LIB_PATH)
     return _lib
 
 
