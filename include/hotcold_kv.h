@@ -137,7 +137,7 @@ typedef struct kv_pool_desc {
     int32_t flags;                 /* KV_POOL_METADATA_ONLY or 0 */
 } kv_pool_desc;
 
-typedef struct kv_pool_stats {
+typedef struct kv_pool_stats_t {
     int32_t free_hot_pages;
     int32_t free_cold_pages;
     int32_t active_sessions;
@@ -154,7 +154,7 @@ typedef struct kv_pool_stats {
     int64_t spilled_pages;         /* pages placed or left in the cold tier by spill */
     int64_t promoted_pages;        /* spilled pages moved back to the hot tier */
     int64_t cold_active_pages;     /* now: pages of ACTIVE sessions living in the cold tier */
-} kv_pool_stats;
+} kv_pool_stats_t;
 
 /* ----------------------------------------------------------------------- */
 /* Pool                                                                     */
@@ -181,7 +181,13 @@ int kv_pool_create(const kv_pool_desc* desc, void* hot_base, size_t hot_bytes, v
 /* Free host bookkeeping.  The caller must have synchronised streams using the pool. */
 void kv_pool_destroy(kv_pool* pool);
 
-int kv_pool_stats_get(const kv_pool* pool, kv_pool_stats* out);
+/*
+ * Introspection: free pages, sessions by state, pages and bytes copied in each
+ * direction, resume hit-rate counts (resident / total pages of resumed
+ * sessions, Sec. IV "Methodology"), LRU, spill and promotion counts.  *out is a
+ * host struct the caller owns.  Errors: KV_ERR_INVALID (NULL argument).
+ */
+int kv_pool_stats(const kv_pool* pool, kv_pool_stats_t* out);
 
 /* ----------------------------------------------------------------------- */
 /* Sessions                                                                 */
@@ -244,7 +250,9 @@ int kv_evict_pages(kv_pool* pool, int32_t n, kv_stream_t stream, int32_t* evicte
  * with another session).  It is its own cold copy, so evicting it writes
  * nothing; its entry keeps naming the cold page until the page is fetched or
  * the whole session is evicted.
- * Errors: KV_ERR_INVALID.
+ * Errors: KV_ERR_INVALID; KV_ERR_STATE when turning spill off while some
+ * session's row still names spilled pages (decode without spill would read
+ * those entries as invalid ids): promote them or evict the session first.
  */
 int kv_pool_set_spill(kv_pool* pool, int32_t enable);
 

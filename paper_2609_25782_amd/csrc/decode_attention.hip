@@ -739,6 +739,8 @@ __attribute__((amdgpu_waves_per_eu(HCK_SPLIT_WAVES_PER_EU))) void decode_split_k
     extern __shared__ int32_t s_pref[];
     block_prefix_pages<kSplitBlockThreads>(a.seq_lens, a.batch, a.pt_stride, s_pref);
     __syncthreads();
+    if (blockIdx.x == 0)  // the combine reads the row prefix instead of rescanning the lengths
+        for (int b = threadIdx.x; b <= a.batch; b += kSplitBlockThreads) a.row_pref[b] = s_pref[b];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kSplitBlockWaves + threadIdx.x / kWave);
     if (wave >= a.waves) return;
@@ -808,17 +810,8 @@ __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArg
     const int quad = lane % kQuads, grp = lane / kQuads;
     const int gid = WIDE ? wave * kGroups + grp : grp;
 
-    int64_t before = 0, total = 0;
-    for (int r = lane; r < a.batch; r += kWave) {
-        const int n = row_pages(a.seq_lens[r], a.pt_stride);
-        total += n;
-        if (r < b) before += n;
-    }
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) {
-        before += __shfl_xor(before, o);
-        total += __shfl_xor(total, o);
-    }
+    // pages of the rows before b, and of all rows (the split kernel's prefix)
+    const int64_t before = a.row_pref[b], total = a.row_pref[a.batch];
     const int32_t len = a.seq_lens[b];
     const bool invalid = len < 0 || static_cast<int64_t>(len) > kPageTokens * a.pt_stride;
     const int nb = row_pages(len, a.pt_stride);

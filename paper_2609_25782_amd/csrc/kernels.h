@@ -39,6 +39,7 @@ struct DecodeArgs {
     float scale_log2;         // softmax scale * log2(e)
     float* part_o;            // [slots][group][head_dim] unnormalised partial outputs
     float* part_ml;           // [slots][2][group] running max (log2 domain) and weight sum
+    int32_t* row_pref;        // [batch + 1] pages before each row (written by the split, read by the combine)
     void* out;                // [batch][num_q_heads][head_dim]
     int32_t* counters;        // [batch * num_kv_heads] arrival counters, zero between calls
     int32_t fused;            // 1: the last wave of each (b, g) merges its partials
@@ -85,6 +86,19 @@ inline int decode_group_waves(int num_kv_heads, int waves) {
 inline size_t decode_partials_bytes(int64_t slots, int group, int head_dim) {
     return static_cast<size_t>(slots) * group * (head_dim + 2) * sizeof(float);
 }
+
+// Decode workspace: the partials, then the row page prefix (batch + 1 int32),
+// rounded up to 256 bytes.
+inline size_t decode_workspace_bytes(int64_t slots, int group, int head_dim, int batch) {
+    const size_t n = decode_partials_bytes(slots, group, head_dim) + (static_cast<size_t>(batch) + 1) * 4;
+    return (n + 255) & ~static_cast<size_t>(255);
+}
+
+// The decode call behind paged_decode_attention and its no-allocation variant
+// (host runtime).  With no_alloc the call takes no profiling events.
+int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page_table, int64_t pt_stride,
+                const int32_t* seq_lens, int32_t batch, int32_t num_q_heads, float scale, void* out,
+                void* workspace, size_t ws_bytes, kv_stream_t stream, bool no_alloc);
 
 hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s,
                                const LaunchEvents& ev = {});

@@ -176,7 +176,7 @@ struct kv_pool {
     std::vector<Session> sessions;
     int64_t clock = 0;                // pause stamps
     std::map<int64_t, int32_t> lru;  // stamp -> sid of paused sessions with resident pages
-    kv_pool_stats st{};
+    kv_pool_stats_t st{};
     int cus = 0;
     int32_t waves_override = 0;
     int32_t copy_blocks = 0;  // cap of the page-copy grid (0: default)
@@ -731,7 +731,7 @@ int kv_pool_create(const kv_pool_desc* desc, void* hot_base, size_t hot_bytes, v
 
 void kv_pool_destroy(kv_pool* pool) { delete pool; }
 
-int kv_pool_stats_get(const kv_pool* pool, kv_pool_stats* out) {
+int kv_pool_stats(const kv_pool* pool, kv_pool_stats_t* out) {
     if (!pool || !out) return fail(KV_ERR_INVALID, "NULL argument");
     *out = pool->st;
     out->free_hot_pages = pool->hot_free.free_count();
@@ -1103,6 +1103,15 @@ int kv_fill_synthetic(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_t seed
 
 int kv_pool_set_spill(kv_pool* pool, int32_t enable) {
     if (!pool || (enable != 0 && enable != 1)) return fail(KV_ERR_INVALID, "bad arguments");
+    if (!enable) {
+        // Without spill, decode reads the pool's rows with the plain kernel, for
+        // which a cold-tagged entry is an invalid id: refuse while rows name
+        // spilled pages (promote them, or evict their sessions, first).
+        for (size_t sid = 0; sid < pool->sessions.size(); ++sid)
+            for (uint8_t sp : pool->sessions[sid].spilled)
+                if (sp)
+                    return fail(KV_ERR_STATE, "session %zu still has pages in the cold tier", sid);
+    }
     pool->spill = enable != 0;
     return KV_OK;
 }
@@ -1400,13 +1409,24 @@ size_t paged_decode_workspace_bytes(const kv_pool* pool, int32_t batch, int32_t 
     DeviceGuard g(pool->d.device);
     const int64_t slots = static_cast<int64_t>(pool->decode_waves()) +
                           static_cast<int64_t>(batch) * pool->d.num_kv_heads;
-    return hck::decode_partials_bytes(slots, group, pool->d.head_dim);
+    return hck::decode_workspace_bytes(slots, group, pool->d.head_dim, batch);
 }
 
 int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const int32_t* page_table,
                            int64_t pt_stride, const int32_t* seq_lens, int32_t batch,
                            int32_t num_q_heads, float scale, void* out, void* workspace,
                            size_t ws_bytes, kv_stream_t stream) {
+    return hck::decode_impl(pool, layer, q, page_table, pt_stride, seq_lens, batch, num_q_heads, scale,
+                            out, workspace, ws_bytes, stream, /*no_alloc=*/false);
+}
+
+}  // extern "C"
+
+namespace hck {
+
+int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page_table, int64_t pt_stride,
+                const int32_t* seq_lens, int32_t batch, int32_t num_q_heads, float scale, void* out,
+                void* workspace, size_t ws_bytes, kv_stream_t stream, bool no_alloc) {
     if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
     if (pool->meta) return fail(KV_ERR_INVALID, "metadata-only pool cannot decode");
     if (layer < 0 || layer >= pool->d.num_layers) return fail(KV_ERR_INVALID, "bad layer %d", layer);
@@ -1432,7 +1452,7 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
     DeviceGuard g(pool->d.device);
     const int32_t waves = pool->decode_waves();
     const int64_t slots = static_cast<int64_t>(waves) + static_cast<int64_t>(batch) * pool->d.num_kv_heads;
-    const size_t need = hck::decode_partials_bytes(slots, group, pool->d.head_dim);
+    const size_t need = hck::decode_workspace_bytes(slots, group, pool->d.head_dim, batch);
     if (ws_bytes < need) return fail(KV_ERR_INVALID, "workspace %zu bytes, need %zu", ws_bytes, need);
     hck::DecodeArgs a;
     a.hot = pool->hot;
@@ -1453,6 +1473,8 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
     a.scale_log2 = scale * 1.4426950408889634f;
     a.part_o = static_cast<float*>(workspace);
     a.part_ml = a.part_o + slots * group * pool->d.head_dim;
+    a.row_pref = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) +
+                                            hck::decode_partials_bytes(slots, group, pool->d.head_dim));
     a.out = out;
     a.counters = pool->counters;
     a.fused = pool->combine_mode == KV_COMBINE_FUSED ? 1 : 0;
@@ -1478,8 +1500,10 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
     const bool capturing = cap != hipStreamCaptureStatusNone;
     if (capturing && (a.fused || staged))
         return fail(KV_ERR_INVALID, "graph capture supports the separate merge without staged pages");
-    // decode calls of one pool share its counters (fused merge): order them across streams
-    if (pool->decode_pending && !capturing) {
+    // Fused-merge calls share the pool's arrival counters: order them across
+    // streams.  Separate-merge calls share nothing of the pool's, so decodes on
+    // different streams (say two batches on disjoint CU sets) run concurrently.
+    if (a.fused && pool->decode_pending) {
         hipError_t w = hipStreamWaitEvent(st, pool->decode_event, 0);
         if (w != hipSuccess) return hip_fail(w, "hipStreamWaitEvent(decode)");
     }
@@ -1487,20 +1511,24 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
         hipError_t w = hipStreamWaitEvent(st, pool->half_ready[half], 0);
         if (w != hipSuccess) return hip_fail(w, "hipStreamWaitEvent(staging)");
     }
-    hck::LaunchEvents ev = capturing ? hck::LaunchEvents{} : pool->prof_events();
+    // The no-allocation entry point takes no profiling events (creating one may allocate).
+    const bool prof = !capturing && !no_alloc;
+    hck::LaunchEvents ev = prof ? pool->prof_events() : hck::LaunchEvents{};
     hipError_t e = hck::launch_decode_split(a, pool->d.head_dim, pool->d.dtype, st, ev);
     pool->prof_done(KV_KERNEL_DECODE_SPLIT, ev, e);
     if (e != hipSuccess) return hip_fail(e, "decode split launch");
     if (!a.fused) {
-        ev = capturing ? hck::LaunchEvents{} : pool->prof_events();
+        ev = prof ? pool->prof_events() : hck::LaunchEvents{};
         e = hck::launch_decode_combine(a, pool->d.head_dim, pool->d.dtype, st, ev);
         pool->prof_done(KV_KERNEL_DECODE_COMBINE, ev, e);
         if (e != hipSuccess) return hip_fail(e, "decode combine launch");
     }
     if (capturing) return KV_OK;
-    e = hipEventRecord(pool->decode_event, st);
-    if (e != hipSuccess) return hip_fail(e, "hipEventRecord(decode)");
-    pool->decode_pending = true;
+    if (a.fused) {
+        e = hipEventRecord(pool->decode_event, st);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord(decode)");
+        pool->decode_pending = true;
+    }
     if (staged) {
         e = hipEventRecord(pool->half_free[half], st);
         if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
@@ -1508,6 +1536,10 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
     }
     return KV_OK;
 }
+
+}  // namespace hck
+
+extern "C" {
 
 int kv_pool_set_staging(kv_pool* pool, void* staging, size_t bytes, int32_t* slots) {
     if (!pool || pool->meta) return fail(KV_ERR_INVALID, "no device pool");

@@ -45,7 +45,7 @@ class kv_pool_desc(ctypes.Structure):
         "flags")]
 
 
-class kv_pool_stats(ctypes.Structure):
+class kv_pool_stats_t(ctypes.Structure):
     _fields_ = [("free_hot_pages", ctypes.c_int32), ("free_cold_pages", ctypes.c_int32),
                 ("active_sessions", ctypes.c_int32), ("paused_sessions", ctypes.c_int32),
                 ("pages_to_cold", ctypes.c_int64), ("pages_to_hot", ctypes.c_int64),
@@ -73,7 +73,7 @@ _SIGS = {
     "kv_pool_create": (ctypes.c_int, [ctypes.POINTER(kv_pool_desc), _P, _SZ, _P, _SZ, _P, _P,
                                       ctypes.POINTER(_P)]),
     "kv_pool_destroy": (None, [_P]),
-    "kv_pool_stats_get": (ctypes.c_int, [_P, ctypes.POINTER(kv_pool_stats)]),
+    "kv_pool_stats": (ctypes.c_int, [_P, ctypes.POINTER(kv_pool_stats_t)]),
     "kv_session_create": (ctypes.c_int, [_P, _I32, _PI32, _P, _PI32]),
     "kv_session_import_cold": (ctypes.c_int, [_P, _I32, _PI32, _PI32]),
     "kv_session_extend": (ctypes.c_int, [_P, _I32, _I32, _P]),
@@ -160,9 +160,9 @@ def kv_pool_destroy(pool: int) -> None:
     _lib.kv_pool_destroy(pool)
 
 
-def kv_pool_stats_get(pool: int) -> dict:
-    st = kv_pool_stats()
-    _check(_lib.kv_pool_stats_get(pool, ctypes.byref(st)), "kv_pool_stats_get")
+def kv_pool_stats(pool: int) -> dict:
+    st = kv_pool_stats_t()
+    _check(_lib.kv_pool_stats(pool, ctypes.byref(st)), "kv_pool_stats")
     return st.as_dict()
 
 

@@ -51,7 +51,7 @@ class HotColdPool:
         self.handle = kv.kv_pool_create(self.desc, self.hot.data_ptr(), self.hot.numel(),
                                         self.cold.data_ptr(), self.cold.numel(),
                                         self.page_table.data_ptr(), _stream(stream))
-        self._ws = None
+        self._ws = {}   # decode workspace per stream: decodes on different streams may overlap
 
     # -- lifetime ----------------------------------------------------------
     def close(self) -> None:
@@ -135,14 +135,21 @@ class HotColdPool:
         kv.kv_pool_set_copy_blocks(self.handle, int(blocks))
 
     def stats(self) -> dict:
-        return kv.kv_pool_stats_get(self.handle)
+        return kv.kv_pool_stats(self.handle)
 
     # -- decode ------------------------------------------------------------
-    def workspace(self, batch: int, num_q_heads: int) -> torch.Tensor:
+    def workspace(self, batch: int, num_q_heads: int, stream=None) -> torch.Tensor:
+        """The decode workspace of `stream` (one per stream: separate-merge decodes
+        on different streams run concurrently and must not share partials)."""
+        key = _stream(stream)
         need = kv.paged_decode_workspace_bytes(self.handle, batch, num_q_heads)
-        if self._ws is None or self._ws.numel() < need:
-            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
-        return self._ws
+        ws = self._ws.get(key)
+        if ws is None or ws.numel() < need:
+            # allocated on that stream, so torch reuses a dropped buffer only in its order
+            with torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream()):
+                ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+            self._ws[key] = ws
+        return ws
 
     def decode(self, layer: int, q: torch.Tensor, seq_lens: torch.Tensor,
                page_table: Optional[torch.Tensor] = None, scale: Optional[float] = None,
@@ -153,7 +160,7 @@ class HotColdPool:
         B, Hq, D = q.shape
         if out is None:
             out = torch.empty_like(q)
-        ws = self.workspace(B, Hq)
+        ws = self.workspace(B, Hq, stream)
         kv.paged_decode_attention(self.handle, layer, q.data_ptr(), pt.data_ptr(), pt.shape[1],
                                   seq_lens.data_ptr(), B, Hq, float(scale if scale is not None else D ** -0.5),
                                   out.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream))

@@ -166,7 +166,7 @@ class LibraryPool:
         return kv.kv_promote_pages(self.h, n)
 
     def stats(self) -> Dict[str, int]:
-        return kv.kv_pool_stats_get(self.h)
+        return kv.kv_pool_stats(self.h)
 
     def close(self) -> None:
         if self.own and self.h:

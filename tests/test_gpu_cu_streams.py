@@ -83,3 +83,46 @@ def test_decode_beside_resume_on_split_streams(dev, copy_slots):
     dec.close()
     cpy.close()
     pool.close()
+
+
+def test_two_batches_decode_concurrently_on_split_streams(dev):
+    """Two batches of one pool decode at the same time on two streams with
+    disjoint CU sets.  Separate-merge decodes share nothing of the pool's, so the
+    library does not order them, and each keeps its own workspace: each output is
+    bit-identical to the same batch decoded alone, and matches the oracle.
+    Repeated with the calls issued in both orders."""
+    from paper_2609_25782_amd.pool import split_streams
+    lens = [5000, 300, 12000, 17, 2048, 7777, 900, 4100]
+    case = Case(1, 32, 4, 128, "bf16", lens, seed=73, slack=1.2)
+    pool = build_gpu(case, dev, pool_kwargs={"max_sessions": 8})
+    q = to_device(case.q, "bf16", dev)
+    sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+    ref = case.oracle_out()
+    halves = []
+    for rows in (slice(0, 4), slice(4, 8)):
+        qa, sa = q[rows].contiguous(), sl[rows].contiguous()
+        pa = pool.page_table[rows].contiguous()
+        alone = pool.decode(0, qa, sa, page_table=pa).clone()
+        torch.cuda.synchronize()
+        tolerance_check(to_host(alone), ref[rows])
+        halves.append((qa, sa, pa, alone))
+    from paper_2609_25782_amd import hotcold_kv as kv
+    _, slots = kv.kv_device_cu_slots(0)
+    s_a, s_b = split_streams(slots // 2)
+    main = torch.cuda.current_stream()
+    for order in ((0, 1), (1, 0)):
+        outs = [torch.empty_like(halves[0][0]), torch.empty_like(halves[1][0])]
+        for s in (s_a, s_b):
+            s.stream.wait_stream(main)
+        for i in order:
+            qa, sa, pa, _ = halves[i]
+            for _ in range(3):
+                pool.decode(0, qa, sa, page_table=pa, out=outs[i], stream=(s_a, s_b)[i].stream)
+        for s in (s_a, s_b):
+            main.wait_stream(s.stream)
+        torch.cuda.synchronize()
+        for i in (0, 1):
+            assert torch.equal(outs[i], halves[i][3])
+    s_a.close()
+    s_b.close()
+    pool.close()

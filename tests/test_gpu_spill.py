@@ -317,6 +317,13 @@ def test_lazy_resume_decodes_in_place_then_promotes(dev, cold):
             tolerance_check(got, case.oracle_out())
 
     check()
+    # spill cannot be turned off while rows name cold pages (decode without
+    # spill would read them as invalid ids); the refused call changes nothing
+    from paper_2609_25782_amd import hotcold_kv as kv
+    with pytest.raises(kv.KVError) as e:
+        pool.set_spill(False)
+    assert e.value.status == kv.KV_ERR_STATE
+    check()
     moved = 0
     while True:
         n = pool.promote(7)
@@ -326,6 +333,8 @@ def test_lazy_resume_decodes_in_place_then_promotes(dev, cold):
         if n == 0:
             break
     assert moved == n_pages and pool.stats()["cold_active_pages"] == 0
+    pool.set_spill(False)                      # nothing spilled any more: accepted
+    check()
     pb = pool.page_bytes
     for sid in range(3):
         _, _, hot, cold_ids = pool.info(sid)

@@ -20,7 +20,7 @@ def _meta_pool(kv, nh, nc, ms, stride):
 
 
 def _snapshot(kv, pool, ms):
-    return [kv.kv_session_info(pool, s) for s in range(ms)], kv.kv_pool_stats_get(pool)
+    return [kv.kv_session_info(pool, s) for s in range(ms)], kv.kv_pool_stats(pool)
 
 
 def _same(kv, pool, model, ms):
@@ -30,7 +30,7 @@ def _same(kv, pool, model, ms):
         assert state == s.state
         if state:
             assert L == s.seq_len and cold == s.cold and hot == s.hot
-    st = kv.kv_pool_stats_get(pool)
+    st = kv.kv_pool_stats(pool)
     assert st["free_hot_pages"] == model.free_hot()
     assert st["free_cold_pages"] == model.free_cold()
     assert st["pages_to_cold"] == model.cold_writes
@@ -176,7 +176,7 @@ def test_metadata_write_drops_cold_copies():
     kv.kv_write_tokens(pool, a, 0, 17, 16, 0, 0)           # pages 1 and 2
     assert kv.kv_session_info(pool, a)[3] == [0, -1, -1]
     kv.kv_evict_session(pool, a)
-    st = kv.kv_pool_stats_get(pool)
+    st = kv.kv_pool_stats(pool)
     assert st["pages_to_cold"] == 5 and kv.kv_session_info(pool, a)[3] == [0, 1, 2]
     kv.kv_pool_destroy(pool)
 
@@ -204,9 +204,9 @@ def test_metadata_append_drops_cold_copies_and_checks_every_row():
     kv.kv_append_tokens(pool, 0, [a, b, a], [39, 0, 31], 0, 0)  # a: page 2 and page 1; b: page 0
     assert kv.kv_session_info(pool, a)[3] == [cold_a[0], -1, -1]
     assert kv.kv_session_info(pool, b)[3] == [-1, cold_b[1]]
-    before = kv.kv_pool_stats_get(pool)["pages_to_cold"]
+    before = kv.kv_pool_stats(pool)["pages_to_cold"]
     kv.kv_evict_sessions(pool, [a, b])
-    assert kv.kv_pool_stats_get(pool)["pages_to_cold"] - before == 3
+    assert kv.kv_pool_stats(pool)["pages_to_cold"] - before == 3
     with pytest.raises(kv.KVError) as e:                       # paused now
         kv.kv_append_tokens(pool, 0, [a], [0], 0, 0)
     assert e.value.status == kv.KV_ERR_STATE
@@ -254,5 +254,36 @@ def test_spill_entry_points_error_codes():
             call()
         assert e.value.status == kv.KV_ERR_INVALID
     kv.kv_resume_sessions_lazy(pool, [a])              # all pages resident: nothing spills
-    assert kv.kv_pool_stats_get(pool)["spilled_pages"] == 0
+    assert kv.kv_pool_stats(pool)["spilled_pages"] == 0
+    kv.kv_pool_destroy(pool)
+
+
+def test_spill_off_refused_while_rows_name_spilled_pages():
+    """Turning spill off while a row still names cold pages would leave decode's
+    plain kernel reading tagged entries as invalid ids: the call is refused with
+    KV_ERR_STATE and nothing changes; after the pages are promoted (or the
+    session evicted) it succeeds."""
+    kv = _lib()
+    pool = _meta_pool(kv, 4, 16, 3, 8)
+    kv.kv_pool_set_spill(pool, True)
+    a = kv.kv_session_create(pool, 6 * 16)          # 4 hot pages, 2 spilled
+    assert kv.kv_pool_stats(pool)["cold_active_pages"] == 2
+    before = _snapshot(kv, pool, 3)
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_pool_set_spill(pool, False)
+    assert e.value.status == kv.KV_ERR_STATE
+    assert _snapshot(kv, pool, 3) == before
+    # a paused session whose row still names its spilled pages blocks it too
+    kv.kv_session_pause(pool, a)
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_pool_set_spill(pool, False)
+    assert e.value.status == kv.KV_ERR_STATE
+    kv.kv_session_destroy(pool, a)
+    kv.kv_pool_set_spill(pool, False)               # nothing spilled: accepted
+    kv.kv_pool_set_spill(pool, True)
+    b = kv.kv_session_create(pool, 6 * 16)
+    with pytest.raises(kv.KVError):
+        kv.kv_pool_set_spill(pool, False)
+    kv.kv_evict_session(pool, b)                     # evicted: the row is cleared
+    kv.kv_pool_set_spill(pool, False)
     kv.kv_pool_destroy(pool)
