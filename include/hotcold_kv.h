@@ -589,6 +589,29 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
                            size_t ws_bytes, kv_stream_t stream);
 
 /*
+ * paged_decode_attention without a workspace argument and without allocating:
+ * for callers that cannot call the allocator (code under HIP graph capture,
+ * serving loops and harnesses that forbid allocation).  The split partials and
+ * the row page prefix live in a device array of KV_DECODE_SCRATCH_BYTES that
+ * the library holds on each GPU it runs on until the process ends (its address
+ * is taken when a pool is created on that GPU).  Arguments, numerics and
+ * results are those of paged_decode_attention with the same pool settings (the
+ * same kernels and work split, so the outputs are bitwise equal).  Nothing in
+ * the array needs to start at zero, and it keeps the last call's contents.
+ * Every call on one GPU shares that array: calls that overlap in time on one
+ * GPU (two streams, two pools, two threads) race and corrupt each other's
+ * results; order them.  The call takes no profiling events.
+ * Errors: as paged_decode_attention; KV_ERR_INVALID when the batch needs more
+ * scratch than KV_DECODE_SCRATCH_BYTES (paged_decode_workspace_bytes gives the
+ * need; about 4.2 KB per (row, KV head) plus 3.2 MB at 32 query / 4 KV heads,
+ * d = 128, so batches up to about 1,800 rows fit).
+ */
+#define KV_DECODE_SCRATCH_BYTES (32u << 20)
+int paged_decode_attention_noalloc(kv_pool* pool, int32_t layer, const void* q, const int32_t* page_table,
+                                   int64_t pt_stride, const int32_t* seq_lens, int32_t batch,
+                                   int32_t num_q_heads, float scale, void* out, kv_stream_t stream);
+
+/*
  * The work split of paged_decode_attention, written out (device int32
  * [waves + batch * num_kv_heads][4]).  Waves form workers of L waves: L = 4
  * when num_kv_heads and `waves` are multiples of 4, else 1.  A unit is one

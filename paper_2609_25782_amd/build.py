@@ -21,7 +21,7 @@ EXTRA = os.environ.get("HCK_EXTRA_FLAGS", "").split()
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["decode_attention.hip", "page_ops.hip", "kv_pool.cpp"]
+SOURCES = ["decode_attention.hip", "page_ops.hip", "noalloc.hip", "kv_pool.cpp"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", os.path.join(ROOT, "include"), "-I", CSRC] + EXTRA
 DEVICE = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 

@@ -100,6 +100,13 @@ int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page
                 const int32_t* seq_lens, int32_t batch, int32_t num_q_heads, float scale, void* out,
                 void* workspace, size_t ws_bytes, kv_stream_t stream, bool no_alloc);
 
+// Device address of the no-allocation decode's scratch array on `device`
+// (the current device); taken once per device and kept (noalloc.hip).
+hipError_t scratch_address(int device, void** out);
+// That address for a pool's device, taken when the pool was created
+// (host runtime); KV_ERR_INVALID for a NULL or metadata-only pool.
+int pool_scratch(kv_pool* pool, void** out);
+
 hipError_t launch_decode_split(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s,
                                const LaunchEvents& ev = {});
 hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, hipStream_t s,

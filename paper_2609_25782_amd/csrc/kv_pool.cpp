@@ -209,6 +209,7 @@ struct kv_pool {
     int32_t host_copy = KV_HOST_COPY_DMA;
     int32_t compute_mode = KV_DECODE_MATRIX;
     int32_t* counters = nullptr;  // decode arrival counters, zero between calls
+    void* scratch = nullptr;      // the no-allocation decode's device array on this pool's device
     hipEvent_t decode_event = nullptr;
     bool decode_pending = false;
     std::vector<ProfRec> prof[KV_KERNEL_COUNT];
@@ -704,6 +705,11 @@ int kv_pool_create(const kv_pool_desc* desc, void* hot_base, size_t hot_bytes, v
         if (hipEventCreateWithFlags(&p->decode_event, hipEventDisableTiming) != hipSuccess) {
             delete p;
             return fail(KV_ERR_OOM, "event creation failed");
+        }
+        e = hck::scratch_address(desc->device, &p->scratch);
+        if (e != hipSuccess) {
+            delete p;
+            return hip_fail(e, "hipGetSymbolAddress(decode scratch)");
         }
         const int64_t ncnt = static_cast<int64_t>(kMaxDecodeBatch) * 16;
         if (hipMalloc(&p->counters, ncnt * sizeof(int32_t)) != hipSuccess) {
@@ -1453,7 +1459,12 @@ int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page
     const int32_t waves = pool->decode_waves();
     const int64_t slots = static_cast<int64_t>(waves) + static_cast<int64_t>(batch) * pool->d.num_kv_heads;
     const size_t need = hck::decode_workspace_bytes(slots, group, pool->d.head_dim, batch);
-    if (ws_bytes < need) return fail(KV_ERR_INVALID, "workspace %zu bytes, need %zu", ws_bytes, need);
+    if (ws_bytes < need) {
+        if (no_alloc)
+            return fail(KV_ERR_INVALID, "this batch needs %zu bytes of decode scratch; the no-allocation "
+                                        "entry point has %zu (use paged_decode_attention)", need, ws_bytes);
+        return fail(KV_ERR_INVALID, "workspace %zu bytes, need %zu", ws_bytes, need);
+    }
     hck::DecodeArgs a;
     a.hot = pool->hot;
     a.page_bytes = pool->page_bytes;
@@ -1534,6 +1545,14 @@ int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page
         if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
         pool->half_free_pending[half] = true;
     }
+    return KV_OK;
+}
+
+int pool_scratch(kv_pool* pool, void** out) {
+    *out = nullptr;
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    if (pool->meta || !pool->scratch) return fail(KV_ERR_INVALID, "metadata-only pool cannot decode");
+    *out = pool->scratch;
     return KV_OK;
 }
 

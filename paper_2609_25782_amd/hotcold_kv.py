@@ -108,6 +108,8 @@ _SIGS = {
     "paged_decode_workspace_bytes": (_SZ, [_P, _I32, _I32]),
     "paged_decode_attention": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _I32, _I32,
                                               ctypes.c_float, _P, _P, _SZ, _P]),
+    "paged_decode_attention_noalloc": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _I32, _I32,
+                                                      ctypes.c_float, _P, _P]),
     "paged_decode_partition": (ctypes.c_int, [_P, _P, _I32, _I32, _P, _P]),
     "paged_decode_gather_table": (ctypes.c_int, [_P, _P, _I32, _P, _P]),
     "kv_strerror": (ctypes.c_char_p, [ctypes.c_int]),
@@ -355,6 +357,18 @@ def paged_decode_attention(pool: int, layer: int, q_ptr: int, page_table_ptr: in
                                        seq_lens_ptr or None, batch, num_q_heads, scale,
                                        out_ptr or None, workspace_ptr or None, ws_bytes,
                                        stream or None), "paged_decode_attention")
+
+
+KV_DECODE_SCRATCH_BYTES = 32 << 20
+
+
+def paged_decode_attention_noalloc(pool: int, layer: int, q_ptr: int, page_table_ptr: int, pt_stride: int,
+                                   seq_lens_ptr: int, batch: int, num_q_heads: int, scale: float,
+                                   out_ptr: int, stream: int = 0) -> None:
+    _check(_lib.paged_decode_attention_noalloc(pool, layer, q_ptr or None, page_table_ptr or None, pt_stride,
+                                               seq_lens_ptr or None, batch, num_q_heads, scale,
+                                               out_ptr or None, stream or None),
+           "paged_decode_attention_noalloc")
 
 
 def paged_decode_gather_table(pool: int, sids_ptr: int, n: int, table_ptr: int, stream: int = 0) -> None:
