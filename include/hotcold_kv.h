@@ -212,8 +212,12 @@ int kv_session_create(kv_pool* pool, int32_t seq_len, const int32_t* hot_pages,
  * Grow an ACTIVE session to new_seq_len tokens: decoding appends each new
  * token's KV (Sec. II; fresh KV goes to the fast tier, data path 3).  Pages for
  * the new tokens are allocated like kv_session_create's and appended to the
- * row; write the tokens' K and V with kv_write_tokens.
- * Errors: KV_ERR_INVALID (shrinking, row stride), KV_ERR_STATE, KV_ERR_NO_HOT_PAGES,
+ * row; write the tokens' K and V with kv_write_tokens, kv_append_tokens or
+ * kv_append_tokens_table.  The new tokens go into the partially filled tail
+ * page first, so extending counts as writing that page: its cold copy is
+ * dropped (the next eviction writes it again, Sec. III write-on-evict).
+ * Errors: KV_ERR_INVALID (shrinking, row stride), KV_ERR_STATE (not ACTIVE, or
+ * a spilled tail page shared with another session), KV_ERR_NO_HOT_PAGES,
  * KV_ERR_NO_COLD_PAGES.
  */
 int kv_session_extend(kv_pool* pool, int32_t sid, int32_t new_seq_len, kv_stream_t stream);
@@ -321,6 +325,18 @@ int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin
                     const void* k, const void* v, kv_stream_t stream);
 
 /*
+ * kv_write_tokens for layers [layer_begin, layer_begin + num_layers) in one
+ * launch: k and v are device arrays [num_layers][n_tok][num_kv_heads][head_dim]
+ * (16-byte aligned).  For writing a whole prompt's KV at once (a turn's tool
+ * output or user text prefilled elsewhere), where one launch per layer would
+ * spend more time launching than moving bytes.
+ * Errors: KV_ERR_INVALID (layer range, token range, alignment), KV_ERR_STATE.
+ */
+int kv_write_tokens_layers(kv_pool* pool, int32_t sid, int32_t layer_begin, int32_t num_layers,
+                           int32_t tok_begin, int32_t n_tok, const void* k, const void* v,
+                           kv_stream_t stream);
+
+/*
  * Batched append for a decode step (data path 3, Sec. III): for one layer, row
  * i of k and v (device arrays [n][num_kv_heads][head_dim], pool dtype) is
  * token positions[i] of ACTIVE session sids[i] (host arrays, n <= 8192).  One
@@ -335,6 +351,35 @@ int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin
  */
 int kv_append_tokens(kv_pool* pool, int32_t layer, const int32_t* sids, const int32_t* positions, int32_t n,
                      const void* k, const void* v, kv_stream_t stream);
+
+/*
+ * A decode step's append resolved on the device (data path 3, Sec. III), so
+ * that a whole serving step (append and decode for every layer) can be
+ * captured into one HIP graph and replayed: no host bookkeeping, no copy list,
+ * one kernel launch.  Entry i writes token positions[i] of row rows[i] of
+ * `table` (device int32 [table_rows][pt_stride], e.g. a batch table from
+ * paged_decode_gather_table, or the pool's own table) for layers
+ * [layer_begin, layer_begin + num_layers): the page is the one that row's
+ * entry positions[i] / 16 names (a hot page, or KV_PAGE_COLD | id: a spilled
+ * page written in place) and the slot is positions[i] % 16.  rows and
+ * positions are device int32 [n] (n <= 8192) read when the kernel runs, so a
+ * graph replay takes their current values; k and v are device arrays
+ * [num_layers][n][num_kv_heads][head_dim] of the pool's dtype, 16-byte aligned.
+ * An entry whose row or position lies outside the table, or whose table entry
+ * names no page of either pool (-1, a staged slot, an id out of range), writes
+ * nothing.  Two entries naming the same token race.
+ * The pool's bookkeeping is not read or changed.  Write-on-evict stays exact
+ * for tokens that extend a session (positions at or past its length before its
+ * last kv_session_extend): the extension already dropped the cold copy of the
+ * page the new tokens go into.  Rewriting older tokens this way would leave
+ * that page's cold copy stale; use kv_write_tokens for those.
+ * Errors: KV_ERR_INVALID (layer range, n, NULL or misaligned buffers, table
+ * shape, metadata-only pool), KV_ERR_HIP.
+ */
+int kv_append_tokens_table(kv_pool* pool, int32_t layer_begin, int32_t num_layers, const int32_t* table,
+                           int64_t pt_stride, int32_t table_rows, const int32_t* rows,
+                           const int32_t* positions, int32_t n, const void* k, const void* v,
+                           kv_stream_t stream);
 
 /*
  * Test and benchmark input: fill every slot of an ACTIVE session's pages, all

@@ -72,6 +72,9 @@ def load_library(path: str):
         ctypes.c_long, ctypes.c_int]
     lib.oracle_page_bytes.restype = ctypes.c_long
     lib.oracle_page_bytes.argtypes = [ctypes.POINTER(_Layout)]
+    lib.oracle_pack_session.restype = ctypes.c_int
+    lib.oracle_pack_session.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Layout), ctypes.c_int,
+                                        ctypes.c_void_p, ctypes.c_long, ctypes.c_void_p, ctypes.c_void_p]
     lib.oracle_elem_offset.restype = ctypes.c_long
     lib.oracle_elem_offset.argtypes = [ctypes.POINTER(_Layout), ctypes.c_long, ctypes.c_int,
                                        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]
@@ -129,6 +132,26 @@ def pack_pool(pool: np.ndarray, num_layers: int, num_kv_heads: int, head_dim: in
     typed = pool.view(store)
     typed[(k_off // e).ravel()] = np.asarray(k, dtype=store).ravel()
     typed[(v_off // e).ravel()] = np.asarray(v, dtype=store).ravel()
+
+
+def pack_session(pool: np.ndarray, num_layers: int, num_kv_heads: int, head_dim: int, dtype: int,
+                 layer: int, pages: np.ndarray, k: np.ndarray, v: np.ndarray) -> None:
+    """``pack_pool`` done by the C oracle's packer (same arguments, same bytes;
+    for the full-size workloads, where the numpy scatter takes minutes)."""
+    store = np.uint16 if dtype == BF16 else np.float32
+    k = np.ascontiguousarray(k, dtype=store)
+    v = np.ascontiguousarray(v, dtype=store)
+    pages = np.ascontiguousarray(pages, dtype=np.int32)
+    L = int(k.shape[0])
+    assert k.shape == v.shape == (L, num_kv_heads, head_dim) and pages.shape[0] * PAGE_SIZE >= L
+    pb = page_bytes(num_layers, num_kv_heads, head_dim, dtype)
+    assert pool.dtype == np.uint8 and pool.flags.c_contiguous
+    assert L == 0 or (int(pages[:(L + PAGE_SIZE - 1) // PAGE_SIZE].max()) + 1) * pb <= pool.size
+    lay = _layout(num_layers, num_kv_heads, head_dim, dtype)
+    rc = _load().oracle_pack_session(pool.ctypes.data, ctypes.byref(lay), int(layer), pages.ctypes.data, L,
+                                     k.ctypes.data, v.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_pack_session failed with status %d" % rc)
 
 
 def paged_attention(pool: np.ndarray, num_pages: int, num_layers: int, num_kv_heads: int,

@@ -149,3 +149,29 @@ int oracle_paged_attention(const void* pool, long num_pages, const oracle_layout
     }
     return status;
 }
+
+/*
+ * Write one session's logical K and V of one layer ([seq_len][num_kv_heads]
+ * [head_dim], elements of the pool's dtype) into a host pool: token t goes to
+ * page pages[t / P], slot t % P, at the offsets oracle_elem_offset gives.  The
+ * same job as the numpy packer (oracle.pack_pool), for sizes numpy is slow on.
+ */
+int oracle_pack_session(void* pool, const oracle_layout* L, int layer, const int32_t* pages, long seq_len,
+                        const void* k, const void* v) {
+    if (!pool || !L || (seq_len > 0 && (!pages || !k || !v))) return -1;
+    const int e = elt_bytes(L->dtype), H = L->num_kv_heads, D = L->head_dim, P = L->page_size;
+    uint8_t* base = (uint8_t*)pool;
+    const uint8_t* kb = (const uint8_t*)k;
+    const uint8_t* vb = (const uint8_t*)v;
+#pragma omp parallel for schedule(static)
+    for (long t = 0; t < seq_len; ++t) {
+        const long page = pages[t / P];
+        for (int g = 0; g < H; ++g)
+            for (int d = 0; d < D; ++d) {
+                const long src = ((t * H + g) * (long)D + d) * e;
+                memcpy(base + oracle_elem_offset(L, page, layer, g, 0, (int)(t % P), d), kb + src, (size_t)e);
+                memcpy(base + oracle_elem_offset(L, page, layer, g, 1, (int)(t % P), d), vb + src, (size_t)e);
+            }
+    }
+    return 0;
+}

@@ -29,7 +29,11 @@ Readings where the paper is silent:
   (no spilling of active pages); a call that would have to evict pages of the
   sessions it resumes fails instead.
 * Writing tokens into a page that has a cold copy invalidates that copy, so the
-  next eviction writes the page again.
+  next eviction writes the page again.  Extending a session counts as writing
+  its partially filled tail page, which the new tokens go into: the extension
+  drops that page's cold copy (and, for a spilled tail page shared with another
+  session, is refused), so appends whose page is resolved on the device need no
+  bookkeeping of their own.
 * Cold pages may be shared by several paused sessions (a virtualised cold
   pool); they are reference counted and freed when the last user lets go.
 * Every failing call leaves the whole state unchanged.
@@ -226,11 +230,17 @@ class PoolModel:
             raise ModelError(ERR_STATE, "not active")
         if new_len < s.seq_len or _pages(new_len) > self.stride:
             raise ModelError(ERR_INVALID, "bad length")
+        tail = s.seq_len // PAGE_TOKENS if new_len > s.seq_len and s.seq_len % PAGE_TOKENS else -1
+        if tail >= 0 and s.hot[tail] < 0 and self.cold_ref[s.cold[tail]] > 1:
+            raise ModelError(ERR_STATE, "tail page spilled to a cold page shared with another session")
         add = _pages(new_len) - len(s.hot)
         victims, cold, pages, spill = self._plan(add)
         self.last_victim_copies = self._evict_victims(victims, cold)
         self._take_hot(pages)
         self._take_cold(spill)
+        if tail >= 0 and s.hot[tail] >= 0 and s.cold[tail] >= 0:   # the new tokens modify it
+            self._release_cold(s.cold[tail])
+            s.cold[tail] = -1
         s.hot += list(pages) + [-1] * len(spill)
         s.cold += [-1] * len(pages) + list(spill)
         s.spilled += [False] * len(pages) + [True] * len(spill)

@@ -176,8 +176,9 @@ struct WriteArgs {
     int64_t page_bytes;
     const int32_t* row;  // device page-table row of the session
     int32_t num_kv_heads, head_dim, dtype, layer;
+    int32_t num_layers = 1;  // layers [layer, layer + num_layers)
     int32_t tok_begin, n_tok;
-    const void* k;       // [n_tok][num_kv_heads][head_dim]
+    const void* k;       // [num_layers][n_tok][num_kv_heads][head_dim]
     const void* v;
 };
 hipError_t launch_write_tokens(const WriteArgs& a, hipStream_t s);
@@ -205,5 +206,24 @@ struct AppendArgs {
     AppendEntry inline_entries[kAppendInline];  // the entries when n <= kAppendInline
 };
 hipError_t launch_append_tokens(const AppendArgs& a, hipStream_t s);
+
+// Appends resolved on the device through a page table: entry r is token
+// positions[r] of table row rows[r], for layers [layer, layer + num_layers).
+struct AppendTableArgs {
+    char* hot;
+    char* cold;
+    int64_t page_bytes;
+    int32_t num_hot, num_cold;   // valid page ids of each pool
+    const int32_t* table;        // device [table_rows][pt_stride]
+    int64_t pt_stride;
+    int32_t table_rows;
+    const int32_t* rows;         // device [n]
+    const int32_t* positions;    // device [n]
+    int32_t n;
+    int32_t num_kv_heads, head_dim, dtype, layer, num_layers;
+    const void* k;               // [num_layers][n][num_kv_heads][head_dim]
+    const void* v;
+};
+hipError_t launch_append_table(const AppendTableArgs& a, hipStream_t s);
 
 }  // namespace hck

@@ -818,6 +818,13 @@ int kv_session_extend(kv_pool* pool, int32_t sid, int32_t new_seq_len, kv_stream
     if (n_new > pool->d.max_pages_per_session)
         return fail(KV_ERR_INVALID, "%d pages exceed the row stride %d", n_new,
                     pool->d.max_pages_per_session);
+    // The new tokens go into the partially filled tail page, if any: extending
+    // counts as writing it (so appends resolved on the device need no
+    // bookkeeping), and a spilled tail page shared with another session cannot
+    // be written.
+    const int32_t tail = (new_seq_len > s->seq_len && s->seq_len % KV_PAGE_TOKENS) ? s->seq_len / KV_PAGE_TOKENS : -1;
+    if (tail >= 0 && s->hot[tail] < 0 && pool->cold_ref[s->cold[tail]] > 1)
+        return fail(KV_ERR_STATE, "tail page %d is spilled to a cold page shared with another session", tail);
     Alloc a;
     int rc = pool->plan_alloc(std::max(n_new - n_old, 0), {}, a);
     if (rc) return rc;
@@ -833,6 +840,10 @@ int kv_session_extend(kv_pool* pool, int32_t sid, int32_t new_seq_len, kv_stream
     pool->commit_victims(a);
     pool->commit_spill(a);
     for (int32_t p : a.pages) pool->hot_free.take(p);
+    if (tail >= 0 && s->hot[tail] >= 0 && s->cold[tail] >= 0) {  // its cold copy goes stale
+        pool->release_cold(s->cold[tail]);
+        s->cold[tail] = -1;
+    }
     s->hot.insert(s->hot.end(), a.pages.begin(), a.pages.end());
     s->hot.resize(n_new, -1);
     s->cold.resize(n_old + a.pages.size(), -1);
@@ -1013,13 +1024,15 @@ int kv_append_tokens(kv_pool* pool, int32_t layer, const int32_t* sids, const in
     return KV_OK;
 }
 
-int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin, int32_t n_tok,
-                    const void* k, const void* v, kv_stream_t stream) {
+int kv_write_tokens_layers(kv_pool* pool, int32_t sid, int32_t layer_begin, int32_t num_layers,
+                           int32_t tok_begin, int32_t n_tok, const void* k, const void* v, kv_stream_t stream) {
     if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
     Session* s = pool->session(sid);
     if (!s) return fail(KV_ERR_INVALID, "bad session id %d", sid);
     if (s->state != KV_SESSION_ACTIVE) return fail(KV_ERR_STATE, "session %d is not active", sid);
-    if (layer < 0 || layer >= pool->d.num_layers) return fail(KV_ERR_INVALID, "bad layer %d", layer);
+    if (layer_begin < 0 || num_layers < 1 || layer_begin + static_cast<int64_t>(num_layers) > pool->d.num_layers)
+        return fail(KV_ERR_INVALID, "layers [%d, %d) outside the pool's %d", layer_begin, layer_begin + num_layers,
+                    pool->d.num_layers);
     if (tok_begin < 0 || n_tok < 0 || static_cast<int64_t>(tok_begin) + n_tok > s->seq_len)
         return fail(KV_ERR_INVALID, "token range outside the session");
     if (n_tok == 0) return KV_OK;
@@ -1029,6 +1042,8 @@ int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin
             return fail(KV_ERR_STATE, "page %d is spilled to a cold page shared with another session", i);
     if (!pool->meta) {
         if (!k || !v) return fail(KV_ERR_INVALID, "NULL k or v");
+        if ((reinterpret_cast<uintptr_t>(k) | reinterpret_cast<uintptr_t>(v)) & 15)
+            return fail(KV_ERR_INVALID, "k and v must be 16-byte aligned");
         DeviceGuard g(pool->d.device);
         hck::WriteArgs a;
         a.hot = pool->hot;
@@ -1038,7 +1053,8 @@ int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin
         a.num_kv_heads = pool->d.num_kv_heads;
         a.head_dim = pool->d.head_dim;
         a.dtype = pool->d.dtype;
-        a.layer = layer;
+        a.layer = layer_begin;
+        a.num_layers = num_layers;
         a.tok_begin = tok_begin;
         a.n_tok = n_tok;
         a.k = k;
@@ -1052,6 +1068,52 @@ int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin
             s->cold[i] = -1;
         }
     }
+    return KV_OK;
+}
+
+int kv_write_tokens(kv_pool* pool, int32_t sid, int32_t layer, int32_t tok_begin, int32_t n_tok,
+                    const void* k, const void* v, kv_stream_t stream) {
+    if (pool && (layer < 0 || layer >= pool->d.num_layers)) return fail(KV_ERR_INVALID, "bad layer %d", layer);
+    return kv_write_tokens_layers(pool, sid, layer, 1, tok_begin, n_tok, k, v, stream);
+}
+
+int kv_append_tokens_table(kv_pool* pool, int32_t layer_begin, int32_t num_layers, const int32_t* table,
+                           int64_t pt_stride, int32_t table_rows, const int32_t* rows, const int32_t* positions,
+                           int32_t n, const void* k, const void* v, kv_stream_t stream) {
+    if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
+    if (pool->meta) return fail(KV_ERR_INVALID, "metadata-only pool has no pages");
+    if (layer_begin < 0 || num_layers < 1 || layer_begin + static_cast<int64_t>(num_layers) > pool->d.num_layers)
+        return fail(KV_ERR_INVALID, "layers [%d, %d) outside the pool's %d", layer_begin, layer_begin + num_layers,
+                    pool->d.num_layers);
+    if (n < 0 || n > kMaxDecodeBatch) return fail(KV_ERR_INVALID, "n %d outside [0, %d]", n, kMaxDecodeBatch);
+    if (n == 0) return KV_OK;
+    if (!table || !rows || !positions || !k || !v) return fail(KV_ERR_INVALID, "NULL buffer");
+    if (pt_stride < 1 || table_rows < 0 || static_cast<int64_t>(table_rows) * pt_stride >= (int64_t(1) << 31))
+        return fail(KV_ERR_INVALID, "bad page-table shape");
+    if ((reinterpret_cast<uintptr_t>(k) | reinterpret_cast<uintptr_t>(v)) & 15)
+        return fail(KV_ERR_INVALID, "k and v must be 16-byte aligned");
+    DeviceGuard g(pool->d.device);
+    hck::AppendTableArgs a;
+    a.hot = pool->hot;
+    a.cold = pool->cold;
+    a.page_bytes = pool->page_bytes;
+    a.num_hot = pool->d.num_hot_pages;
+    a.num_cold = pool->cold ? pool->d.num_cold_pages : 0;
+    a.table = table;
+    a.pt_stride = pt_stride;
+    a.table_rows = table_rows;
+    a.rows = rows;
+    a.positions = positions;
+    a.n = n;
+    a.num_kv_heads = pool->d.num_kv_heads;
+    a.head_dim = pool->d.head_dim;
+    a.dtype = pool->d.dtype;
+    a.layer = layer_begin;
+    a.num_layers = num_layers;
+    a.k = k;
+    a.v = v;
+    hipError_t e = hck::launch_append_table(a, pool->strm(stream));
+    if (e != hipSuccess) return hip_fail(e, "append_table launch");
     return KV_OK;
 }
 

@@ -247,14 +247,14 @@ __device__ __forceinline__ void write_token_group(char* lh, int64_t tile, int sl
     }
 }
 
-// Tokens [tok_begin, tok_begin + n_tok) of one layer: one block per (page,
-// KV head).  The page's tokens in the range are read from the source rows
-// ([token][kv_head][head_dim], each token's dims contiguous) into LDS with
-// 16-byte loads, then written out in the tile layouts with 16-byte stores: K
-// as groups of x dims, consecutive threads on consecutive tokens; V transposed
-// to dims-major rows of 16 tokens.  Slots of the page outside the range keep
-// their bytes: a V store that would cover one of them is done element by
-// element instead.
+// Tokens [tok_begin, tok_begin + n_tok) of layers [layer, layer + num_layers):
+// one block per (page, KV head, layer).  The page's tokens in the range are
+// read from the source rows ([layer][token][kv_head][head_dim], each token's
+// dims contiguous) into LDS with 16-byte loads, then written out in the tile
+// layouts with 16-byte stores: K as groups of x dims, consecutive threads on
+// consecutive tokens; V transposed to dims-major rows of 16 tokens.  Slots of
+// the page outside the range keep their bytes: a V store that would cover one
+// of them is done element by element instead.
 template <typename T>
 __global__ __launch_bounds__(kBlockThreads) void write_tokens_kernel(WriteArgs a) {
     constexpr int x = 16 / sizeof(T);            // elements per 16 bytes
@@ -267,6 +267,8 @@ __global__ __launch_bounds__(kBlockThreads) void write_tokens_kernel(WriteArgs a
     const int p0 = a.tok_begin / kPageTokens;
     const int page = p0 + static_cast<int>(blockIdx.x);
     const int head = static_cast<int>(blockIdx.y);
+    const int layer = a.layer + static_cast<int>(blockIdx.z);
+    const int64_t layer_src = static_cast<int64_t>(blockIdx.z) * a.n_tok * a.num_kv_heads * D;
     const int t_base = page * kPageTokens;
     const int s0 = max(a.tok_begin, t_base) - t_base;                       // first slot written
     const int s1 = min(a.tok_begin + a.n_tok, t_base + kPageTokens) - t_base;  // one past the last
@@ -274,13 +276,14 @@ __global__ __launch_bounds__(kBlockThreads) void write_tokens_kernel(WriteArgs a
     for (int e = tid; e < kPageTokens * groups; e += kBlockThreads) {
         const int t = e / groups, cd = e % groups;
         if (t < s0 || t >= s1) continue;
-        const int64_t src = (static_cast<int64_t>(t_base + t - a.tok_begin) * a.num_kv_heads + head) * D + cd * x;
+        const int64_t src =
+            layer_src + (static_cast<int64_t>(t_base + t - a.tok_begin) * a.num_kv_heads + head) * D + cd * x;
         *reinterpret_cast<u32x4*>(&s_k[t][cd * x]) = *reinterpret_cast<const u32x4*>(static_cast<const T*>(a.k) + src);
         *reinterpret_cast<u32x4*>(&s_v[t][cd * x]) = *reinterpret_cast<const u32x4*>(static_cast<const T*>(a.v) + src);
     }
     __syncthreads();
     char* lh = page_address(a.hot, a.cold, a.row[page], a.page_bytes) +
-               (static_cast<int64_t>(a.layer) * a.num_kv_heads + head) * 2 * tile;
+               (static_cast<int64_t>(layer) * a.num_kv_heads + head) * 2 * tile;
     // K tile: [group][token][x]
     for (int e = tid; e < groups * kPageTokens; e += kBlockThreads) {
         const int cd = e / kPageTokens, t = e % kPageTokens;
@@ -326,6 +329,42 @@ __global__ __launch_bounds__(kBlockThreads) void append_tokens_kernel(const Appe
                    (static_cast<int64_t>(a.layer) * a.num_kv_heads + head) * 2 * tile;
         const int64_t src = ((static_cast<int64_t>(r) * a.num_kv_heads + head) * a.head_dim + cd * x) * elt;
         write_token_group(lh, tile, e.slot, cd, x, elt, static_cast<const char*>(a.k) + src,
+                          static_cast<const char*>(a.v) + src);
+    }
+}
+
+// Appends whose page is resolved on the device: entry r writes token
+// positions[r] of batch row rows[r] for layers [layer, layer + num_layers),
+// into the page that row's page-table entry names (a hot page, or a spilled
+// page of the cold pool), at slot positions[r] % 16.  One thread per (layer,
+// entry, KV head, 16-byte group of dims).  An entry whose row, position or
+// page-table entry does not name a page of either pool writes nothing.
+__global__ __launch_bounds__(kBlockThreads) void append_table_kernel(const AppendTableArgs a) {
+    const int elt = a.dtype == kDtypeBf16 ? 2 : 4;
+    const int x = 16 / elt;
+    const int groups = a.head_dim / x;
+    const int64_t tile = static_cast<int64_t>(kPageTokens) * a.head_dim * elt;
+    const int64_t per_layer = static_cast<int64_t>(a.n) * a.num_kv_heads * groups;
+    const int64_t total = per_layer * a.num_layers;
+    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; gi < total;
+         gi += static_cast<int64_t>(gridDim.x) * kBlockThreads) {
+        const int li = static_cast<int>(gi / per_layer);
+        const int64_t wi = gi % per_layer;
+        const int cd = static_cast<int>(wi % groups);
+        const int head = static_cast<int>((wi / groups) % a.num_kv_heads);
+        const int r = static_cast<int>(wi / (static_cast<int64_t>(groups) * a.num_kv_heads));
+        const int32_t row = a.rows[r], pos = a.positions[r];
+        if (row < 0 || row >= a.table_rows || pos < 0 || pos / kPageTokens >= a.pt_stride) continue;
+        const int32_t pid = a.table[static_cast<int64_t>(row) * a.pt_stride + pos / kPageTokens];
+        const unsigned id = static_cast<unsigned>(pid) & static_cast<unsigned>(kPageIdMask);
+        const unsigned tag = static_cast<unsigned>(pid) >> 29;   // 0 hot, 2 cold; others name no page
+        if (!((tag == 0 && id < static_cast<unsigned>(a.num_hot)) ||
+              (tag == 2 && id < static_cast<unsigned>(a.num_cold))))
+            continue;
+        char* lh = page_address(a.hot, a.cold, pid, a.page_bytes) +
+                   (static_cast<int64_t>(a.layer + li) * a.num_kv_heads + head) * 2 * tile;
+        const int64_t src = (((static_cast<int64_t>(li) * a.n + r) * a.num_kv_heads + head) * a.head_dim + cd * x) * elt;
+        write_token_group(lh, tile, pos % kPageTokens, cd, x, elt, static_cast<const char*>(a.k) + src,
                           static_cast<const char*>(a.v) + src);
     }
 }
@@ -452,8 +491,10 @@ hipError_t launch_fill_synthetic(const SynthArgs& a, hipStream_t s) {
 hipError_t launch_write_tokens(const WriteArgs& a, hipStream_t s) {
     if (a.n_tok <= 0) return hipSuccess;
     if (a.head_dim > 128 || a.head_dim % 16) return hipErrorInvalidValue;
+    if (a.num_layers < 1 || a.num_layers > 65535) return hipErrorInvalidValue;
     const int pages = (a.tok_begin + a.n_tok - 1) / kPageTokens - a.tok_begin / kPageTokens + 1;
-    const dim3 grid(static_cast<unsigned>(pages), static_cast<unsigned>(a.num_kv_heads));
+    const dim3 grid(static_cast<unsigned>(pages), static_cast<unsigned>(a.num_kv_heads),
+                    static_cast<unsigned>(a.num_layers));
     if (a.dtype == kDtypeBf16)
         hipLaunchKernelGGL(write_tokens_kernel<unsigned short>, grid, dim3(kBlockThreads), 0, s, a);
     else
@@ -466,6 +507,14 @@ hipError_t launch_append_tokens(const AppendArgs& a, hipStream_t s) {
     const int64_t work = static_cast<int64_t>(a.n) * a.num_kv_heads * (a.head_dim / x);
     if (work <= 0) return hipSuccess;
     hipLaunchKernelGGL(append_tokens_kernel, dim3(grid_for(work, 16384)), dim3(kBlockThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_append_table(const AppendTableArgs& a, hipStream_t s) {
+    const int x = a.dtype == kDtypeBf16 ? 8 : 4;
+    const int64_t work = static_cast<int64_t>(a.n) * a.num_kv_heads * (a.head_dim / x) * a.num_layers;
+    if (work <= 0) return hipSuccess;
+    hipLaunchKernelGGL(append_table_kernel, dim3(grid_for(work, 16384)), dim3(kBlockThreads), 0, s, a);
     return hipGetLastError();
 }
 

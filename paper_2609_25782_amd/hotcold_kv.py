@@ -83,6 +83,8 @@ _SIGS = {
     "kv_session_info": (ctypes.c_int, [_P, _I32, _PI32, _PI32, _PI32, _PI32, _I32]),
     "kv_write_tokens": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P]),
     "kv_append_tokens": (ctypes.c_int, [_P, _I32, _P, _P, _I32, _P, _P, _P]),
+    "kv_write_tokens_layers": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _I32, _P, _P, _P]),
+    "kv_append_tokens_table": (ctypes.c_int, [_P, _I32, _I32, _P, _I64, _I32, _P, _P, _I32, _P, _P, _P]),
     "kv_fill_synthetic": (ctypes.c_int, [_P, _I32, _I32, _U64, ctypes.c_float, _P]),
     "kv_fill_synthetic_pages": (ctypes.c_int, [_P, _I32, _I32, _U64, ctypes.c_float, _I32, _I32, _P]),
     "kv_evict_session": (ctypes.c_int, [_P, _I32, _P]),
@@ -232,6 +234,20 @@ def kv_append_tokens(pool: int, layer: int, sids, positions, k: int, v: int, str
     pa = (ctypes.c_int32 * max(n, 1))(*positions)
     _check(_lib.kv_append_tokens(pool, layer, sa, pa, n, k or None, v or None, stream or None),
            "kv_append_tokens")
+
+
+def kv_write_tokens_layers(pool: int, sid: int, layer_begin: int, num_layers: int, tok_begin: int, n_tok: int,
+                           k_ptr: int, v_ptr: int, stream: int = 0) -> None:
+    _check(_lib.kv_write_tokens_layers(pool, sid, layer_begin, num_layers, tok_begin, n_tok, k_ptr or None,
+                                       v_ptr or None, stream or None), "kv_write_tokens_layers")
+
+
+def kv_append_tokens_table(pool: int, layer_begin: int, num_layers: int, table_ptr: int, pt_stride: int,
+                           table_rows: int, rows_ptr: int, positions_ptr: int, n: int, k_ptr: int, v_ptr: int,
+                           stream: int = 0) -> None:
+    _check(_lib.kv_append_tokens_table(pool, layer_begin, num_layers, table_ptr or None, pt_stride, table_rows,
+                                       rows_ptr or None, positions_ptr or None, n, k_ptr or None, v_ptr or None,
+                                       stream or None), "kv_append_tokens_table")
 
 
 def kv_fill_synthetic(pool: int, sid: int, gen_sid: int, seed: int, value_mult: float,

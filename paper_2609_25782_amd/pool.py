@@ -101,6 +101,26 @@ class HotColdPool:
         assert k.dtype == self.torch_dtype and k.device == self.device
         kv.kv_append_tokens(self.handle, layer, sids, positions, k.data_ptr(), v.data_ptr(), _stream(stream))
 
+    def write_tokens_layers(self, sid: int, layer_begin: int, tok_begin: int, k: torch.Tensor, v: torch.Tensor,
+                            stream=None) -> None:
+        """k and v [num_layers][n_tok][kv_heads][head_dim]: tokens of layers layer_begin.. in one launch."""
+        assert k.is_contiguous() and v.is_contiguous() and k.shape == v.shape and k.dim() == 4
+        assert k.dtype == self.torch_dtype and k.device == self.device
+        kv.kv_write_tokens_layers(self.handle, sid, layer_begin, k.shape[0], tok_begin, k.shape[1], k.data_ptr(),
+                                  v.data_ptr(), _stream(stream))
+
+    def append_tokens_table(self, layer_begin: int, table: torch.Tensor, rows: torch.Tensor, positions: torch.Tensor,
+                            k: torch.Tensor, v: torch.Tensor, stream=None) -> None:
+        """Device-resolved append: entry i is token positions[i] of table row rows[i]; k and v
+        [num_layers][n][kv_heads][head_dim].  Capturable in a HIP graph."""
+        assert table.dtype == torch.int32 and table.is_contiguous() and table.dim() == 2
+        assert rows.dtype == positions.dtype == torch.int32 and rows.shape == positions.shape
+        assert k.is_contiguous() and v.is_contiguous() and k.shape == v.shape and k.dim() == 4
+        assert k.shape[1] == rows.shape[0] and k.dtype == self.torch_dtype
+        kv.kv_append_tokens_table(self.handle, layer_begin, k.shape[0], table.data_ptr(), table.shape[1],
+                                  table.shape[0], rows.data_ptr(), positions.data_ptr(), rows.shape[0],
+                                  k.data_ptr(), v.data_ptr(), _stream(stream))
+
     def fill_synthetic(self, sid: int, gen_sid: int, seed: int, value_mult: float, stream=None) -> None:
         kv.kv_fill_synthetic(self.handle, sid, gen_sid, seed, float(value_mult), _stream(stream))
 

@@ -31,11 +31,44 @@ Value recipe for coordinate ``c`` (a packed 64-bit integer, see ``coord``):
 
 from __future__ import annotations
 
+import ctypes
 import math
+import os
+import subprocess
+import threading
 from dataclasses import dataclass, field
 from typing import List, Optional
 
 import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "synth_gen.c")
+_LIB_PATH = os.path.join(_HERE, "libsynth_gen.so")
+_lock = threading.Lock()
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile the C form of the value generator (gcc, OpenMP)."""
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", "-o", tmp, _SRC])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            build()
+            lib = ctypes.CDLL(_LIB_PATH)
+            lib.synth_session_kv.restype = None
+            lib.synth_session_kv.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                             ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
+                                             ctypes.c_void_p, ctypes.c_void_p]
+            _lib = lib
+    return _lib
 
 GOLDEN = np.uint64(0x9E3779B97F4A7C15)
 _M1 = np.uint64(0xBF58476D1CE4E5B9)
@@ -104,8 +137,25 @@ def session_kv(seed: int, sid: int, seq_len: int, layer: int, num_kv_heads: int,
                head_dim: int, scale: float, dtype: str):
     """Logical K and V of one session and layer, shape ``[seq_len, num_kv_heads, head_dim]``.
 
-    bf16 is returned as uint16 bit patterns, f32 as float32.
+    bf16 is returned as uint16 bit patterns, f32 as float32.  Computed by the C
+    form of the generator (``synth_gen.c``, the same definition step for step;
+    ``session_kv_numpy`` is the numpy form, and tests hold the two equal bit for
+    bit).
     """
+    store = np.uint16 if dtype == DTYPE_BF16 else np.float32
+    shape = (int(seq_len), int(num_kv_heads), int(head_dim))
+    k = np.empty(shape, store)
+    v = np.empty(shape, store)
+    if k.size:
+        _load().synth_session_kv(int(seed), int(sid), int(seq_len), int(layer), int(num_kv_heads),
+                                 int(head_dim), float(value_multiplier(scale)),
+                                 1 if dtype == DTYPE_BF16 else 0, k.ctypes.data, v.ctypes.data)
+    return k, v
+
+
+def session_kv_numpy(seed: int, sid: int, seq_len: int, layer: int, num_kv_heads: int,
+                     head_dim: int, scale: float, dtype: str):
+    """``session_kv`` computed with numpy from ``values_f32`` (the reference form)."""
     t = np.arange(seq_len, dtype=np.uint64)[:, None, None]
     g = np.arange(num_kv_heads, dtype=np.uint64)[None, :, None]
     d = np.arange(head_dim, dtype=np.uint64)[None, None, :]

@@ -253,6 +253,31 @@ def test_pack_pool_matches_accessor():
             assert pool[off:off + 2].view(np.uint16)[0] == arr[t, g, dd]
 
 
+def test_c_packer_equals_numpy_packer():
+    """The C packer (used for the full-size workloads) writes exactly the numpy
+    packer's bytes, over random page lists, both dtypes, ragged lengths and
+    every layer of a 3-layer pool; untouched bytes stay untouched."""
+    rng = np.random.default_rng(13)
+    for dtype, store, hkv, d in ((oracle.BF16, np.uint16, 4, 128), (oracle.F32, np.float32, 2, 64),
+                                 (oracle.BF16, np.uint16, 1, 64)):
+        pb = oracle.page_bytes(3, hkv, d, dtype)
+        for L in (1, 15, 16, 17, 100):
+            n = (L + 15) // 16
+            pages = rng.permutation(n + 3)[:n].astype(np.int32)
+            for layer in range(3):
+                if store is np.uint16:
+                    k = rng.integers(0, 65535, size=(L, hkv, d), dtype=np.uint16)
+                    v = rng.integers(0, 65535, size=(L, hkv, d), dtype=np.uint16)
+                else:
+                    k = rng.standard_normal((L, hkv, d)).astype(np.float32)
+                    v = rng.standard_normal((L, hkv, d)).astype(np.float32)
+                a = rng.integers(0, 256, size=(n + 3) * pb, dtype=np.uint8)
+                b = a.copy()
+                oracle.pack_pool(a, 3, hkv, d, dtype, layer, pages, k, v)
+                oracle.pack_session(b, 3, hkv, d, dtype, layer, pages, k, v)
+                assert np.array_equal(a, b)
+
+
 def test_p12_paper_shape_numbers():
     """96 KiB of KV per token and 1.5 MiB per 16-token page at 48 layers x 4 KV heads x 128, bf16."""
     with open(os.path.join(GOLDEN, "paper_numbers.json")) as f:

@@ -335,3 +335,37 @@ def test_lazy_resume_hand_worked():
     assert m.promote(5) == [(1, 1)] and m.row(a) == [0, 1, 2, -1]
     with pytest.raises(ModelError):
         PoolModel(4, 4, 2, 2).resume_lazy([0])    # needs spill
+
+
+def test_extend_drops_the_tail_page_cold_copy_hand_worked():
+    """Extending a session writes its partially filled tail page (the new tokens
+    go there first): that page's cold copy is dropped and the next eviction
+    writes it again; full pages keep theirs.  A full tail page is left alone.  A
+    spilled tail page shared with another session cannot take new tokens."""
+    m = PoolModel(num_hot=8, num_cold=8, max_sessions=3, max_pages_per_session=4)
+    a = m.create(20)                 # pages 0, 1 (tokens 16..19 in page 1)
+    assert m.evict(a) == [(0, 0), (1, 1)]
+    m.resume([a])                    # hot 0, 1 again; cold copies 0, 1 valid
+    assert m.sessions[a].cold == [0, 1]
+    m.extend(a, 21)                  # token 20 goes into page 1: its copy is stale
+    assert m.sessions[a].cold == [0, -1] and m.free_cold() == 7
+    m.extend(a, 40)                  # tokens 21..39: page 1 again, and a new page 2
+    assert m.row(a) == [0, 1, 2, -1] and m.sessions[a].cold == [0, -1, -1]
+    assert m.evict(a) == [(1, 1), (2, 2)] and m.cold_writes == 4
+    m.resume([a])
+    b = m.create(32)                 # two full pages
+    m.evict(b)
+    m.resume([b])
+    m.extend(b, 33)                  # the tail page was full: the new token opens page 2
+    assert m.sessions[b].cold[:2] != [-1, -1] and m.sessions[b].cold[2] == -1
+    # spill: a lazily resumed session whose spilled tail page is shared
+    s = PoolModel(num_hot=2, num_cold=8, max_sessions=3, max_pages_per_session=4, spill=True)
+    x = s.import_cold(20, [5, 6])
+    y = s.import_cold(20, [7, 6])    # cold page 6 shared by both tails
+    s.resume_lazy([x])
+    before = copy.deepcopy(s.__dict__)
+    with pytest.raises(ModelError) as e:
+        s.extend(x, 21)
+    assert e.value.code == ERR_STATE and s.__dict__ == before
+    s.extend(x, 20)                  # no new tokens: nothing is written, accepted
+    assert y == 1 and s.sessions[x].seq_len == 20

@@ -36,3 +36,21 @@ def test_workload_placements_are_disjoint():
     assert len(pages) == len(set(pages.tolist())) and pages.max() < w.hot_pages
     assert all(len(p) == synth.pages_for(L) for p, L in zip(w.placement, w.seq_lens))
     assert w.seq_lens.min() >= 8192 and w.seq_lens.max() <= 32768
+
+
+def test_c_generator_equals_numpy_generator():
+    """The C form of the generator gives the numpy form's bits: bf16 and f32, odd
+    sizes, high session, layer and token fields, several scales."""
+    for seed, sid, L, layer, hkv, d, scale, dt in (
+            (0, 0, 1, 0, 1, 64, 1.0, "f32"), (7, 3, 37, 2, 4, 128, 0.0884, "bf16"),
+            (2 ** 40 + 5, 1048575, 19, 63, 2, 64, 1.0, "bf16"), (11, 900, 300, 47, 4, 128, 1.0, "f32"),
+            (3, 5, 5000, 0, 4, 128, 1 / 128 ** 0.5, "bf16")):
+        a = synth.session_kv(seed, sid, L, layer, hkv, d, scale, dt)
+        b = synth.session_kv_numpy(seed, sid, L, layer, hkv, d, scale, dt)
+        for x, y in zip(a, b):
+            assert x.dtype == y.dtype and x.shape == y.shape == (L, hkv, d)
+            assert np.array_equal(x.view(np.uint8), y.view(np.uint8))
+    # token fields up to 2^23 - 1
+    a = synth.session_kv(1, 2, 1, 3, 1, 64, 1.0, "bf16")
+    c = synth.coord(synth.KIND_K, 2, 3, 0, 0, np.arange(64, dtype=np.uint64))
+    assert np.array_equal(a[0][0, 0], synth.f32_to_bf16_bits(synth.values_f32(1, c, 1.0)))
