@@ -633,7 +633,7 @@ def _pct(xs):
             "p90": round(float(np.percentile(xs, 90)), 3)}
 
 
-def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
+def measure_configs(seed: int, steps: int = 10, warmup: int = 3, only=None):
     """Decode throughput on the other workloads: the tiny one (launch-bound), the
     48-layer step (B=64, lognormal lengths, all 48 layers per step, ~170 GB) and
     the skewed one (B=128, power-law lengths up to 256K, one layer timed, also
@@ -645,8 +645,11 @@ def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
     from paper_2609_25782_amd.pool import HotColdPool
     out = {}
     dev = torch.device("cuda", 0)
-    for name, w in (("tiny", synth.config_tiny(seed)), ("step48", synth.config_step48(seed)),
-                    ("skewed", synth.config_skewed(seed))):
+    for name, make in (("tiny", synth.config_tiny), ("step48", synth.config_step48),
+                       ("skewed", synth.config_skewed)):
+        if only and name not in only:
+            continue
+        w = make(seed)
         pool = HotColdPool(w.num_layers, w.num_kv_heads, w.head_dim, w.dtype, w.hot_pages, 0, w.batch,
                            max(synth.pages_for(int(w.seq_lens.max())), 1))
         mult = float(synth.value_multiplier(w.value_scale))
@@ -685,6 +688,9 @@ def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
         pool.close()
         del pool
         torch.cuda.empty_cache()
+    if only:
+        return out
+    out["combine_scaling"] = measure_combine_scaling(seed)
     out["graph_step48"] = measure_graph(seed)
     out["append"] = measure_append(seed)
     log("append: %s" % json.dumps(out["append"]))
@@ -719,6 +725,52 @@ def measure_configs(seed: int, steps: int = 10, warmup: int = 3):
     del a, x
     torch.cuda.empty_cache()
     return out
+
+
+def measure_combine_scaling(seed: int, steps: int = 10, warmup: int = 3):
+    """Split and combine kernel times (the library's profiling hook) for one
+    layer at batches of 128, 1,024 and 8,192 short sessions (512 tokens each):
+    the combine reads each row's page prefix from the split kernel instead of
+    every block rescanning all lengths, so its cost follows the partials it
+    merges, not the batch squared."""
+    import torch
+    import synth
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+    rows = []
+    L = 512
+    for B in (128, 1024, 8192):
+        pool = HotColdPool(1, 4, 128, "bf16", B * synth.pages_for(L), 0, B, synth.pages_for(L))
+        mult = float(synth.value_multiplier(1.0 / math.sqrt(128)))
+        for b in range(B):
+            pool.create_session(L)
+        for b in range(B):
+            pool.fill_synthetic(b, b, seed, mult)
+        q = torch.randn(B, 32, 128, generator=torch.Generator().manual_seed(seed)).to(torch.bfloat16).cuda()
+        sl = torch.full((B,), L, dtype=torch.int32, device="cuda")
+        pt = pool.page_table[:B]
+        out_t = torch.empty_like(q)
+        for _ in range(warmup):
+            pool.decode(0, q, sl, page_table=pt, out=out_t)
+        torch.cuda.synchronize()
+        kv.kv_pool_set_profiling(pool.handle, True)
+        for k in range(kv.KV_KERNEL_COUNT):
+            kv.kv_pool_profile_read(pool.handle, k)
+        for _ in range(steps):
+            pool.decode(0, q, sl, page_table=pt, out=out_t)
+        torch.cuda.synchronize()
+        n1, ms1 = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_DECODE_SPLIT)
+        n2, ms2 = kv.kv_pool_profile_read(pool.handle, kv.KV_KERNEL_DECODE_COMBINE)
+        kv.kv_pool_set_profiling(pool.handle, False)
+        nbytes = sum(decode_bytes([L] * B, 32, 4, 128, 2))
+        rows.append({"batch": B, "seq_len": L, "split_us": round(1e3 * ms1 / n1, 2),
+                     "combine_us": round(1e3 * ms2 / n2, 2),
+                     "GBps_kernels": round(nbytes / ((ms1 / n1 + ms2 / n2) / 1e3) / 1e9, 1)})
+        log("combine scaling: %s" % json.dumps(rows[-1]))
+        pool.close()
+        del pool
+        torch.cuda.empty_cache()
+    return rows
 
 
 def measure_evict(seed: int, reps: int = 3):
@@ -819,25 +871,128 @@ def measure_append(seed: int, steps: int = 20, warmup: int = 3):
         out[name] = {"ms_per_step": round(e0.elapsed_time(e1) / steps, 4),
                      "host_ms_per_step": round(1e3 * host / steps, 4),
                      "calls_per_step": NL if batched else NL * B}
-    # a prompt of 8,192 tokens into one session, every layer
+    # a prompt of 8,192 tokens into one session, every layer: one call per layer,
+    # and one call for all 48 (kv_write_tokens_layers)
     sid = pool.create_session(prompt)
-    kp = torch.randn((prompt, 4, 128), generator=g, device=dev).to(torch.bfloat16)
-    vp = torch.randn((prompt, 4, 128), generator=g, device=dev).to(torch.bfloat16)
-    for _ in range(2):
-        for layer in range(NL):
-            pool.write_tokens(sid, layer, 0, kp, vp)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(5):
-        for layer in range(NL):
-            pool.write_tokens(sid, layer, 0, kp, vp)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / 5
+    kp = torch.randn((NL, prompt, 4, 128), generator=g, device=dev).to(torch.bfloat16)
+    vp = torch.randn((NL, prompt, 4, 128), generator=g, device=dev).to(torch.bfloat16)
     nbytes = 2 * prompt * 4 * 128 * 2 * NL          # K and V written (the same again read)
-    out["prompt_write"] = {"tokens": prompt, "ms": round(ms, 4), "bytes_written": nbytes,
-                           "GBps_written": round(nbytes / (ms / 1e3) / 1e9, 1)}
+
+    def per_layer():
+        for layer in range(NL):
+            pool.write_tokens(sid, layer, 0, kp[layer], vp[layer])
+
+    def all_layers():
+        pool.write_tokens_layers(sid, 0, 0, kp, vp)
+
+    for name, fn in (("prompt_write", per_layer), ("prompt_write_one_call", all_layers)):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(7):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        ms = float(np.median(times))
+        out[name] = {"tokens": prompt, "layers": NL, "calls": NL if fn is per_layer else 1, "ms": round(ms, 4),
+                     "bytes_written": nbytes, "GBps_written": round(nbytes / (ms / 1e3) / 1e9, 1),
+                     "GBps_read_write": round(2 * nbytes / (ms / 1e3) / 1e9, 1),
+                     "frac_of_hbm_peak": round(2 * nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+        log("append: %s %s" % (name, json.dumps(out[name])))
+    pool.close()
+    del kp, vp
+    torch.cuda.empty_cache()
+    out["graph_step"] = measure_graph_append(seed)
+    return out
+
+
+def measure_graph_append(seed: int, steps: int = 20, warmup: int = 3):
+    """A serving step captured in one HIP graph at the paper's shape (48 layers,
+    32 sessions of 8K tokens): the batch-table gather, then for every layer the
+    step's token appended and the decode, with the append fused into the decode
+    launch (paged_decode_attention_append) or as a launch of its own through the
+    table (kv_append_tokens_table).  Against the same graph without appends this
+    gives the append's cost inside a captured step.  The host extends every
+    session by one token before each replay."""
+    import torch
+    import synth
+    from paper_2609_25782_amd.pool import HotColdPool
+    B, NL, L0 = 32, 48, 8192
+    total = 4 * (warmup + steps) + 2          # tokens appended over all graphs' replays
+    pool = HotColdPool(NL, 4, 128, "bf16", B * (synth.pages_for(L0 + total) + 1), 0, B,
+                       synth.pages_for(L0 + total) + 1)
+    dev = pool.device
+    mult = float(synth.value_multiplier(1.0 / math.sqrt(128)))
+    for b in range(B):
+        pool.create_session(L0)
+        pool.fill_synthetic(b, b, seed, mult)
+    q = torch.randn(B, 32, 128, generator=torch.Generator().manual_seed(seed)).to(torch.bfloat16).to(dev)
+    k_new = (0.05 * torch.randn(NL, B, 4, 128, generator=torch.Generator().manual_seed(seed + 1))).to(
+        torch.bfloat16).to(dev)
+    v_new = k_new.flip(0).contiguous()
+    sid_t = torch.arange(B, dtype=torch.int32, device=dev)
+    rows_t = torch.arange(B, dtype=torch.int32, device=dev)
+    pos_t = torch.zeros(B, dtype=torch.int32, device=dev)
+    sl_t = torch.zeros(B, dtype=torch.int32, device=dev)
+    table = torch.empty((B, pool.stride), dtype=torch.int32, device=dev)
+    outs = [torch.empty_like(q) for _ in range(NL)]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    lens = [L0] * B
+
+    def body(append, decode):
+        pool.gather_table(sid_t, out=table, stream=s)
+        for l in range(NL):
+            if append == "table":
+                pool.append_tokens_table(l, table, rows_t, pos_t, k_new[l:l + 1], v_new[l:l + 1], stream=s)
+            if decode:
+                pool.decode(l, q, sl_t, page_table=table, out=outs[l], stream=s,
+                            k_new=k_new[l] if append == "fused" else None,
+                            v_new=v_new[l] if append == "fused" else None)
+
+    def advance():
+        for b in range(B):
+            lens[b] += 1
+            pool.extend(b, lens[b], stream=s)
+        pos_t.copy_(torch.tensor([n - 1 for n in lens], dtype=torch.int32), non_blocking=False)
+        sl_t.copy_(torch.tensor(lens, dtype=torch.int32), non_blocking=False)
+
+    graphs = {}
+    with torch.cuda.stream(s):
+        advance()
+        body("table", True)                     # eager once: the workspace exists before capture
+        torch.cuda.synchronize()
+        for name, a, d in (("table_append_and_decode", "table", True), ("fused_append_decode", "fused", True),
+                           ("decode_only", None, True), ("table_append_only", "table", False)):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s):
+                body(a, d)
+            graphs[name] = g
+        res = {}
+        for name, g in graphs.items():
+            times = []
+            for it in range(warmup + steps):
+                if name != "decode_only":
+                    advance()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(s)
+                g.replay()
+                e1.record(s)
+                torch.cuda.synchronize()
+                if it >= warmup:
+                    times.append(e0.elapsed_time(e1))
+            res[name] = float(np.median(times))
+    out = {"sessions": B, "layers": NL, "context": L0,
+           "step_ms": {k: round(v, 4) for k, v in res.items()},
+           "append_ms_per_step_in_graph": round(res["fused_append_decode"] - res["decode_only"], 4),
+           "table_append_ms_per_step_in_graph": round(res["table_append_and_decode"] - res["decode_only"], 4)}
+    log("append: graph step %s" % json.dumps(out))
+    del graphs
     pool.close()
     torch.cuda.empty_cache()
     return out
@@ -1038,6 +1193,9 @@ def main():
                     help="write a scratch buffer of this many MiB before every timed step, so the "
                          "decode starts with the 256 MB Infinity Cache and the L2s holding other data")
     ap.add_argument("--full-json", default="", help="also write the full result (every sweep row) here")
+    ap.add_argument("--only-config", default="", choices=["", "tiny", "step48", "skewed"],
+                    help="profiling aid: time only this workload's decode (no hot-path step) and print "
+                         "its figures")
     args = ap.parse_args()
     sections = set() if args.no_resume_mix else {x for x in args.sections.split(",") if x and x != "none"}
     unknown = sections - {"resume48", "host", "replay", "spill", "configs"}
@@ -1057,6 +1215,10 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda", 0)
+    if args.only_config:
+        print(json.dumps(measure_configs(args.seed, steps=args.steps, warmup=args.warmup,
+                                         only=[args.only_config])), flush=True)
+        return
     w = synth.config_layer(args.seed, batch=args.batch)
     R = args.resume_per_step
     rng = np.random.Generator(np.random.PCG64([args.seed, 7]))
@@ -1351,8 +1513,21 @@ def compact(result: dict) -> dict:
             if name in c:
                 out["configs"][name] = {"us_per_call_median": c[name]["us_per_call"]["median"],
                                         "GBps": c[name]["GBps"], "pct_of_peak": c[name]["pct_of_peak"]}
+        a = c.get("append")
+        if isinstance(a, dict):
+            keep = {}
+            if "batched_append" in a:
+                keep["host_resolved_ms_per_step"] = a["batched_append"]["ms_per_step"]
+            for name in ("prompt_write", "prompt_write_one_call"):
+                if name in a:
+                    keep[name + "_GBps_read_write"] = a[name]["GBps_read_write"]
+                    keep[name + "_ms"] = a[name]["ms"]
+            if "graph_step" in a:
+                keep["graph_append_ms_per_step"] = a["graph_step"]["append_ms_per_step_in_graph"]
+                keep["graph_step_ms"] = a["graph_step"]["step_ms"]
+            out["configs"]["append"] = keep
         for name, x in c.items():
-            if name not in ("tiny", "step48", "skewed", "context") and isinstance(x, dict):
+            if name not in ("tiny", "step48", "skewed", "context", "append") and isinstance(x, dict):
                 out["configs"][name] = {k: v for k, v in x.items() if not isinstance(v, (list, dict))}
     return out
 

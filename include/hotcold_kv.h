@@ -25,18 +25,29 @@
  * ---------------------------------------------------------------------------
  * KV is stored in pages of KV_PAGE_TOKENS = 16 tokens (paged KV cache, Sec. II;
  * 16 tokens x 96 KiB per token = the paper's 1.5 MiB block, Sec. IV).  Hot and
- * cold pools use the same page format and separate int32 page-id spaces.  One
- * page holds, for every layer and KV head, a K tile and a V tile:
+ * cold pools have separate int32 page-id spaces.  One page holds, for every
+ * layer and KV head, a K tile and a V tile:
  *
- *   page    = [num_layers][num_kv_heads][2 (K tile, V tile)][tile]
+ *   page    = [num_layers][slice]        slice = [num_kv_heads][2 (K tile, V tile)][tile]
  *   tile    = KV_PAGE_TOKENS * head_dim elements
  *   K tile  : element (token t, dim d) at index ((d / x) * 16 + t) * x + d % x,
  *             x = 16 bytes / element size (8 for bf16, 4 for float32):
  *             16-byte groups of x consecutive dims, token-minor.
  *   V tile  : element (t, d) at index d * 16 + t (dims-major, token-minor).
  *
- * page_bytes = num_layers * num_kv_heads * 2 * 16 * head_dim * element size
- * (1.5 MiB for 48 layers x 4 KV heads x 128 dims x bf16).
+ * page_bytes = num_layers * slice_bytes, slice_bytes = num_kv_heads * 2 * 16 *
+ * head_dim * element size (1.5 MiB pages and 32 KiB slices for 48 layers x 4
+ * KV heads x 128 dims x bf16).
+ *
+ * Where the pages sit:
+ *   cold pool  page-major: page c is contiguous at cold_base + c * page_bytes,
+ *              in the order above (the capacity tier's 1.5 MiB block);
+ *   hot pool   layer-major: the slice of page p for layer l is at
+ *              hot_base + (l * num_hot_pages + p) * slice_bytes.
+ * A decode step reads one layer of every active page; layer-major keeps those
+ * reads within 1 / num_layers of the hot pool, which the GPU's address
+ * translation serves with far fewer misses than the same slices spread over
+ * the whole pool.  Copies between the pools convert one layout into the other.
  *
  * A page table is int32 [rows][stride]; row r, entry i is the hot page holding
  * tokens 16 i .. 16 i + 15 of that row's session, -1 when unused.
@@ -632,6 +643,30 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
                            int64_t pt_stride, const int32_t* seq_lens, int32_t batch,
                            int32_t num_q_heads, float scale, void* out, void* workspace,
                            size_t ws_bytes, kv_stream_t stream);
+
+/*
+ * A decode step's append fused into its decode (data paths 3 and 1, Sec. III):
+ * for each batch row b with 0 < L = seq_lens[b] <= 16 * pt_stride, the row's
+ * new token, k_new / v_new row b (device arrays [batch][num_kv_heads][head_dim]
+ * of the pool's dtype, 16-byte aligned), is written as token L - 1 into the
+ * page that page-table entry (L - 1) / 16 names (a hot page, or KV_PAGE_COLD | id:
+ * a spilled page written in place), and then out[b] is the attention over
+ * tokens [0, L), the new one included, exactly as paged_decode_attention would
+ * give after a separate append.  The wave that reads the row's last page for a
+ * KV head writes that head's part of the token first, so the append costs no
+ * launch of its own and no extra pass: one kernel launch per layer serves a
+ * whole decode step's attention and KV append, and a serving step captured in
+ * a HIP graph holds no append nodes.  A tail entry naming no page writes
+ * nothing (and that row decodes to NaN, as in paged_decode_attention).  The
+ * pool's bookkeeping is untouched: call kv_session_extend first, which drops
+ * the cold copy of the page receiving the token.  A layer with staged entries
+ * (paged_decode_prefetch) is refused: the token must go to the page itself.
+ * Other arguments and errors as paged_decode_attention.
+ */
+int paged_decode_attention_append(kv_pool* pool, int32_t layer, const void* q, const void* k_new,
+                                  const void* v_new, const int32_t* page_table, int64_t pt_stride,
+                                  const int32_t* seq_lens, int32_t batch, int32_t num_q_heads, float scale,
+                                  void* out, void* workspace, size_t ws_bytes, kv_stream_t stream);
 
 /*
  * paged_decode_attention without a workspace argument and without allocating:

@@ -104,7 +104,7 @@ struct PageSrc {
     const char* hot = nullptr;
     const char* cold = nullptr;
     const char* stage = nullptr;
-    int64_t page_bytes = 0, slice_bytes = 0;
+    int64_t hot_stride = 0, cold_stride = 0, slice_bytes = 0;
     unsigned num_hot = 0, num_cold = 0, num_stage = 0;
 };
 
@@ -116,7 +116,7 @@ __device__ __forceinline__ void load_page(PageRegs<D, BF16>& r, const PageSrc& p
                                           unsigned koff, unsigned voff) {
     using S = Shape<D, BF16>;
     const char* lh_base = ps.hot;
-    int64_t stride = ps.page_bytes;
+    int64_t stride = ps.hot_stride;
     unsigned n = ps.num_hot;
     unsigned id = static_cast<unsigned>(pid);
     if constexpr (TIERED) {
@@ -128,6 +128,7 @@ __device__ __forceinline__ void load_page(PageRegs<D, BF16>& r, const PageSrc& p
             n = ps.num_stage;
         } else if (tag == 2) {
             lh_base = ps.cold;
+            stride = ps.cold_stride;
             n = ps.num_cold;
         } else if (tag != 0) {
             n = 0;
@@ -365,6 +366,58 @@ __device__ void combine_segment(const DecodeArgs& a, int b, int g, const SegWave
     }
 }
 
+// Fused append (paged_decode_attention_append): the piece holding a row's last
+// page first writes the row's new token, k_new / v_new row b for this wave's
+// KV head, into that page at slot (L - 1) % 16, then orders those stores before
+// its own loads of the page (the same wave is the only reader of that page's
+// tiles for this KV head in the launch).  Rows with L <= 0 or an invalid L, and
+// tail entries that name no page (or a staging slot), write nothing.
+template <int D, bool BF16, bool TIERED>
+__device__ __forceinline__ void append_new_token(const DecodeArgs& a, const PageSrc& ps, const int32_t* row,
+                                                 const Piece& pc, int nb, int seq_len, int lane) {
+    using S = Shape<D, BF16>;
+    if (!a.k_new || pc.p1 != nb || seq_len <= 0 || a.seq_lens[pc.b] != seq_len) return;
+    unsigned id = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(row[nb - 1]));
+    const char* base = ps.hot;
+    int64_t stride = ps.hot_stride;
+    unsigned n = ps.num_hot;
+    if constexpr (TIERED) {
+        const unsigned tag = id >> 29;  // 0 hot, 2 cold; a staged slot is a copy, not the page
+        id &= static_cast<unsigned>(kPageIdMask);
+        if (tag == 2) {
+            base = ps.cold;
+            stride = ps.cold_stride;
+            n = ps.num_cold;
+        } else if (tag != 0) {
+            n = 0;
+        }
+    }
+    if (id >= n) return;
+    char* lh = const_cast<char*>(base) + static_cast<int64_t>(id) * stride;
+    const int slot = (seq_len - 1) % kPageTokens;
+    const int64_t src = (static_cast<int64_t>(pc.b) * a.num_kv_heads + pc.g) * D * S::kElt;
+    const char* ks = static_cast<const char*>(a.k_new) + src;
+    const char* vs = static_cast<const char*>(a.v_new) + src;
+    constexpr int x = 16 / S::kElt;  // elements per 16-byte group of the K tile
+    if (lane < D / x)
+        *reinterpret_cast<u32x4*>(lh + (static_cast<int64_t>(lane) * kPageTokens + slot) * 16) =
+            *reinterpret_cast<const u32x4*>(ks + 16 * lane);
+    for (int d = lane; d < D; d += kWave) {
+        char* vd = lh + S::kTile + (static_cast<int64_t>(d) * kPageTokens + slot) * S::kElt;
+        if constexpr (BF16)
+            *reinterpret_cast<unsigned short*>(vd) = reinterpret_cast<const unsigned short*>(vs)[d];
+        else
+            *reinterpret_cast<unsigned*>(vd) = reinterpret_cast<const unsigned*>(vs)[d];
+    }
+    // Other lanes of this wave read these bytes back with the page's loads.  A
+    // workgroup-scope release/acquire orders that in the memory model; waiting
+    // for the stores to be acknowledged makes the order independent of how the
+    // L1 treats the nontemporal loads (once per row's tail page: negligible).
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
 __device__ __forceinline__ int load_ids(const int32_t* __restrict__ row, int first, int end,
                                         int lane) {
     const int i = first + lane;
@@ -399,16 +452,18 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
     const int32_t* row = a.page_table + static_cast<int64_t>(pc.b) * a.pt_stride;
     const int64_t head_off = static_cast<int64_t>(pc.g) * 2 * S::kTile;
     PageSrc ps;
-    ps.hot = a.hot + a.layer_offset + head_off;
-    ps.page_bytes = a.page_bytes;
+    ps.hot = a.hot + head_off;
+    ps.hot_stride = a.hot_stride;
     ps.num_hot = static_cast<unsigned>(a.num_pages);
     if constexpr (TIERED) {
-        ps.cold = a.cold + a.layer_offset + head_off;
+        ps.cold = a.cold + head_off;
+        ps.cold_stride = a.cold_stride;
         ps.stage = a.stage + head_off;
         ps.slice_bytes = a.slice_bytes;
         ps.num_cold = static_cast<unsigned>(a.num_cold_pages);
         ps.num_stage = static_cast<unsigned>(a.num_stage_slots);
     }
+    append_new_token<D, BF16, TIERED>(a, ps, row, pc, nb, seq_len, lane);
     const unsigned koff = 16u * lane;
     const unsigned voff = BF16 ? (32u * (lane & 15) + 8u * qg) : (64u * (lane & 15) + 16u * qg);
     // valid tokens of the row's last page (16 when full)
@@ -638,16 +693,18 @@ __device__ void run_piece_valu(const DecodeArgs& a, const Piece& pc, int nb, int
     const int32_t* row = a.page_table + static_cast<int64_t>(pc.b) * a.pt_stride;
     const int64_t head_off = static_cast<int64_t>(pc.g) * 2 * S::kTile;
     PageSrc ps;
-    ps.hot = a.hot + a.layer_offset + head_off;
-    ps.page_bytes = a.page_bytes;
+    ps.hot = a.hot + head_off;
+    ps.hot_stride = a.hot_stride;
     ps.num_hot = static_cast<unsigned>(a.num_pages);
     if constexpr (TIERED) {
-        ps.cold = a.cold + a.layer_offset + head_off;
+        ps.cold = a.cold + head_off;
+        ps.cold_stride = a.cold_stride;
         ps.stage = a.stage + head_off;
         ps.slice_bytes = a.slice_bytes;
         ps.num_cold = static_cast<unsigned>(a.num_cold_pages);
         ps.num_stage = static_cast<unsigned>(a.num_stage_slots);
     }
+    append_new_token<D, true, TIERED>(a, ps, row, pc, nb, seq_len, lane);
     const int qg = lane >> 4;
     const unsigned koff = 16u * lane;
     const unsigned voff = 32u * (lane & 15) + 8u * qg;

@@ -20,11 +20,26 @@ enum { kDtypeBf16 = 0, kDtypeF32 = 1 };
 // Waves per 256-thread block of the decode kernel.
 constexpr int kBlockWavesHost = 4;
 
+// Where the pages of one pool live.  The slice of page p for layer l (its K
+// and V tiles of every KV head, [kv_head][K tile, V tile]) starts at
+// base + p * page_stride + l * layer_stride.  The hot pool is layer-major
+// (page_stride = one slice, layer_stride = all of the pool's slices of one
+// layer), so one layer's decode reads within 1 / num_layers of the pool; the
+// cold pool is page-major (page_stride = one page, layer_stride = one slice),
+// each 16-token block contiguous as the capacity tier stores it.
+struct PoolGeom {
+    char* base = nullptr;
+    int64_t page_stride = 0;
+    int64_t layer_stride = 0;
+};
+__host__ __device__ __forceinline__ char* slice_at(const PoolGeom& g, int64_t page, int64_t layer) {
+    return g.base + page * g.page_stride + layer * g.layer_stride;
+}
+
 // Everything the split-K decode kernel and its combine read.
 struct DecodeArgs {
-    const char* hot;          // hot pool base
-    int64_t page_bytes;       // bytes per page
-    int64_t layer_offset;     // byte offset of the layer inside a page
+    const char* hot;          // slice of hot page 0 for the decoded layer
+    int64_t hot_stride;       // bytes between the slices of consecutive hot page ids
     int32_t num_pages;        // hot pages; ids outside [0, num_pages) are rejected
     int32_t num_kv_heads;
     int32_t group;            // query heads per KV head (1..16)
@@ -46,12 +61,17 @@ struct DecodeArgs {
     // Tiered entries (honoured when `tiered` is set): KV_PAGE_COLD names a page
     // of the cold pool, KV_PAGE_STAGED a slot of this layer's staging buffer.
     int32_t tiered;
-    const char* cold;         // cold pool base (device-visible address)
+    const char* cold;         // slice of cold page 0 for the decoded layer (device-visible address)
+    int64_t cold_stride;      // bytes between the slices of consecutive cold page ids
     int32_t num_cold_pages;
     const char* stage;        // staging buffer of this layer: [slot][kv_head][K tile, V tile]
     int32_t num_stage_slots;
     int64_t slice_bytes;      // bytes of one staging slot
     int32_t valu;             // 1: the split runs its products on the vector ALU (bf16, group <= 8)
+    // Fused append (nullable): row b's token L - 1, [batch][num_kv_heads][head_dim], written
+    // into its page before the page is read.
+    const void* k_new;
+    const void* v_new;
 };
 
 // Events a launch records at its kernel's start and end (the library's
@@ -98,7 +118,8 @@ inline size_t decode_workspace_bytes(int64_t slots, int group, int head_dim, int
 // (host runtime).  With no_alloc the call takes no profiling events.
 int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page_table, int64_t pt_stride,
                 const int32_t* seq_lens, int32_t batch, int32_t num_q_heads, float scale, void* out,
-                void* workspace, size_t ws_bytes, kv_stream_t stream, bool no_alloc);
+                void* workspace, size_t ws_bytes, kv_stream_t stream, bool no_alloc,
+                const void* k_new = nullptr, const void* v_new = nullptr);
 
 // Device address of the no-allocation decode's scratch array on `device`
 // (the current device); taken once per device and kept (noalloc.hip).
@@ -129,22 +150,17 @@ struct CopyEntry {
     int32_t pt_value;  // value written there
 };
 
-// For n entries (device array): copies the whole page src_base[e.src] to
-// dst_base[e.dst] where e.src >= 0, and writes page_table[e.pt_index] =
-// e.pt_value where e.pt_index >= 0.
-// max_blocks caps the persistent grid (0: the default cap).
-hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_bytes,
-                            const CopyEntry* entries, int32_t n, int32_t* page_table,
+// For n entries (device array): copies `layers` slices of slice_bytes each
+// (a multiple of 4 KiB), slice l of page e.src in `src` to slice l of page
+// e.dst in `dst`, where e.src >= 0, and writes page_table[e.pt_index] =
+// e.pt_value where e.pt_index >= 0.  Whole pages between the pools: layers =
+// num_layers.  One layer's slices into the staging buffer: layers = 1, src
+// based at that layer.  by_layer walks the copy layer by layer instead of page
+// by page (for copies out of the layer-major hot pool).  max_blocks caps the
+// persistent grid (0: the default).
+hipError_t launch_page_copy(const PoolGeom& src, const PoolGeom& dst, int64_t slice_bytes, int32_t layers,
+                            bool by_layer, const CopyEntry* entries, int32_t n, int32_t* page_table,
                             int32_t max_blocks, hipStream_t s, const LaunchEvents& ev = {});
-
-// The general form: `bytes` (a multiple of 4 KiB) from src_base + e.src *
-// src_stride to dst_base + e.dst * dst_stride.  With src_base at a layer's
-// offset inside cold pages and dst the staging buffer, it gathers one layer's
-// slices of spilled pages.
-hipError_t launch_slice_copy(const char* src_base, int64_t src_stride, char* dst_base,
-                             int64_t dst_stride, int64_t bytes, const CopyEntry* entries, int32_t n,
-                             int32_t* page_table, int32_t max_blocks, hipStream_t s,
-                             const LaunchEvents& ev = {});
 
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t s);
 
@@ -157,9 +173,9 @@ hipError_t launch_read_probe(const void* buf, int64_t bytes, uint32_t* out, int3
 hipError_t launch_table_writes(const CopyEntry* entries, int32_t n, int32_t* page_table, hipStream_t s);
 
 struct SynthArgs {
-    char* hot;
-    char* cold;          // for rows naming spilled pages (KV_PAGE_COLD)
-    int64_t page_bytes;
+    PoolGeom hot;
+    PoolGeom cold;       // for rows naming spilled pages (KV_PAGE_COLD)
+    int64_t slice_bytes;
     const int32_t* row;  // device page-table row of the session
     int32_t first_page;  // first logical page filled
     int32_t num_pages;   // pages filled
@@ -171,9 +187,8 @@ struct SynthArgs {
 hipError_t launch_fill_synthetic(const SynthArgs& a, hipStream_t s);
 
 struct WriteArgs {
-    char* hot;
-    char* cold;          // for rows naming spilled pages (KV_PAGE_COLD)
-    int64_t page_bytes;
+    PoolGeom hot;
+    PoolGeom cold;       // for rows naming spilled pages (KV_PAGE_COLD)
     const int32_t* row;  // device page-table row of the session
     int32_t num_kv_heads, head_dim, dtype, layer;
     int32_t num_layers = 1;  // layers [layer, layer + num_layers)
@@ -195,9 +210,8 @@ struct AppendEntry {
 constexpr int kAppendInline = 256;
 
 struct AppendArgs {
-    char* hot;
-    char* cold;
-    int64_t page_bytes;
+    PoolGeom hot;
+    PoolGeom cold;
     const AppendEntry* entries;  // device [n] when n > kAppendInline
     int32_t n;
     int32_t num_kv_heads, head_dim, dtype, layer;
@@ -210,9 +224,8 @@ hipError_t launch_append_tokens(const AppendArgs& a, hipStream_t s);
 // Appends resolved on the device through a page table: entry r is token
 // positions[r] of table row rows[r], for layers [layer, layer + num_layers).
 struct AppendTableArgs {
-    char* hot;
-    char* cold;
-    int64_t page_bytes;
+    PoolGeom hot;
+    PoolGeom cold;
     int32_t num_hot, num_cold;   // valid page ids of each pool
     const int32_t* table;        // device [table_rows][pt_stride]
     int64_t pt_stride;

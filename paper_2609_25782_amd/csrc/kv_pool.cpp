@@ -206,6 +206,10 @@ struct kv_pool {
     bool profiling = false;
     int32_t combine_mode = KV_COMBINE_SEPARATE;
     char* cold_host = nullptr;      // host address of a pinned-host cold pool (null otherwise)
+    // Pool geometries: the hot pool is layer-major (one layer's slices of all
+    // pages together: a decode reads within 1 / num_layers of it), the cold
+    // pool page-major (each 16-token block contiguous).
+    hck::PoolGeom hot_geom, cold_geom;
     int32_t host_copy = KV_HOST_COPY_DMA;
     int32_t compute_mode = KV_DECODE_MATRIX;
     int32_t* counters = nullptr;  // decode arrival counters, zero between calls
@@ -351,12 +355,12 @@ struct kv_pool {
         }
     }
 
-    // Enqueue page copies (in chunks that fit a staging slot).  Entries that
+    // Enqueue whole-page copies between the pools (in chunks that fit a
+    // staging slot): cold -> hot when to_hot, else hot -> cold.  Entries that
     // only write the page table (rows cleared on eviction, resident pages
     // remapped on resume) go to the table-write kernel instead, so the copy
     // grid only walks pages that move.
-    int submit_copies(const char* src, char* dst, const std::vector<hck::CopyEntry>& all,
-                      hipStream_t s, int kernel_id) {
+    int submit_copies(bool to_hot, const std::vector<hck::CopyEntry>& all, hipStream_t s, int kernel_id) {
         std::vector<hck::CopyEntry> entries, writes;
         entries.reserve(all.size());
         for (const hck::CopyEntry& e : all) {
@@ -369,8 +373,9 @@ struct kv_pool {
             int rc = submit_table_writes(writes, s);
             if (rc) return rc;
         }
-        if (cold_host && host_copy == KV_HOST_COPY_DMA && (src == cold || dst == cold))
-            return submit_dma_copies(src, dst, entries, s, kernel_id);
+        if (cold_host && host_copy == KV_HOST_COPY_DMA) return submit_dma_copies(to_hot, entries, s, kernel_id);
+        const hck::PoolGeom& src = to_hot ? cold_geom : hot_geom;
+        const hck::PoolGeom& dst = to_hot ? hot_geom : cold_geom;
         for (size_t off = 0; off < entries.size(); off += kStagingEntries) {
             const int32_t n = static_cast<int32_t>(
                 std::min<size_t>(kStagingEntries, entries.size() - off));
@@ -382,9 +387,8 @@ struct kv_pool {
                                           hipMemcpyHostToDevice, s);
             if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(copy list)");
             const hck::LaunchEvents ev = prof_events();
-            e = hck::launch_page_copy(src, dst, page_bytes,
-                                      static_cast<const hck::CopyEntry*>(slot->dev), n, pt,
-                                      copy_blocks, s, ev);
+            e = hck::launch_page_copy(src, dst, slice_bytes, d.num_layers, /*by_layer=*/!to_hot,
+                                      static_cast<const hck::CopyEntry*>(slot->dev), n, pt, copy_blocks, s, ev);
             prof_done(kernel_id, ev, e);
             if (e != hipSuccess) return hip_fail(e, "page copy launch");
             e = hipEventRecord(slot->done, s);
@@ -394,35 +398,47 @@ struct kv_pool {
         return KV_OK;
     }
 
-    // Enqueue page-table element writes only (entries' pt_index / pt_value).
-    // Page copies to or from a pinned-host cold pool on the DMA engines: one
-    // hipMemcpyAsync per run of pages consecutive on both sides, then the
-    // page-table entries (stream-ordered after the copies).  A copy kernel
+    // Page copies to or from a pinned-host cold pool on the DMA engines, then
+    // the page-table entries (stream-ordered after the copies).  A copy kernel
     // reading or writing host memory keeps its waves waiting on PCIe in the
     // CUs' memory pipelines, which slows a decode running on another stream
-    // many times over; the DMA engines use no CU.
-    int submit_dma_copies(const char* src, char* dst, const std::vector<hck::CopyEntry>& entries,
-                          hipStream_t s, int kernel_id) {
+    // many times over; the DMA engines use no CU.  A host page is contiguous
+    // and a hot page is one slice per layer.  A run of k pages consecutive on
+    // both sides is min(k, num_layers) 2D copies: one per page (num_layers
+    // rows of one slice), or for long runs one per layer (k rows of one slice,
+    // contiguous in the hot pool, a page apart in host memory).
+    int submit_dma_copies(bool to_hot, const std::vector<hck::CopyEntry>& entries, hipStream_t s, int kernel_id) {
         if (entries.empty()) return KV_OK;
-        const bool to_host = dst == cold;
-        const char* src_base = to_host ? src : cold_host;
-        char* dst_base = to_host ? cold_host : dst;
-        const hipMemcpyKind kind = to_host ? hipMemcpyDeviceToHost : hipMemcpyHostToDevice;
+        const hipMemcpyKind kind = to_hot ? hipMemcpyHostToDevice : hipMemcpyDeviceToHost;
+        const size_t slice = static_cast<size_t>(slice_bytes);
         const hck::LaunchEvents ev = prof_events();
         hipError_t e = ev.start ? hipEventRecord(ev.start, s) : hipSuccess;
+        auto copy2d = [&](char* hot_p, size_t hot_pitch, char* host_p, size_t host_pitch, size_t rows) {
+            return to_hot ? hipMemcpy2DAsync(hot_p, hot_pitch, host_p, host_pitch, slice, rows, kind, s)
+                          : hipMemcpy2DAsync(host_p, host_pitch, hot_p, hot_pitch, slice, rows, kind, s);
+        };
         for (size_t i = 0; i < entries.size() && e == hipSuccess;) {
             size_t j = i + 1;
             while (j < entries.size() && entries[j].src == entries[j - 1].src + 1 &&
                    entries[j].dst == entries[j - 1].dst + 1)
                 ++j;
-            e = hipMemcpyAsync(dst_base + static_cast<int64_t>(entries[i].dst) * page_bytes,
-                               src_base + static_cast<int64_t>(entries[i].src) * page_bytes,
-                               static_cast<size_t>(j - i) * page_bytes, kind, s);
+            const size_t k = j - i;
+            const int32_t hp = to_hot ? entries[i].dst : entries[i].src;
+            const int32_t cp = to_hot ? entries[i].src : entries[i].dst;
+            char* host_p = cold_host + static_cast<int64_t>(cp) * page_bytes;
+            if (k >= static_cast<size_t>(d.num_layers)) {
+                for (int32_t l = 0; l < d.num_layers && e == hipSuccess; ++l)
+                    e = copy2d(hck::slice_at(hot_geom, hp, l), slice, host_p + l * slice, page_bytes, k);
+            } else {
+                for (size_t m = 0; m < k && e == hipSuccess; ++m)
+                    e = copy2d(hck::slice_at(hot_geom, hp + static_cast<int32_t>(m), 0), hot_geom.layer_stride,
+                               host_p + m * page_bytes, slice, d.num_layers);
+            }
             i = j;
         }
         if (e == hipSuccess && ev.stop) e = hipEventRecord(ev.stop, s);
         prof_done(kernel_id, ev, e);
-        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(host-tier pages)");
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpy2DAsync(host-tier pages)");
         std::vector<hck::CopyEntry> writes;
         for (const hck::CopyEntry& c : entries)
             if (c.pt_index >= 0) writes.push_back(hck::CopyEntry{-1, -1, c.pt_index, c.pt_value});
@@ -590,7 +606,7 @@ struct kv_pool {
                                              v.sid * d.max_pages_per_session + v.page, -1});
             k += copy;
         }
-        int rc = submit_copies(hot, cold, entries, s, KV_KERNEL_EVICT_COPY);
+        int rc = submit_copies(false, entries, s, KV_KERNEL_EVICT_COPY);
         if (!rc) rc = note_frees(s);
         return rc;
     }
@@ -668,6 +684,7 @@ int kv_pool_create(const kv_pool_desc* desc, void* hot_base, size_t hot_bytes, v
     p->d = *desc;
     p->meta = meta;
     p->page_bytes = static_cast<int64_t>(pb);
+    p->slice_bytes = static_cast<int64_t>(pb) / desc->num_layers;
     p->hot_free.init(desc->num_hot_pages);
     p->cold_free.init(desc->num_cold_pages);
     p->cold_ref.assign(desc->num_cold_pages, 0);
@@ -689,6 +706,8 @@ int kv_pool_create(const kv_pool_desc* desc, void* hot_base, size_t hot_bytes, v
         } else {
             p->cold = static_cast<char*>(cold_base);
         }
+        p->hot_geom = hck::PoolGeom{p->hot, p->slice_bytes, p->slice_bytes * desc->num_hot_pages};
+        p->cold_geom = hck::PoolGeom{p->cold, p->page_bytes, p->slice_bytes};
         e = hipDeviceGetAttribute(&p->cus, hipDeviceAttributeMultiprocessorCount, desc->device);
         if (e != hipSuccess) {
             delete p;
@@ -995,9 +1014,8 @@ int kv_append_tokens(kv_pool* pool, int32_t layer, const int32_t* sids, const in
             if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(append list)");
             a.entries = static_cast<const hck::AppendEntry*>(slot->dev);
         }
-        a.hot = pool->hot;
-        a.cold = pool->cold;
-        a.page_bytes = pool->page_bytes;
+        a.hot = pool->hot_geom;
+        a.cold = pool->cold_geom;
         a.n = n;
         a.num_kv_heads = pool->d.num_kv_heads;
         a.head_dim = pool->d.head_dim;
@@ -1046,9 +1064,8 @@ int kv_write_tokens_layers(kv_pool* pool, int32_t sid, int32_t layer_begin, int3
             return fail(KV_ERR_INVALID, "k and v must be 16-byte aligned");
         DeviceGuard g(pool->d.device);
         hck::WriteArgs a;
-        a.hot = pool->hot;
-        a.cold = pool->cold;
-        a.page_bytes = pool->page_bytes;
+        a.hot = pool->hot_geom;
+        a.cold = pool->cold_geom;
         a.row = pool->pt + static_cast<int64_t>(sid) * pool->d.max_pages_per_session;
         a.num_kv_heads = pool->d.num_kv_heads;
         a.head_dim = pool->d.head_dim;
@@ -1094,9 +1111,8 @@ int kv_append_tokens_table(kv_pool* pool, int32_t layer_begin, int32_t num_layer
         return fail(KV_ERR_INVALID, "k and v must be 16-byte aligned");
     DeviceGuard g(pool->d.device);
     hck::AppendTableArgs a;
-    a.hot = pool->hot;
-    a.cold = pool->cold;
-    a.page_bytes = pool->page_bytes;
+    a.hot = pool->hot_geom;
+    a.cold = pool->cold_geom;
     a.num_hot = pool->d.num_hot_pages;
     a.num_cold = pool->cold ? pool->d.num_cold_pages : 0;
     a.table = table;
@@ -1136,9 +1152,9 @@ int kv_fill_synthetic_pages(kv_pool* pool, int32_t sid, int32_t gen_sid, uint64_
             return fail(KV_ERR_STATE, "page %d is spilled to a cold page shared with another session", i);
     DeviceGuard g(pool->d.device);
     hck::SynthArgs a;
-    a.hot = pool->hot;
-    a.cold = pool->cold;
-    a.page_bytes = pool->page_bytes;
+    a.hot = pool->hot_geom;
+    a.cold = pool->cold_geom;
+    a.slice_bytes = pool->slice_bytes;
     a.row = pool->pt + static_cast<int64_t>(sid) * pool->d.max_pages_per_session;
     a.first_page = first_page;
     a.num_pages = num_pages;
@@ -1213,7 +1229,7 @@ int kv_promote_pages(kv_pool* pool, int32_t n, kv_stream_t stream, int32_t* prom
         }
         rc = pool->order_after_frees(st);
         if (!rc) rc = pool->submit_victims(a, st);
-        if (!rc) rc = pool->submit_copies(pool->cold, pool->hot, copies, st, KV_KERNEL_PAGE_COPY);
+        if (!rc) rc = pool->submit_copies(true, copies, st, KV_KERNEL_PAGE_COPY);
         if (!rc) rc = pool->submit_table_writes(writes, st);
         if (rc) return rc;
     }
@@ -1270,7 +1286,7 @@ int kv_evict_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_t
                 k += copy;
             }
         }
-        int rc = pool->submit_copies(pool->hot, pool->cold, entries, st, KV_KERNEL_EVICT_COPY);
+        int rc = pool->submit_copies(false, entries, st, KV_KERNEL_EVICT_COPY);
         if (!rc) rc = pool->note_frees(st);
         if (rc) return rc;
     }
@@ -1347,7 +1363,7 @@ int kv_resume_sessions(kv_pool* pool, const int32_t* sids, int32_t n, kv_stream_
         }
         rc = pool->order_after_frees(st);
         if (!rc) rc = pool->submit_victims(a, st);
-        if (!rc) rc = pool->submit_copies(pool->cold, pool->hot, entries, st, KV_KERNEL_PAGE_COPY);
+        if (!rc) rc = pool->submit_copies(true, entries, st, KV_KERNEL_PAGE_COPY);
         if (rc) return rc;
     }
     pool->commit_victims(a);
@@ -1488,13 +1504,23 @@ int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const in
                             out, workspace, ws_bytes, stream, /*no_alloc=*/false);
 }
 
+int paged_decode_attention_append(kv_pool* pool, int32_t layer, const void* q, const void* k_new,
+                                  const void* v_new, const int32_t* page_table, int64_t pt_stride,
+                                  const int32_t* seq_lens, int32_t batch, int32_t num_q_heads, float scale,
+                                  void* out, void* workspace, size_t ws_bytes, kv_stream_t stream) {
+    if (!k_new || !v_new) return fail(KV_ERR_INVALID, "NULL k_new or v_new");
+    return hck::decode_impl(pool, layer, q, page_table, pt_stride, seq_lens, batch, num_q_heads, scale,
+                            out, workspace, ws_bytes, stream, /*no_alloc=*/false, k_new, v_new);
+}
+
 }  // extern "C"
 
 namespace hck {
 
 int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page_table, int64_t pt_stride,
                 const int32_t* seq_lens, int32_t batch, int32_t num_q_heads, float scale, void* out,
-                void* workspace, size_t ws_bytes, kv_stream_t stream, bool no_alloc) {
+                void* workspace, size_t ws_bytes, kv_stream_t stream, bool no_alloc, const void* k_new,
+                const void* v_new) {
     if (!pool) return fail(KV_ERR_INVALID, "NULL pool");
     if (pool->meta) return fail(KV_ERR_INVALID, "metadata-only pool cannot decode");
     if (layer < 0 || layer >= pool->d.num_layers) return fail(KV_ERR_INVALID, "bad layer %d", layer);
@@ -1517,6 +1543,9 @@ int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page
         return fail(KV_ERR_INVALID, "workspace must be 256-byte aligned");
     if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(out)) & 15)
         return fail(KV_ERR_INVALID, "q and out must be 16-byte aligned");
+    if ((k_new != nullptr) != (v_new != nullptr) ||
+        ((reinterpret_cast<uintptr_t>(k_new) | reinterpret_cast<uintptr_t>(v_new)) & 15))
+        return fail(KV_ERR_INVALID, "k_new and v_new: both or neither, 16-byte aligned");
     DeviceGuard g(pool->d.device);
     const int32_t waves = pool->decode_waves();
     const int64_t slots = static_cast<int64_t>(waves) + static_cast<int64_t>(batch) * pool->d.num_kv_heads;
@@ -1528,10 +1557,8 @@ int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page
         return fail(KV_ERR_INVALID, "workspace %zu bytes, need %zu", ws_bytes, need);
     }
     hck::DecodeArgs a;
-    a.hot = pool->hot;
-    a.page_bytes = pool->page_bytes;
-    a.layer_offset = static_cast<int64_t>(layer) * pool->d.num_kv_heads * 2 * KV_PAGE_TOKENS *
-                     pool->d.head_dim * static_cast<int64_t>(elt_size(pool->d.dtype));
+    a.hot = hck::slice_at(pool->hot_geom, 0, layer);
+    a.hot_stride = pool->hot_geom.page_stride;
     a.num_pages = pool->d.num_hot_pages;
     a.num_kv_heads = pool->d.num_kv_heads;
     a.group = group;
@@ -1553,13 +1580,18 @@ int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page
     a.fused = pool->combine_mode == KV_COMBINE_FUSED ? 1 : 0;
     a.tiered = pool->tiered() ? 1 : 0;
     a.valu = valu ? 1 : 0;
-    a.cold = pool->cold;
+    a.cold = pool->cold ? hck::slice_at(pool->cold_geom, 0, layer) : nullptr;
+    a.cold_stride = pool->cold_geom.page_stride;
     a.num_cold_pages = pool->cold ? pool->d.num_cold_pages : 0;
     a.slice_bytes = pool->slice_bytes;
     a.stage = nullptr;
     a.num_stage_slots = 0;
+    a.k_new = k_new;
+    a.v_new = v_new;
     const int half = layer & 1;
     const bool staged = pool->stage_slots > 0 && !pool->plan.empty() && pool->half_layer[half] == layer;
+    if (staged && k_new)
+        return fail(KV_ERR_INVALID, "the fused append writes pages, not staged copies: no staged layer");
     if (staged) {
         a.stage = pool->stage + static_cast<int64_t>(half) * pool->stage_slots * pool->slice_bytes;
         a.num_stage_slots = static_cast<int32_t>(pool->plan.size());
@@ -1628,10 +1660,8 @@ int kv_pool_set_staging(kv_pool* pool, void* staging, size_t bytes, int32_t* slo
     DeviceGuard g(pool->d.device);
     if (pool->decode_pending) (void)hipEventSynchronize(pool->decode_event);
     pool->free_staging_state();
-    const int64_t slice = static_cast<int64_t>(pool->d.num_kv_heads) * 2 * KV_PAGE_TOKENS *
-                          pool->d.head_dim * static_cast<int64_t>(elt_size(pool->d.dtype));
+    const int64_t slice = pool->slice_bytes;
     const int64_t n = staging ? static_cast<int64_t>(bytes) / (2 * slice) : 0;
-    pool->slice_bytes = slice;
     pool->stage = n > 0 ? static_cast<char*>(staging) : nullptr;
     pool->stage_slots = static_cast<int32_t>(std::min<int64_t>(n, int64_t(1) << 28));
     if (pool->stage_slots > 0) {
@@ -1735,12 +1765,13 @@ int paged_decode_prefetch(kv_pool* pool, int32_t layer, kv_stream_t copy_stream)
     if (pool->plan_ready_pending) e = hipStreamWaitEvent(cs, pool->plan_ready, 0);
     if (e == hipSuccess && pool->half_free_pending[half]) e = hipStreamWaitEvent(cs, pool->half_free[half], 0);
     if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(prefetch)");
-    const int64_t layer_offset = static_cast<int64_t>(layer) * pool->slice_bytes;
-    char* dst = pool->stage + static_cast<int64_t>(half) * pool->stage_slots * pool->slice_bytes;
+    // layer `layer` of each planned cold page into its staging slot
+    const hck::PoolGeom src{hck::slice_at(pool->cold_geom, 0, layer), pool->cold_geom.page_stride, 0};
+    const hck::PoolGeom dst{pool->stage + static_cast<int64_t>(half) * pool->stage_slots * pool->slice_bytes,
+                            pool->slice_bytes, 0};
     const hck::LaunchEvents ev = pool->prof_events();
-    e = hck::launch_slice_copy(pool->cold + layer_offset, pool->page_bytes, dst, pool->slice_bytes,
-                               pool->slice_bytes, pool->plan_dev, static_cast<int32_t>(pool->plan.size()),
-                               nullptr, pool->copy_blocks, cs, ev);
+    e = hck::launch_page_copy(src, dst, pool->slice_bytes, 1, false, pool->plan_dev,
+                              static_cast<int32_t>(pool->plan.size()), nullptr, pool->copy_blocks, cs, ev);
     pool->prof_done(KV_KERNEL_PREFETCH_COPY, ev, e);
     if (e != hipSuccess) return hip_fail(e, "prefetch launch");
     e = hipEventRecord(pool->half_ready[half], cs);

@@ -44,36 +44,51 @@ namespace {
 #define HCK_COPY_MAX_UNROLL 8
 #endif
 
-// Address of the page a session row names: a hot page, or a spilled page of the
-// cold pool (KV_PAGE_COLD).  The host writes rows only with such entries.
-__device__ __forceinline__ char* page_address(char* hot, char* cold, int32_t pid, int64_t page_bytes) {
-    return (pid & kPageCold) ? cold + static_cast<int64_t>(pid & kPageIdMask) * page_bytes
-                             : hot + static_cast<int64_t>(pid) * page_bytes;
+// The slice of layer `layer` of the page a session row names: a hot page, or a
+// spilled page of the cold pool (KV_PAGE_COLD).  The host writes rows only
+// with such entries.
+__device__ __forceinline__ char* entry_slice(const PoolGeom& hot, const PoolGeom& cold, int32_t pid, int layer) {
+    return (pid & kPageCold) ? slice_at(cold, pid & kPageIdMask, layer) : slice_at(hot, pid, layer);
 }
 
 // A block copies chunks of `U` x 4 KiB: every thread moves U 16-byte words, all
 // loads issued before the first store.  The host picks U so that a chunk
-// divides the page, so the body has no bounds checks (pages are always a
-// multiple of 4 KiB: two tiles of at least 2 KiB per layer and KV head).  The
-// grid is persistent: block i takes chunks i, i + grid, ... of the whole copy
-// list, so a multi-GB resume is a few thousand long-lived blocks rather than
-// millions of short ones.
+// divides a slice (one layer of a page, a multiple of 4 KiB: two tiles of at
+// least 2 KiB per KV head), so no chunk crosses from one slice to the next and
+// the body has no bounds checks; each side maps (page, slice) through its own
+// pool geometry.  The grid is persistent: block i takes chunks i, i + grid, ...
+// of the whole copy list, so a multi-GB resume is a few thousand long-lived
+// blocks rather than millions of short ones.  Chunks are walked page by page,
+// or with `by_layer` layer by layer (every page's slice of layer 0 first): a
+// copy out of the layer-major hot pool then reads within one layer's share of
+// it at a time, which address translation serves far better than slices
+// spread over the whole pool (reads stall on it; the scattered writes of the
+// other direction are posted and hurt less).
 template <int U>
 __global__ __launch_bounds__(kBlockThreads) void page_copy_kernel(
-    const char* __restrict__ src_base, int64_t src_stride, char* __restrict__ dst_base,
-    int64_t dst_stride, const CopyEntry* __restrict__ entries, int32_t n, int chunks_per_page,
-    int32_t* __restrict__ page_table) {
-    const int64_t total = static_cast<int64_t>(n) * chunks_per_page;
+    const PoolGeom src, const PoolGeom dst, const CopyEntry* __restrict__ entries, int32_t n,
+    int chunks_per_entry, int chunks_per_slice, int by_layer, int32_t* __restrict__ page_table) {
+    const int64_t total = static_cast<int64_t>(n) * chunks_per_entry;
+    const int64_t per_layer = static_cast<int64_t>(n) * chunks_per_slice;
     for (int64_t flat = blockIdx.x; flat < total; flat += gridDim.x) {
-        const int ent = static_cast<int>(flat / chunks_per_page);
-        const int chunk = static_cast<int>(flat % chunks_per_page);
+        int ent, layer, cs;
+        if (by_layer) {
+            layer = static_cast<int>(flat / per_layer);
+            const int64_t rem = flat % per_layer;
+            ent = static_cast<int>(rem / chunks_per_slice);
+            cs = static_cast<int>(rem % chunks_per_slice);
+        } else {
+            ent = static_cast<int>(flat / chunks_per_entry);
+            const int chunk = static_cast<int>(flat % chunks_per_entry);
+            layer = chunk / chunks_per_slice;
+            cs = chunk % chunks_per_slice;
+        }
         const CopyEntry e = entries[ent];
-        if (chunk == 0 && threadIdx.x == 0 && e.pt_index >= 0) page_table[e.pt_index] = e.pt_value;
+        if (layer == 0 && cs == 0 && threadIdx.x == 0 && e.pt_index >= 0) page_table[e.pt_index] = e.pt_value;
         if (e.src < 0) continue;
-        const int64_t base = static_cast<int64_t>(chunk) * U * kBlockThreads * 16;
-        const u32x4* s =
-            reinterpret_cast<const u32x4*>(src_base + e.src * src_stride + base) + threadIdx.x;
-        u32x4* d = reinterpret_cast<u32x4*>(dst_base + e.dst * dst_stride + base) + threadIdx.x;
+        const int64_t off = static_cast<int64_t>(cs) * U * kBlockThreads * 16;
+        const u32x4* s = reinterpret_cast<const u32x4*>(slice_at(src, e.src, layer) + off) + threadIdx.x;
+        u32x4* d = reinterpret_cast<u32x4*>(slice_at(dst, e.dst, layer) + off) + threadIdx.x;
         u32x4 buf[U];
 #pragma unroll
         for (int i = 0; i < U; ++i)
@@ -175,7 +190,7 @@ __global__ __launch_bounds__(kBlockThreads) void fill_synthetic_kernel(SynthArgs
     const int elt = bf16 ? 2 : 4;
     const int x = 16 / elt;
     const int64_t tile = static_cast<int64_t>(kPageTokens) * a.head_dim * elt;
-    const int64_t groups_per_page = a.page_bytes / 16;
+    const int64_t groups_per_page = a.slice_bytes * a.num_layers / 16;
     const int64_t total = groups_per_page * a.num_pages;
     const uint64_t key = splitmix_mix(a.seed);
     for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; gi < total;
@@ -223,7 +238,7 @@ __global__ __launch_bounds__(kBlockThreads) void fill_synthetic_kernel(SynthArgs
                                           a.value_mult));
             }
         }
-        *reinterpret_cast<u32x4*>(page_address(a.hot, a.cold, pid, a.page_bytes) + byte) =
+        *reinterpret_cast<u32x4*>(entry_slice(a.hot, a.cold, pid, layer) + byte % a.slice_bytes) =
             u32x4{words[0], words[1], words[2], words[3]};
     }
 }
@@ -282,8 +297,7 @@ __global__ __launch_bounds__(kBlockThreads) void write_tokens_kernel(WriteArgs a
         *reinterpret_cast<u32x4*>(&s_v[t][cd * x]) = *reinterpret_cast<const u32x4*>(static_cast<const T*>(a.v) + src);
     }
     __syncthreads();
-    char* lh = page_address(a.hot, a.cold, a.row[page], a.page_bytes) +
-               (static_cast<int64_t>(layer) * a.num_kv_heads + head) * 2 * tile;
+    char* lh = entry_slice(a.hot, a.cold, a.row[page], layer) + static_cast<int64_t>(head) * 2 * tile;
     // K tile: [group][token][x]
     for (int e = tid; e < groups * kPageTokens; e += kBlockThreads) {
         const int cd = e / kPageTokens, t = e % kPageTokens;
@@ -325,8 +339,7 @@ __global__ __launch_bounds__(kBlockThreads) void append_tokens_kernel(const Appe
         const int head = static_cast<int>((gi / groups) % a.num_kv_heads);
         const int r = static_cast<int>(gi / (static_cast<int64_t>(groups) * a.num_kv_heads));
         const AppendEntry e = a.n <= kAppendInline ? a.inline_entries[r] : a.entries[r];
-        char* lh = page_address(a.hot, a.cold, e.page, a.page_bytes) +
-                   (static_cast<int64_t>(a.layer) * a.num_kv_heads + head) * 2 * tile;
+        char* lh = entry_slice(a.hot, a.cold, e.page, a.layer) + static_cast<int64_t>(head) * 2 * tile;
         const int64_t src = ((static_cast<int64_t>(r) * a.num_kv_heads + head) * a.head_dim + cd * x) * elt;
         write_token_group(lh, tile, e.slot, cd, x, elt, static_cast<const char*>(a.k) + src,
                           static_cast<const char*>(a.v) + src);
@@ -361,8 +374,7 @@ __global__ __launch_bounds__(kBlockThreads) void append_table_kernel(const Appen
         if (!((tag == 0 && id < static_cast<unsigned>(a.num_hot)) ||
               (tag == 2 && id < static_cast<unsigned>(a.num_cold))))
             continue;
-        char* lh = page_address(a.hot, a.cold, pid, a.page_bytes) +
-                   (static_cast<int64_t>(a.layer + li) * a.num_kv_heads + head) * 2 * tile;
+        char* lh = entry_slice(a.hot, a.cold, pid, a.layer + li) + static_cast<int64_t>(head) * 2 * tile;
         const int64_t src = (((static_cast<int64_t>(li) * a.n + r) * a.num_kv_heads + head) * a.head_dim + cd * x) * elt;
         write_token_group(lh, tile, pos % kPageTokens, cd, x, elt, static_cast<const char*>(a.k) + src,
                           static_cast<const char*>(a.v) + src);
@@ -425,39 +437,32 @@ int grid_for(int64_t work, int cap) {
 
 }  // namespace
 
-hipError_t launch_page_copy(const char* src_base, char* dst_base, int64_t page_bytes,
-                            const CopyEntry* entries, int32_t n, int32_t* page_table,
+hipError_t launch_page_copy(const PoolGeom& src, const PoolGeom& dst, int64_t slice_bytes, int32_t layers,
+                            bool by_layer, const CopyEntry* entries, int32_t n, int32_t* page_table,
                             int32_t max_blocks, hipStream_t s, const LaunchEvents& ev) {
-    return launch_slice_copy(src_base, page_bytes, dst_base, page_bytes, page_bytes, entries, n,
-                             page_table, max_blocks, s, ev);
-}
-
-hipError_t launch_slice_copy(const char* src_base, int64_t src_stride, char* dst_base,
-                             int64_t dst_stride, int64_t bytes, const CopyEntry* entries, int32_t n,
-                             int32_t* page_table, int32_t max_blocks, hipStream_t s,
-                             const LaunchEvents& ev) {
     if (n <= 0) return hipSuccess;
     constexpr int64_t kRow = static_cast<int64_t>(kBlockThreads) * 16;  // 4 KiB
-    if (bytes % kRow || bytes <= 0) return hipErrorInvalidValue;
-    const int64_t rows = bytes / kRow;
+    if (slice_bytes % kRow || slice_bytes <= 0 || layers < 1) return hipErrorInvalidValue;
+    const int64_t rows = slice_bytes / kRow;  // per slice
     // a caller's budget (max_blocks) keeps few blocks: they take the large chunks
-    const bool fine = max_blocks <= 0 && rows * n <= HCK_COPY_FINE_ROWS;
+    const bool fine = max_blocks <= 0 && rows * layers * n <= HCK_COPY_FINE_ROWS;
     constexpr int kMaxU = HCK_COPY_MAX_UNROLL;
     const int u = fine ? 1
                 : (kMaxU >= 8 && rows % 8 == 0) ? 8
                 : (kMaxU >= 4 && rows % 4 == 0) ? 4
                 : (kMaxU >= 2 && rows % 2 == 0) ? 2 : 1;
-    const int64_t chunks = rows / u;
-    const int64_t work = chunks * n;
+    const int cps = static_cast<int>(rows / u);
+    const int cpe = cps * layers;
+    const int64_t work = static_cast<int64_t>(cpe) * n;
     const int64_t cap = max_blocks > 0 ? max_blocks : fine ? HCK_COPY_FINE_BLOCKS : HCK_COPY_MAX_BLOCKS;
     const int64_t blocks = work < cap ? work : cap;
-    const int cpp = static_cast<int>(chunks);
     const void* k = u == 8   ? reinterpret_cast<const void*>(&page_copy_kernel<8>)
                     : u == 4 ? reinterpret_cast<const void*>(&page_copy_kernel<4>)
                     : u == 2 ? reinterpret_cast<const void*>(&page_copy_kernel<2>)
                              : reinterpret_cast<const void*>(&page_copy_kernel<1>);
-    void* args[] = {&src_base, &src_stride, &dst_base, &dst_stride, &entries, &n, const_cast<int*>(&cpp),
-                    &page_table};
+    int bl = by_layer ? 1 : 0;
+    void* args[] = {const_cast<PoolGeom*>(&src), const_cast<PoolGeom*>(&dst), &entries, &n,
+                    const_cast<int*>(&cpe), const_cast<int*>(&cps), &bl, &page_table};
     return launch_kernel(k, dim3(static_cast<unsigned>(blocks)), dim3(kBlockThreads), args, 0, s, ev);
 }
 
@@ -482,7 +487,7 @@ hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t s) 
 }
 
 hipError_t launch_fill_synthetic(const SynthArgs& a, hipStream_t s) {
-    const int64_t groups = a.page_bytes / 16 * a.num_pages;
+    const int64_t groups = a.slice_bytes * a.num_layers / 16 * a.num_pages;
     if (groups <= 0) return hipSuccess;
     hipLaunchKernelGGL(fill_synthetic_kernel, dim3(grid_for(groups, 16384)), dim3(kBlockThreads), 0, s, a);
     return hipGetLastError();

@@ -110,6 +110,8 @@ _SIGS = {
     "paged_decode_workspace_bytes": (_SZ, [_P, _I32, _I32]),
     "paged_decode_attention": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _I32, _I32,
                                               ctypes.c_float, _P, _P, _SZ, _P]),
+    "paged_decode_attention_append": (ctypes.c_int, [_P, _I32, _P, _P, _P, _P, _I64, _P, _I32, _I32,
+                                                     ctypes.c_float, _P, _P, _SZ, _P]),
     "paged_decode_attention_noalloc": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _I32, _I32,
                                                       ctypes.c_float, _P, _P]),
     "paged_decode_partition": (ctypes.c_int, [_P, _P, _I32, _I32, _P, _P]),
@@ -373,6 +375,16 @@ def paged_decode_attention(pool: int, layer: int, q_ptr: int, page_table_ptr: in
                                        seq_lens_ptr or None, batch, num_q_heads, scale,
                                        out_ptr or None, workspace_ptr or None, ws_bytes,
                                        stream or None), "paged_decode_attention")
+
+
+def paged_decode_attention_append(pool: int, layer: int, q_ptr: int, k_new_ptr: int, v_new_ptr: int,
+                                  page_table_ptr: int, pt_stride: int, seq_lens_ptr: int, batch: int,
+                                  num_q_heads: int, scale: float, out_ptr: int, workspace_ptr: int, ws_bytes: int,
+                                  stream: int = 0) -> None:
+    _check(_lib.paged_decode_attention_append(pool, layer, q_ptr or None, k_new_ptr or None, v_new_ptr or None,
+                                              page_table_ptr or None, pt_stride, seq_lens_ptr or None, batch,
+                                              num_q_heads, scale, out_ptr or None, workspace_ptr or None,
+                                              ws_bytes, stream or None), "paged_decode_attention_append")
 
 
 KV_DECODE_SCRATCH_BYTES = 32 << 20

@@ -53,6 +53,27 @@ class HotColdPool:
                                         self.page_table.data_ptr(), _stream(stream))
         self._ws = {}   # decode workspace per stream: decodes on different streams may overlap
 
+    # -- layout ------------------------------------------------------------
+    @property
+    def slice_bytes(self) -> int:
+        """Bytes of one layer of one page: [kv_head][K tile, V tile]."""
+        return self.page_bytes // self.num_layers
+
+    def hot_pages(self) -> torch.Tensor:
+        """The hot pool as [num_hot_pages][num_layers][slice_bytes], a view in page
+        order.  The hot pool is layer-major: the slice of page p for layer l sits at
+        byte (l * num_hot_pages + p) * slice_bytes."""
+        return self.hot.view(self.num_layers, max(self.num_hot_pages, 1), self.slice_bytes).transpose(0, 1)
+
+    def hot_page_bytes(self, ids=None) -> torch.Tensor:
+        """Hot pages (all, or the ids given) as [n][page_bytes] in the cold pool's
+        page-major order (a copy): what the same pages hold, byte for byte, once
+        copied to the cold tier."""
+        v = self.hot_pages()
+        if ids is not None:
+            v = v[torch.as_tensor(ids, dtype=torch.long, device=self.device).reshape(-1)]
+        return v.reshape(v.shape[0], self.page_bytes)
+
     # -- lifetime ----------------------------------------------------------
     def close(self) -> None:
         if getattr(self, "handle", None):
@@ -173,7 +194,10 @@ class HotColdPool:
 
     def decode(self, layer: int, q: torch.Tensor, seq_lens: torch.Tensor,
                page_table: Optional[torch.Tensor] = None, scale: Optional[float] = None,
-               out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+               out: Optional[torch.Tensor] = None, stream=None, k_new: Optional[torch.Tensor] = None,
+               v_new: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """Decode attention of one layer; with k_new / v_new ([B][kv_heads][head_dim]) each
+        row's token seq_lens[b] - 1 is appended first, in the same launch."""
         pt = self.page_table if page_table is None else page_table
         assert q.is_contiguous() and q.dtype == self.torch_dtype and q.dim() == 3
         assert pt.dtype == torch.int32 and pt.is_contiguous() and seq_lens.dtype == torch.int32
@@ -181,9 +205,17 @@ class HotColdPool:
         if out is None:
             out = torch.empty_like(q)
         ws = self.workspace(B, Hq, stream)
-        kv.paged_decode_attention(self.handle, layer, q.data_ptr(), pt.data_ptr(), pt.shape[1],
-                                  seq_lens.data_ptr(), B, Hq, float(scale if scale is not None else D ** -0.5),
-                                  out.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream))
+        s = float(scale if scale is not None else D ** -0.5)
+        if k_new is None:
+            kv.paged_decode_attention(self.handle, layer, q.data_ptr(), pt.data_ptr(), pt.shape[1],
+                                      seq_lens.data_ptr(), B, Hq, s, out.data_ptr(), ws.data_ptr(), ws.numel(),
+                                      _stream(stream))
+        else:
+            assert k_new.is_contiguous() and v_new.is_contiguous() and k_new.shape == v_new.shape
+            assert k_new.shape == (B, self.num_kv_heads, D) and k_new.dtype == self.torch_dtype
+            kv.paged_decode_attention_append(self.handle, layer, q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(),
+                                             pt.data_ptr(), pt.shape[1], seq_lens.data_ptr(), B, Hq, s,
+                                             out.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream))
         return out
 
     def gather_table(self, sids: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:

@@ -81,7 +81,12 @@ def _fake_result():
                                                        for m in ("direct", "prefetch")] * 2},
         "configs": {n: {"us_per_call": {"median": 1.0, "p10": 1.0, "p90": 1.0}, "GBps": 1.0, "pct_of_peak": 1.0,
                         "workload": "w" * 40} for n in ("tiny", "step48", "skewed")}
-        | {"graph_step48": [row] * 6, "append": {"sessions": 32, "batched_append": row},
+        | {"graph_step48": [row] * 6,
+           "append": {"sessions": 32, "batched_append": {"ms_per_step": 0.7, **row}, "per_session_write": row,
+                      "prompt_write": {"ms": 0.37, "GBps_read_write": 4300.0, **row},
+                      "prompt_write_one_call": {"ms": 0.28, "GBps_read_write": 5700.0, **row},
+                      "graph_step": {"step_ms": {"a": 1.0, "b": 0.9}, "append_ms_per_step_in_graph": 0.05,
+                                     "config": "c" * 100}},
            "context": row},
     }
 
@@ -96,3 +101,4 @@ def test_stdout_line_stays_short_and_keeps_the_headline_fields():
     assert out["resume48"]["ms_per_session"] == 2.5
     assert out["configs"]["step48"]["GBps"] == 1.0
     assert len(out["spill_decode_step_ms"]) == 16
+    assert out["configs"]["append"]["graph_append_ms_per_step"] == 0.05

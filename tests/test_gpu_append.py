@@ -63,7 +63,7 @@ def test_decode_step_appends_match_packer(dev, dtype, D):
     for b, L in enumerate(lens):
         pages = np.array(pool.info(sids[b])[2], np.int32)
         oracle.pack_pool(want, NL, hkv, D, ORACLE_DTYPE[dtype], layer, pages, *kv_rows[b])
-    assert np.array_equal(pool.hot.cpu().numpy(), want)
+    assert np.array_equal(pool.hot_page_bytes().cpu().numpy().reshape(-1), want)
     pool.close()
 
 
@@ -88,7 +88,7 @@ def test_appends_into_spilled_pages(dev, cold):
     _append_all(pool, dev, dtype, layer, sids, lens, kv_rows)
     torch.cuda.synchronize()
     pb = pool.page_bytes
-    hot = pool.hot.view(-1, pb).cpu().numpy()
+    hot = pool.hot_page_bytes().cpu().numpy()
     cold_img = pool.cold.view(-1, pb).cpu().numpy()
     spilled = 0
     for b, L in enumerate(lens):
@@ -125,7 +125,7 @@ def test_long_lists_through_a_staging_slot(dev):
     torch.cuda.synchronize()
     want = np.zeros(pool.hot.numel(), np.uint8)
     oracle.pack_pool(want, NL, hkv, D, ORACLE_DTYPE[dtype], layer, np.array(pool.info(sid)[2], np.int32), k, v)
-    assert np.array_equal(pool.hot.cpu().numpy(), want)
+    assert np.array_equal(pool.hot_page_bytes().cpu().numpy().reshape(-1), want)
     pool.close()
 
 

@@ -70,7 +70,7 @@ def test_write_tokens_layers_matches_packer_and_per_layer_writes(dev, dtype, D):
     kk[:, t0:t1], vv[:, t0:t1] = k[:, t0:t1], v[:, t0:t1]
     for l in range(l0, l0 + nl):
         oracle.pack_pool(want, NL, hkv, D, ORACLE_DTYPE[dtype], l, np.array(pages, np.int32), kk[l], vv[l])
-    got = [p.hot.cpu().numpy() for p in pools]
+    got = [p.hot_page_bytes().cpu().numpy().reshape(-1) for p in pools]
     assert np.array_equal(got[0], got[1])
     assert np.array_equal(got[0], want)
     from paper_2609_25782_amd import hotcold_kv as kv
@@ -126,7 +126,7 @@ def test_append_table_matches_packer_and_decodes(dev, cold):
                              kvs[b][0][l], kvs[b][1][l])
         img = img.reshape(-1, pb)
         for i, (h, c) in enumerate(zip(hot_ids, cold_ids)):
-            src = pool.hot.view(-1, pb)[h] if h >= 0 else pool.cold.view(-1, pb)[c]
+            src = pool.hot_page_bytes([h])[0] if h >= 0 else pool.cold.view(-1, pb)[c]
             got = src.cpu().numpy()
             # the tail page's slots past L were never written: compare the written tokens only
             mask = _token_mask(NL, hkv, D, pb, min(16, L - 16 * i))
@@ -161,7 +161,7 @@ def test_append_table_skips_entries_naming_no_page(dev):
     pool.append_tokens_table(0, table, rows, pos, k, k.clone())
     torch.cuda.synchronize()
     pb = pool.page_bytes
-    hot = pool.hot.view(-1, pb).cpu().numpy()
+    hot = pool.hot_page_bytes().cpu().numpy()
     changed = sorted(set(np.flatnonzero(hot.any(axis=1)).tolist()))
     assert changed == [2, 5]
     assert not pool.cold.cpu().numpy().any()
@@ -211,9 +211,11 @@ def test_extension_keeps_write_on_evict_exact_for_device_appends(dev):
     pool.close()
 
 
-def test_serving_step_graph_matches_eager_steps(dev):
+@pytest.mark.parametrize("append", ["table", "fused"])
+def test_serving_step_graph_matches_eager_steps(dev, append):
     """One captured graph per step shape: gather the batch table, then for each
-    of 4 layers append the step's token (resolved on the device) and decode.
+    of 4 layers append the step's token (resolved on the device: a separate
+    launch through the table, or fused into the decode launch) and decode.
     Replayed for 40 steps with the host's extensions and the new tokens' values
     written in place between replays; the same steps done eagerly (host-
     resolved appends) on a second pool give bitwise equal outputs and pages,
@@ -262,8 +264,13 @@ def test_serving_step_graph_matches_eager_steps(dev):
             def graph_step():
                 pools[0].gather_table(sid_t, out=table, stream=s)
                 for l in range(NL):
-                    pools[0].append_tokens_table(l, table, rows_t, pos_t, k_new[l:l + 1], v_new[l:l + 1], stream=s)
-                    pools[0].decode(l, qs[l], sl_t, page_table=table, out=outs[l], stream=s)
+                    if append == "table":
+                        pools[0].append_tokens_table(l, table, rows_t, pos_t, k_new[l:l + 1], v_new[l:l + 1],
+                                                     stream=s)
+                        pools[0].decode(l, qs[l], sl_t, page_table=table, out=outs[l], stream=s)
+                    else:
+                        pools[0].decode(l, qs[l], sl_t, page_table=table, out=outs[l], stream=s,
+                                        k_new=k_new[l], v_new=v_new[l])
 
             if g is None:
                 graph_step()                             # eager once: workspace allocated before capture
@@ -284,5 +291,116 @@ def test_serving_step_graph_matches_eager_steps(dev):
     assert torch.equal(pools[0].hot, pools[1].hot)
     for l in range(NL):
         tolerance_check(to_host(outs[l]), cases[l].oracle_out())
+    for p in pools:
+        p.close()
+
+
+@pytest.mark.parametrize("dtype,D,hq,hkv,waves,vector", [
+    ("bf16", 128, 32, 4, None, False), ("bf16", 128, 32, 4, 5, False), ("bf16", 64, 8, 2, None, False),
+    ("f32", 64, 8, 2, None, False), ("f32", 128, 16, 1, 7, False), ("bf16", 128, 32, 4, None, True),
+    ("bf16", 64, 16, 2, 3, True)])
+def test_fused_append_equals_append_then_decode(dev, dtype, D, hq, hkv, waves, vector):
+    """paged_decode_attention_append against kv_append_tokens followed by
+    paged_decode_attention on a twin pool: bitwise equal outputs and pages, for
+    tails in a fresh page (L - 1 = 16 k), mid-page and at a page end, rows of
+    length 0 (nothing appended) and 1, both work-split shapes (workers of four
+    waves, and of one), and both forms of the split kernel.  Unwritten slots
+    hold NaN, so a token the decode did not see written would show.  The last
+    step also matches the oracle."""
+    from paper_2609_25782_amd.pool import HotColdPool
+    NL, layer = 2, 1
+    L0 = [0, 15, 16, 17, 31, 100, 1, 250]
+    final = [L + 2 if L > 0 else 0 for L in L0]          # two fused steps
+    B = len(L0)
+    stride = max(synth.pages_for(L) for L in final) + 1
+    n_pages = sum(synth.pages_for(L) for L in final) + 5
+    pools = [HotColdPool(NL, hkv, D, dtype, n_pages, 0, B, stride) for _ in range(2)]
+    kvs = [synth.session_kv(SEED, b, L, layer, hkv, D, 1.0, dtype) for b, L in enumerate(final)]
+    perm = np.random.default_rng(SEED + 1).permutation(n_pages)
+    for p in pools:
+        if dtype == "bf16":
+            p.hot.view(torch.int16).fill_(0x7FC0)
+        else:
+            p.hot.view(torch.float32).fill_(float("nan"))
+        p.set_compute(vector)
+        if waves:
+            p.set_waves(waves)
+        off = 0
+        for b, L in enumerate(L0):
+            n = synth.pages_for(final[b])
+            # pages for the final length up front: placement as a random permutation
+            assert p.create_session(16 * n, [int(x) for x in perm[off:off + n]]) == b
+            off += n
+            if L:
+                p.write_tokens(b, layer, 0, to_device(kvs[b][0][:L], dtype, dev), to_device(kvs[b][1][:L], dtype, dev))
+    case = Case(NL, hq, hkv, D, dtype, final, seed=SEED, layer=layer)
+    q = to_device(case.q, dtype, dev)
+    for step in (1, 2):
+        lens = [L + step if L > 0 else 0 for L in L0]
+        sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+        rows = [b for b in range(B) if lens[b] > 0]
+        kn = np.zeros((B, hkv, D), kvs[0][0].dtype)
+        vn = np.zeros((B, hkv, D), kvs[0][0].dtype)
+        for b in rows:
+            kn[b], vn[b] = kvs[b][0][lens[b] - 1], kvs[b][1][lens[b] - 1]
+        kn_t, vn_t = to_device(kn, dtype, dev), to_device(vn, dtype, dev)
+        fused = pools[0].decode(layer, q, sl, page_table=pools[0].page_table[:B], k_new=kn_t, v_new=vn_t).clone()
+        pools[1].append_tokens(layer, rows, [lens[b] - 1 for b in rows], kn_t[rows].contiguous(),
+                               vn_t[rows].contiguous())
+        sep = pools[1].decode(layer, q, sl, page_table=pools[1].page_table[:B]).clone()
+        torch.cuda.synchronize()
+        assert torch.equal(fused, sep), "step %d" % step
+        assert torch.isfinite(fused.float()).all()
+    assert torch.equal(pools[0].hot.view(torch.int16), pools[1].hot.view(torch.int16))
+    tolerance_check(to_host(fused), case.oracle_out(), max_norm=1e-2 if dtype == "bf16" else 1e-5)
+    for p in pools:
+        p.close()
+
+
+@pytest.mark.parametrize("cold", ["device", "host"])
+def test_fused_append_into_spilled_tail_pages(dev, cold):
+    """With spill on, tail pages in the cold tier receive the fused append in
+    place; the outputs equal the separate append's, and a layer decoded through
+    staging refuses the fused append."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import HotColdPool
+    NL, hkv, D, hq, dtype = 2, 2, 128, 16, "bf16"
+    L0 = [40, 17, 90, 5]
+    B = len(L0)
+    need = sum(synth.pages_for(L + 1) for L in L0)
+    pools = [HotColdPool(NL, hkv, D, dtype, need // 2, need + 4, B, 8, cold_location=cold) for _ in range(2)]
+    kvs = [synth.session_kv(SEED, b, L + 1, 0, hkv, D, 1.0, dtype) for b, L in enumerate(L0)]
+    for p in pools:
+        p.set_spill(True)
+        for b, L in enumerate(L0):
+            assert p.create_session(L) == b
+            p.write_tokens(b, 0, 0, to_device(kvs[b][0][:L], dtype, dev), to_device(kvs[b][1][:L], dtype, dev))
+            p.extend(b, L + 1)
+    assert pools[0].stats()["cold_active_pages"] > 0
+    sids = torch.arange(B, dtype=torch.int32, device=dev)
+    tables = [p.gather_table(sids) for p in pools]
+    lens = [L + 1 for L in L0]
+    sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+    case = Case(NL, hq, hkv, D, dtype, lens, seed=SEED, layer=0)
+    q = to_device(case.q, dtype, dev)
+    kn = to_device(np.stack([kvs[b][0][L] for b, L in enumerate(L0)]), dtype, dev)
+    vn = to_device(np.stack([kvs[b][1][L] for b, L in enumerate(L0)]), dtype, dev)
+    fused = pools[0].decode(0, q, sl, page_table=tables[0], k_new=kn, v_new=vn).clone()
+    pools[1].append_tokens(0, list(range(B)), L0, kn, vn)
+    sep = pools[1].decode(0, q, sl, page_table=tables[1]).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(fused, sep)
+    tolerance_check(to_host(fused), case.oracle_out())
+    # staging: the fused append is refused for a staged layer
+    staging = torch.empty(2 * 16 * pools[0].slice_bytes, dtype=torch.uint8, device=dev)
+    kv.kv_pool_set_staging(pools[0].handle, staging.data_ptr(), staging.numel())
+    table = torch.empty((B, pools[0].stride), dtype=torch.int32, device=dev)
+    assert kv.paged_decode_stage(pools[0].handle, list(range(B)), table.data_ptr()) > 0
+    kv.paged_decode_prefetch(pools[0].handle, 0)
+    with pytest.raises(kv.KVError) as e:
+        pools[0].decode(0, q, sl, page_table=table, k_new=kn, v_new=vn)
+    assert e.value.status == kv.KV_ERR_INVALID
+    torch.cuda.synchronize()
+    kv.kv_pool_set_staging(pools[0].handle, 0, 0)
     for p in pools:
         p.close()

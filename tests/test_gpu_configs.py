@@ -104,7 +104,7 @@ def test_layer_config_full_size(dev):
     used = np.zeros(num_hot, bool)
     used[np.concatenate(w.placement)] = True
     free = torch.from_numpy(np.flatnonzero(~used)).to(dev)
-    pool.hot.view(num_hot, -1).view(torch.int16).index_fill_(0, free, 0x7FC0)
+    pool.hot_pages().view(torch.int16).index_fill_(0, free, 0x7FC0)
     dirty = pool.decode(0, q, sl, page_table=pt).clone()
     torch.cuda.synchronize()
     assert torch.equal(dirty, clean)
@@ -224,13 +224,12 @@ def test_resume_mix_config_full_size(dev):
     want_rows = np.array([model.row(s) for s in chosen], dtype=np.int32)
     assert np.array_equal(got_rows, want_rows)
     pb = pool.page_bytes
-    hot = pool.hot.view(-1, pb)
     total = 0
     for per in copies:
         src = torch.tensor([c for c, _ in per], dtype=torch.long, device=dev)
         dst = torch.tensor([h for _, h in per], dtype=torch.long, device=dev)
         for i in range(0, len(per), 512):
-            assert torch.equal(hot.index_select(0, dst[i:i + 512]), view.index_select(0, src[i:i + 512]))
+            assert torch.equal(pool.hot_page_bytes(dst[i:i + 512]), view.index_select(0, src[i:i + 512]))
         total += len(per)
     _say("resumed %d pages (%.1f GiB), all bit-exact" % (total, total * pb / 2 ** 30))
     # the active sessions were not touched: all 32 decode at layer 10 as the oracle says

@@ -31,7 +31,7 @@ def test_fill_synthetic_matches_generator(dev, dtype, D, NL, hkv):
     mult = float(synth.value_multiplier(0.7))
     pool.fill_synthetic(sid, 5, 1234, mult)
     torch.cuda.synchronize()
-    got = pool.hot.cpu().numpy()
+    got = pool.hot_page_bytes().cpu().numpy().reshape(-1)
     od = ORACLE_DTYPE[dtype]
     want = np.zeros_like(got)
     n_tok = 16 * len(pages)  # the fill writes every slot of every page
@@ -58,7 +58,7 @@ def test_write_tokens_matches_packer(dev, dtype):
     torch.cuda.synchronize()
     want = np.zeros(pool.hot.numel(), np.uint8)
     oracle.pack_pool(want, NL, hkv, D, ORACLE_DTYPE[dtype], 1, np.array([4, 1, 5, 0]), k, v)
-    assert np.array_equal(pool.hot.cpu().numpy(), want)
+    assert np.array_equal(pool.hot_page_bytes().cpu().numpy().reshape(-1), want)
     pool.close()
 
 
@@ -73,7 +73,7 @@ def test_decode_reads_oracle_packed_pool(dev):
     for b in range(case.batch):
         k, v = case.kv[b]
         oracle.pack_pool(host, 2, 2, 128, oracle.BF16, 1, case.placement[b], k, v)
-    pool.hot.copy_(torch.from_numpy(host).to(dev))
+    pool.hot_pages().copy_(torch.from_numpy(host).to(dev).view(pool.num_hot_pages, pool.num_layers, -1))
     for b, L in enumerate(case.seq_lens):
         pool.create_session(L, [int(p) for p in case.placement[b]])
     q = to_device(case.q, "bf16", dev)

@@ -33,6 +33,12 @@ def _pages(t: torch.Tensor, page_bytes: int, ids) -> np.ndarray:
         np.zeros((0, page_bytes), np.uint8)
 
 
+def _hot_pages(pool, ids) -> np.ndarray:
+    """Host copy of the given hot pages in page order (the hot pool is layer-major)."""
+    return pool.hot_page_bytes([int(i) for i in ids]).cpu().numpy() if len(ids) else \
+        np.zeros((0, pool.page_bytes), np.uint8)
+
+
 def _random_fill(pool, seed):
     g = torch.Generator(device=pool.device)
     g.manual_seed(seed)
@@ -78,7 +84,7 @@ def test_tiny_resume_config(dev, cold):
     for per in copies:
         src = [c for c, _ in per]
         dst = [h for _, h in per]
-        assert np.array_equal(_pages(pool.hot, pb, dst), _pages(cold_before, pb, src))
+        assert np.array_equal(_hot_pages(pool, dst), _pages(cold_before, pb, src))
     assert torch.equal(pool.cold, cold_before)  # resume never writes the cold tier
     st = pool.stats()
     assert st["pages_to_hot"] == 32 and st["resumes"] == 2
@@ -173,7 +179,7 @@ def test_aliased_cold_pages_resume(dev):
     _check_table(pool, model)
     pb = pool.page_bytes
     for per in copies:
-        assert np.array_equal(_pages(pool.hot, pb, [h for _, h in per]),
+        assert np.array_equal(_hot_pages(pool, [h for _, h in per]),
                               _pages(cold_before, pb, [c for c, _ in per]))
     pool.close()
 
@@ -194,7 +200,7 @@ def test_random_sequences_match_model(dev, cold, host_kernel):
     _random_fill(pool, 3)
     torch.cuda.synchronize()
     # expected content of every hot and cold page, tracked through the copies
-    hot_img = pool.hot.view(nh, -1).cpu().numpy().copy()
+    hot_img = pool.hot_page_bytes().cpu().numpy().copy()
     cold_img = pool.cold.view(nc, -1).cpu().numpy().copy()
     rng = np.random.default_rng(4)
 
@@ -316,7 +322,7 @@ def test_random_sequences_match_model(dev, cold, host_kernel):
             assert st["lru_evicted_pages"] == model.lru_evicted
             assert (st["resume_pages_resident"], st["resume_pages_total"]) == (model.resume_resident,
                                                                                model.resume_total)
-            gpu_hot = pool.hot.view(nh, -1).cpu().numpy()
+            gpu_hot = pool.hot_page_bytes().cpu().numpy()
             gpu_cold = pool.cold.view(nc, -1).cpu().numpy()
             for s in model.sessions:
                 for p in s.hot:
@@ -347,7 +353,7 @@ def test_resume_48_layer_pages(dev):
     st0, L0, hot0, cold0 = pool.info(0)
     pb = pool.page_bytes
     for i in (0, 1, len(hot0) - 1, 150):
-        assert torch.equal(pool.hot.view(-1, pb)[hot0[i]], pool.cold.view(-1, pb)[cold0[i]])
+        assert torch.equal(pool.hot_page_bytes([hot0[i]])[0], pool.cold.view(-1, pb)[cold0[i]])
     # decode layer 31 of both sessions against the oracle on regenerated KV
     from helpers import Case
     case = Case(48, 32, 4, 128, "bf16", lens, seed=77, layer=31,
@@ -419,7 +425,7 @@ def test_copy_lists_larger_than_one_staging_slot(dev):
         st, L, hot, cold = pool.info(sid)
         h = torch.tensor(hot, dtype=torch.long, device=dev)
         c = torch.tensor(cold, dtype=torch.long, device=dev)
-        assert torch.equal(pool.hot.view(-1, pb).index_select(0, h), pool.cold.view(-1, pb).index_select(0, c))
+        assert torch.equal(pool.hot_page_bytes(h), pool.cold.view(-1, pb).index_select(0, c))
     pool.close()
 
 
@@ -448,7 +454,6 @@ def test_copy_launch_shapes_and_budget(dev):
     for n, cold in zip((fine, coarse), lists):
         assert pool.import_cold(16 * n, cold) == model.import_cold(16 * n, cold)
     pb = pool.page_bytes
-    hot = pool.hot.view(-1, pb)
 
     def resume_and_check(sid, what):
         pool.resume([sid])
@@ -459,7 +464,7 @@ def test_copy_launch_shapes_and_budget(dev):
         idx = sorted(set([0, len(h) - 1] + [int(x) for x in rng.choice(len(h), size=300, replace=False)]))
         hh = torch.tensor([h[i] for i in idx], dtype=torch.long, device=dev)
         cc = torch.tensor([c[i] for i in idx], dtype=torch.long, device=dev)
-        assert torch.equal(hot.index_select(0, hh), view.index_select(0, cc))
+        assert torch.equal(pool.hot_page_bytes(hh), view.index_select(0, cc))
         _say("%s: %d pages resumed, %d copied, %d sampled pages bit-exact" % (what, len(h), copied, len(idx)))
         return copied
 
@@ -493,7 +498,7 @@ def test_frees_on_alternating_streams_are_all_waited_for(dev):
     hot_big = pool.info(big)[2]
     torch.cuda.synchronize()
     idx = torch.tensor(hot_big, dtype=torch.long, device=dev)
-    before = pool.hot.view(-1, pb).index_select(0, idx)
+    before = pool.hot_page_bytes(idx)
     sa, sb, sc = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
     torch.cuda.synchronize()
     _say("evict %d pages of %d KiB on stream A, destroy on B, refill on C" % (n, pb // 1024))

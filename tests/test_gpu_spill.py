@@ -60,7 +60,7 @@ def test_spill_sequences_match_model(dev, cold, host_kernel):
     model = PoolModel(nh, nc, ms, stride, spill=True)
     _random_fill(pool, 5)
     torch.cuda.synchronize()
-    hot_img = pool.hot.view(nh, -1).cpu().numpy().copy()
+    hot_img = pool.hot_page_bytes().cpu().numpy().copy()
     cold_img = pool.cold.view(nc, -1).cpu().numpy().copy()
     rng = np.random.default_rng(6)
 
@@ -128,7 +128,7 @@ def test_spill_sequences_match_model(dev, cold, host_kernel):
     assert st["spilled_pages"] == model.spilled_pages > 10
     assert st["promoted_pages"] == model.promoted_pages > 3
     assert np.any((got >= 0) & ((got & COLD_BIT) != 0))
-    hot_now = pool.hot.view(nh, -1).cpu().numpy()
+    hot_now = pool.hot_page_bytes().cpu().numpy()
     cold_now = pool.cold.view(nc, -1).cpu().numpy()
     for s in model.sessions:
         for h, c in zip(s.hot, s.cold):
@@ -276,7 +276,7 @@ def test_promote_and_write_into_spilled_pages(dev):
     pb = pool.page_bytes
     for h, c in zip(hot1, cold1):
         if h >= 0 and c >= 0:
-            assert torch.equal(pool.hot.view(-1, pb)[h], pool.cold.view(-1, pb)[c])
+            assert torch.equal(pool.hot_page_bytes([h])[0], pool.cold.view(-1, pb)[c])
     pool.resume(0)                        # nothing free or evictable: stays in the cold tier
     assert all(h < 0 for h in pool.info(0)[2])
     check()
@@ -339,7 +339,7 @@ def test_lazy_resume_decodes_in_place_then_promotes(dev, cold):
     for sid in range(3):
         _, _, hot, cold_ids = pool.info(sid)
         for h, c in zip(hot, cold_ids):
-            assert torch.equal(pool.hot.view(-1, pb)[h].cpu(), pool.cold.view(-1, pb)[c].cpu())
+            assert torch.equal(pool.hot_page_bytes([h])[0].cpu(), pool.cold.view(-1, pb)[c].cpu())
     pool.close()
 
 
