@@ -871,8 +871,26 @@ def measure_append(seed: int, steps: int = 20, warmup: int = 3):
         out[name] = {"ms_per_step": round(e0.elapsed_time(e1) / steps, 4),
                      "host_ms_per_step": round(1e3 * host / steps, 4),
                      "calls_per_step": NL if batched else NL * B}
-    # a prompt of 8,192 tokens into one session, every layer: one call per layer,
-    # and one call for all 48 (kv_write_tokens_layers)
+    pool.close()
+    torch.cuda.empty_cache()
+    out.update(measure_prompt_write(seed))
+    out["graph_step"] = measure_graph_append(seed)
+    return out
+
+
+def measure_prompt_write(seed: int, reps: int = 7):
+    """Fresh KV of a whole prompt (data path 3): 8,192 tokens into one session
+    at the paper's shape (48 layers, 4 KV heads, 128, bf16), one
+    kv_write_tokens call per layer, and one kv_write_tokens_layers call for all
+    48.  Algorithmic bytes: the K and V written, and the same again read."""
+    import torch
+    from paper_2609_25782_amd.pool import HotColdPool
+    NL, prompt = 48, 8192
+    pool = HotColdPool(NL, 4, 128, "bf16", prompt // 16 + 2, 0, 1, prompt // 16 + 1)
+    dev = pool.device
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    out = {}
     sid = pool.create_session(prompt)
     kp = torch.randn((NL, prompt, 4, 128), generator=g, device=dev).to(torch.bfloat16)
     vp = torch.randn((NL, prompt, 4, 128), generator=g, device=dev).to(torch.bfloat16)
@@ -890,7 +908,7 @@ def measure_append(seed: int, steps: int = 20, warmup: int = 3):
             fn()
         torch.cuda.synchronize()
         times = []
-        for _ in range(7):
+        for _ in range(reps):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
             fn()
@@ -906,7 +924,6 @@ def measure_append(seed: int, steps: int = 20, warmup: int = 3):
     pool.close()
     del kp, vp
     torch.cuda.empty_cache()
-    out["graph_step"] = measure_graph_append(seed)
     return out
 
 
@@ -1193,7 +1210,7 @@ def main():
                     help="write a scratch buffer of this many MiB before every timed step, so the "
                          "decode starts with the 256 MB Infinity Cache and the L2s holding other data")
     ap.add_argument("--full-json", default="", help="also write the full result (every sweep row) here")
-    ap.add_argument("--only-config", default="", choices=["", "tiny", "step48", "skewed"],
+    ap.add_argument("--only-config", default="", choices=["", "tiny", "step48", "skewed", "prompt_write"],
                     help="profiling aid: time only this workload's decode (no hot-path step) and print "
                          "its figures")
     args = ap.parse_args()
@@ -1215,6 +1232,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda", 0)
+    if args.only_config == "prompt_write":
+        print(json.dumps(measure_prompt_write(args.seed, reps=args.steps)), flush=True)
+        return
     if args.only_config:
         print(json.dumps(measure_configs(args.seed, steps=args.steps, warmup=args.warmup,
                                          only=[args.only_config])), flush=True)

@@ -262,6 +262,23 @@ __device__ __forceinline__ void write_token_group(char* lh, int64_t tile, int sl
     }
 }
 
+// Fresh KV is read once from its source and not read again until a later
+// decode step, long after it has left the caches: its 16-byte loads and stores
+// are nontemporal by default (HCK_WRITE_NONTEMPORAL).
+#ifndef HCK_WRITE_NONTEMPORAL
+#define HCK_WRITE_NONTEMPORAL 1
+#endif
+__device__ __forceinline__ u32x4 stream_load(const u32x4* p) {
+    if (HCK_WRITE_NONTEMPORAL) return __builtin_nontemporal_load(p);
+    return *p;
+}
+__device__ __forceinline__ void stream_store(u32x4* p, const u32x4& v) {
+    if (HCK_WRITE_NONTEMPORAL)
+        __builtin_nontemporal_store(v, p);
+    else
+        *p = v;
+}
+
 // Tokens [tok_begin, tok_begin + n_tok) of layers [layer, layer + num_layers):
 // one block per (page, KV head, layer).  The page's tokens in the range are
 // read from the source rows ([layer][token][kv_head][head_dim], each token's
@@ -293,8 +310,10 @@ __global__ __launch_bounds__(kBlockThreads) void write_tokens_kernel(WriteArgs a
         if (t < s0 || t >= s1) continue;
         const int64_t src =
             layer_src + (static_cast<int64_t>(t_base + t - a.tok_begin) * a.num_kv_heads + head) * D + cd * x;
-        *reinterpret_cast<u32x4*>(&s_k[t][cd * x]) = *reinterpret_cast<const u32x4*>(static_cast<const T*>(a.k) + src);
-        *reinterpret_cast<u32x4*>(&s_v[t][cd * x]) = *reinterpret_cast<const u32x4*>(static_cast<const T*>(a.v) + src);
+        *reinterpret_cast<u32x4*>(&s_k[t][cd * x]) =
+            stream_load(reinterpret_cast<const u32x4*>(static_cast<const T*>(a.k) + src));
+        *reinterpret_cast<u32x4*>(&s_v[t][cd * x]) =
+            stream_load(reinterpret_cast<const u32x4*>(static_cast<const T*>(a.v) + src));
     }
     __syncthreads();
     char* lh = entry_slice(a.hot, a.cold, a.row[page], layer) + static_cast<int64_t>(head) * 2 * tile;
@@ -302,8 +321,8 @@ __global__ __launch_bounds__(kBlockThreads) void write_tokens_kernel(WriteArgs a
     for (int e = tid; e < groups * kPageTokens; e += kBlockThreads) {
         const int cd = e / kPageTokens, t = e % kPageTokens;
         if (t < s0 || t >= s1) continue;
-        *reinterpret_cast<u32x4*>(lh + (static_cast<int64_t>(cd) * kPageTokens + t) * 16) =
-            *reinterpret_cast<const u32x4*>(&s_k[t][cd * x]);
+        stream_store(reinterpret_cast<u32x4*>(lh + (static_cast<int64_t>(cd) * kPageTokens + t) * 16),
+                     *reinterpret_cast<const u32x4*>(&s_k[t][cd * x]));
     }
     // V tile: [dim][token]; one 16-byte store covers x consecutive tokens of a dim
     constexpr int kChunks = kPageTokens / x;
@@ -316,8 +335,8 @@ __global__ __launch_bounds__(kBlockThreads) void write_tokens_kernel(WriteArgs a
             T w[x];
 #pragma unroll
             for (int j = 0; j < x; ++j) w[j] = s_v[t0 + j][d];
-            *reinterpret_cast<u32x4*>(vt + static_cast<int64_t>(d) * kPageTokens + t0) =
-                *reinterpret_cast<const u32x4*>(w);
+            stream_store(reinterpret_cast<u32x4*>(vt + static_cast<int64_t>(d) * kPageTokens + t0),
+                         *reinterpret_cast<const u32x4*>(w));
         } else {
             for (int j = 0; j < x; ++j)
                 if (t0 + j >= s0 && t0 + j < s1) vt[static_cast<int64_t>(d) * kPageTokens + t0 + j] = s_v[t0 + j][d];
