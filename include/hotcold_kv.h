@@ -567,6 +567,14 @@ int paged_decode_gather_table(kv_pool* pool, const int32_t* sids, int32_t n, int
  * layer l + 1 of the batch's spilled pages are gathered from the cold tier into
  * HBM, and layer l + 1 then reads only HBM.
  *
+ * Whether staging pays depends on the cold tier: over device memory it only
+ * adds an HBM write and read per spilled byte, and over PCIe reading spilled
+ * pages in place (spill on, no staging) measured faster at every spilled share
+ * tried (0.25-100% of a 48-layer step's pages), because in-kernel reads overlap
+ * PCIe with the other waves' HBM reads while staging adds a launch and a
+ * cross-stream wait per layer.  It is for capacity tiers whose access latency
+ * a layer's decode can hide and in-kernel reads cannot.
+ *
  * kv_pool_set_staging gives the pool a device buffer for this (256-byte
  * aligned; NULL or 0 bytes removes it).  It holds two halves (even and odd
  * layers) of `slots` slots each, a slot being one layer of one page:
