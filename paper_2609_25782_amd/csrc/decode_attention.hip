@@ -263,6 +263,38 @@ __device__ __forceinline__ void compute_page(SegmentState<D, BF16>& st, PageRegs
     }
 }
 
+// Fused merge: the split's partials cross between XCDs as device-scope
+// stores and loads (cache-policy bit SC1 on gfx950).  The L2 of each XCD
+// writes such stores through and does not serve such loads from its own
+// lines, so neither the arrival nor the merge needs a whole-L2 write-back
+// or invalidate.
+constexpr int kScopeDevice = 16;  // SC1: device-scope coherence
+
+// The workspace's partials through one buffer resource (offsets from part_o).
+struct PartialsRsrc {
+    __amdgpu_buffer_rsrc_t rs;
+    const char* base;
+    __device__ explicit PartialsRsrc(const DecodeArgs& a) : base(reinterpret_cast<const char*>(a.part_o)) {
+        rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.part_o), static_cast<short>(0), 0x7FFFFFFF,
+                                               kRsrcWord3);
+    }
+    __device__ unsigned off(const float* p) const {
+        return static_cast<unsigned>(reinterpret_cast<const char*>(p) - base);
+    }
+    __device__ void store4(float* p, const f32x4& v) const {
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs, off(p), 0, kScopeDevice);
+    }
+    __device__ void store1(float* p, float v) const {
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rs, off(p), 0, kScopeDevice);
+    }
+    __device__ f32x4 load4(const float* p) const {
+        return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off(p), 0, kScopeDevice));
+    }
+    __device__ float load1(const float* p) const {
+        return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off(p), 0, kScopeDevice));
+    }
+};
+
 __device__ __forceinline__ void lse_merge(float& M, float& den, f32x4& acc, float m2, float l2,
                                           const f32x4& o2) {
     const float Mn = fmaxf(M, m2);
@@ -316,6 +348,7 @@ __device__ void fill_segment(const DecodeArgs& a, int b, int g, float value, int
 template <int D, bool BF16>
 __device__ void combine_segment(const DecodeArgs& a, int b, int g, const SegWaves& sw, int64_t T,
                                 int lane) {
+    const PartialsRsrc pr(a);
     constexpr int kQuads = D / 4;
     constexpr int kMaxItems = (16 * kQuads + kWave - 1) / kWave;
     const int items = a.group * kQuads;
@@ -342,9 +375,10 @@ __device__ void combine_segment(const DecodeArgs& a, int b, int g, const SegWave
             const int idx = it * kWave + lane;
             if (idx < items) {
                 const int h = idx / kQuads, quad = idx % kQuads;
-                mk[it] = pml[h];
-                lk[it] = pml[a.group + h];
-                ok[it] = *reinterpret_cast<const f32x4*>(a.part_o + (slot * a.group + h) * D + 4 * quad);
+                const float* po = a.part_o + (slot * a.group + h) * D + 4 * quad;
+                mk[it] = pr.load1(pml + h);
+                lk[it] = pr.load1(pml + a.group + h);
+                ok[it] = pr.load4(po);
             }
         }
 #pragma unroll
@@ -506,27 +540,38 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
     if (bad) l = __builtin_nanf("");
     if (hvalid) {
         float* po = a.part_o + (static_cast<int64_t>(pc.slot) * a.group + h) * D + 4 * qg;
+        float* pml = a.part_ml + static_cast<int64_t>(pc.slot) * 2 * a.group;
+        if (a.fused) {
+            const PartialsRsrc pr(a);
 #pragma unroll
-        for (int c = 0; c < S::kChunks; ++c) *reinterpret_cast<f32x4*>(po + 16 * c) = st.o[c];
-        if (qg == 0) {
-            float* pml = a.part_ml + static_cast<int64_t>(pc.slot) * 2 * a.group;
-            pml[h] = st.m;
-            pml[a.group + h] = l;
+            for (int c = 0; c < S::kChunks; ++c) pr.store4(po + 16 * c, st.o[c]);
+            if (qg == 0) {
+                pr.store1(pml + h, st.m);
+                pr.store1(pml + a.group + h, l);
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < S::kChunks; ++c) *reinterpret_cast<f32x4*>(po + 16 * c) = st.o[c];
+            if (qg == 0) {
+                pml[h] = st.m;
+                pml[a.group + h] = l;
+            }
         }
     }
     if (a.fused) {
-        // The wave that delivers the last partial of (b, g) merges them all.  The
-        // arrival count is a release (this wave's partial becomes visible to every
-        // XCD: on gfx950 an L2 write-back) and only the merging wave acquires.
+        // The wave that delivers the last partial of (b, g) merges them all.
         const SegWaves sw = seg_waves(seg_first_unit, nb, total_units, a.waves / a.group_waves);
         int32_t* cnt = a.counters + pc.b * a.num_kv_heads + pc.g;
         int prev = 0;
-        if (lane == 0) prev = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        // The partials went out as device-scope stores: once this wave's are
+        // acknowledged they are visible to every XCD, and the merging wave
+        // reads them back with device-scope loads.
+        __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        if (lane == 0) prev = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         prev = __builtin_amdgcn_readfirstlane(__shfl(prev, 0));
         if (prev + 1 == sw.pieces) {
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             combine_segment<D, BF16>(a, pc.b, pc.g, sw, total_units, lane);
-            if (lane == 0) atomicExch(cnt, 0);  // ready for the next call
+            if (lane == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // next call
         }
     }
 }
