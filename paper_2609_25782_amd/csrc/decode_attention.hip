@@ -346,16 +346,22 @@ __device__ void fill_segment(const DecodeArgs& a, int b, int g, float value, int
 }
 
 template <int D, bool BF16>
-__device__ void combine_segment(const DecodeArgs& a, int b, int g, const SegWaves& sw, int64_t T,
+__device__ void combine_segment(const DecodeArgs& a, int b, int g, int64_t u_a, int nb, int64_t T,
                                 int lane) {
     const PartialsRsrc pr(a);
     constexpr int kQuads = D / 4;
     constexpr int kMaxItems = (16 * kQuads + kWave - 1) / kWave;
+    constexpr int kBatch = 4;  // partials whose loads are in flight together
     const int items = a.group * kQuads;
     const int gw = a.group_waves;
     const int64_t sseg = static_cast<int64_t>(b) * (a.num_kv_heads / gw) + g / gw;
     const int w = g % gw;
     const int N = a.waves / gw;
+    // fewer workers than units: workers k_first.. each hold one piece; more:
+    // each unit is a piece, held by the worker that owns it
+    const bool per_unit = N > T;
+    const int k_first = static_cast<int>(((u_a + 1) * N - 1) / T);
+    const int count = per_unit ? nb : static_cast<int>(((u_a + nb) * N - 1) / T) - k_first + 1;
     float M[kMaxItems], den[kMaxItems];
     f32x4 acc[kMaxItems];
 #pragma unroll
@@ -364,26 +370,33 @@ __device__ void combine_segment(const DecodeArgs& a, int b, int g, const SegWave
         den[it] = 0.f;
         acc[it] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    for (int k = sw.k_first; k <= sw.k_last; ++k) {
-        if (static_cast<int64_t>(k) * T / N == static_cast<int64_t>(k + 1) * T / N) continue;
-        const int64_t slot = (static_cast<int64_t>(k) + sseg) * gw + w;
-        const float* pml = a.part_ml + slot * 2 * a.group;
-        float mk[kMaxItems], lk[kMaxItems];
-        f32x4 ok[kMaxItems];
+    for (int i0 = 0; i0 < count; i0 += kBatch) {
+        float mk[kBatch][kMaxItems], lk[kBatch][kMaxItems];
+        f32x4 ok[kBatch][kMaxItems];
 #pragma unroll
-        for (int it = 0; it < kMaxItems; ++it) {
-            const int idx = it * kWave + lane;
-            if (idx < items) {
-                const int h = idx / kQuads, quad = idx % kQuads;
-                const float* po = a.part_o + (slot * a.group + h) * D + 4 * quad;
-                mk[it] = pr.load1(pml + h);
-                lk[it] = pr.load1(pml + a.group + h);
-                ok[it] = pr.load4(po);
+        for (int j = 0; j < kBatch; ++j) {
+            const int i = i0 + j < count ? i0 + j : count - 1;  // past the end: reload the last, unused
+            const int k = per_unit ? static_cast<int>(((u_a + i + 1) * N - 1) / T) : k_first + i;
+            const int64_t slot = (static_cast<int64_t>(k) + sseg) * gw + w;
+            const float* pml = a.part_ml + slot * 2 * a.group;
+#pragma unroll
+            for (int it = 0; it < kMaxItems; ++it) {
+                const int idx = it * kWave + lane;
+                if (idx < items) {
+                    const int h = idx / kQuads, quad = idx % kQuads;
+                    mk[j][it] = pr.load1(pml + h);
+                    lk[j][it] = pr.load1(pml + a.group + h);
+                    ok[j][it] = pr.load4(a.part_o + (slot * a.group + h) * D + 4 * quad);
+                }
             }
         }
 #pragma unroll
-        for (int it = 0; it < kMaxItems; ++it)
-            if (it * kWave + lane < items) lse_merge(M[it], den[it], acc[it], mk[it], lk[it], ok[it]);
+        for (int j = 0; j < kBatch; ++j)
+            if (i0 + j < count)
+#pragma unroll
+                for (int it = 0; it < kMaxItems; ++it)
+                    if (it * kWave + lane < items)
+                        lse_merge(M[it], den[it], acc[it], mk[j][it], lk[j][it], ok[j][it]);
     }
     const int32_t len = a.seq_lens[b];
     const bool invalid = static_cast<int64_t>(len) > kPageTokens * a.pt_stride;
@@ -462,8 +475,8 @@ __device__ __forceinline__ int load_ids(const int32_t* __restrict__ row, int fir
 // R page buffers form a ring: while one page is computed, the next R - 1 are
 // in flight.
 template <int D, bool BF16, int R, bool TIERED>
-__device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_len, int lane,
-                          int64_t seg_first_unit, int64_t total_units) {
+__device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_len, bool row_invalid,
+                          int lane, int64_t seg_first_unit, int64_t total_units) {
     using S = Shape<D, BF16>;
     const int h = lane & 15, qg = lane >> 4;
     const bool hvalid = h < a.group;
@@ -538,6 +551,19 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
 
     float l = wave_sum_4(st.l);
     if (bad) l = __builtin_nanf("");
+    if (pc.p0 == 0 && pc.p1 == nb) {
+        // The piece is the whole segment: its normalised result is the output.
+        // (o + 0) / l is what merging this one partial gives, bit for bit.
+        if (hvalid) {
+            const float nan = __builtin_nanf("");
+            const int64_t orow = (static_cast<int64_t>(pc.b) * a.num_q_heads + pc.g * a.group + h) * D + 4 * qg;
+#pragma unroll
+            for (int c = 0; c < S::kChunks; ++c)
+                store_quad<D, BF16>(a, orow + 16 * c,
+                                    row_invalid ? f32x4{nan, nan, nan, nan} : (st.o[c] + 0.f) / l);
+        }
+        return;
+    }
     if (hvalid) {
         float* po = a.part_o + (static_cast<int64_t>(pc.slot) * a.group + h) * D + 4 * qg;
         float* pml = a.part_ml + static_cast<int64_t>(pc.slot) * 2 * a.group;
@@ -570,7 +596,7 @@ __device__ void run_piece(const DecodeArgs& a, const Piece& pc, int nb, int seq_
         if (lane == 0) prev = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         prev = __builtin_amdgcn_readfirstlane(__shfl(prev, 0));
         if (prev + 1 == sw.pieces) {
-            combine_segment<D, BF16>(a, pc.b, pc.g, sw, total_units, lane);
+            combine_segment<D, BF16>(a, pc.b, pc.g, seg_first_unit, nb, total_units, lane);
             if (lane == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // next call
         }
     }
@@ -709,8 +735,8 @@ __device__ __forceinline__ void compute_page_valu(ValuState<D>& st, PageRegs<D, 
 }
 
 template <int D, int R, bool TIERED>
-__device__ void run_piece_valu(const DecodeArgs& a, const Piece& pc, int nb, int seq_len, int lane,
-                               ValuLds<D>& sm) {
+__device__ void run_piece_valu(const DecodeArgs& a, const Piece& pc, int nb, int seq_len, bool row_invalid,
+                               int lane, ValuLds<D>& sm) {
     using S = Shape<D, true>;
     constexpr int kGroups = D / 8;
     // the group's queries (zero beyond `group` heads) into LDS
@@ -813,6 +839,22 @@ __device__ void run_piece_valu(const DecodeArgs& a, const Piece& pc, int nb, int
 #pragma unroll
         for (int e = 0; e < 2; ++e) l[e] += __shfl_xor(l[e], o);
     const int dl = lane & 15;
+    if (pc.p0 == 0 && pc.p1 == nb) {
+        // the whole segment: write its output (what merging one partial gives)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int h = 2 * qg + e;
+            if (h < a.group) {
+                const float den = bad ? __builtin_nanf("") : l[e];
+                __bf16* orow = static_cast<__bf16*>(a.out) +
+                               (static_cast<int64_t>(pc.b) * a.num_q_heads + pc.g * a.group + h) * D + dl;
+#pragma unroll
+                for (int c = 0; c < S::kChunks; ++c)
+                    orow[16 * c] = static_cast<__bf16>(row_invalid ? __builtin_nanf("") : (o2[e][c] + 0.f) / den);
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
         const int h = 2 * qg + e;
@@ -850,24 +892,27 @@ __attribute__((amdgpu_waves_per_eu(HCK_SPLIT_WAVES_PER_EU))) void decode_split_k
     const int gw = a.group_waves;
     const int heads = a.num_kv_heads / gw;
     const int worker = wave / gw, w_in = wave % gw;
-    if (a.fused) {
-        // rows with no pages get no partials: write them here (0 for L = 0, NaN for L < 0)
-        for (int seg = wave; seg < a.batch * a.num_kv_heads; seg += a.waves) {
-            const int b = seg / a.num_kv_heads;
-            const int32_t len = a.seq_lens[b];
-            if (len <= 0)
-                fill_segment<D, BF16>(a, b, seg % a.num_kv_heads, len == 0 ? 0.f : __builtin_nanf(""), lane);
-        }
+    // rows with no pages get no pieces: write them here (0 for L = 0, NaN for L < 0)
+    for (int seg = wave; seg < a.batch * a.num_kv_heads; seg += a.waves) {
+        const int b = seg / a.num_kv_heads;
+        const int32_t len = a.seq_lens[b];
+        if (len <= 0)
+            fill_segment<D, BF16>(a, b, seg % a.num_kv_heads, len == 0 ? 0.f : __builtin_nanf(""), lane);
     }
     const int64_t total = static_cast<int64_t>(lds_uniform(s_pref + a.batch)) * heads;
     int64_t u, u1;
     wave_units(total, worker, a.waves / gw, u, u1);
+    // the segment (row, head group) whose first piece this worker holds and
+    // whose other pieces belong to later workers: the combine merges it
+    int32_t split_seg = -1;
     while (u < u1) {
         Piece pc = piece_at<true>(s_pref, a.batch, heads, worker, u, u1);
         if (pc.p1 <= pc.p0) break;  // cannot happen for a consistent prefix; never spin
         const int nb = lds_uniform(s_pref + pc.b + 1) - lds_uniform(s_pref + pc.b);
         const int32_t len = a.seq_lens[pc.b];
         const int seq_len = len < kPageTokens * nb ? len : kPageTokens * nb;
+        const bool row_invalid = static_cast<int64_t>(len) > kPageTokens * a.pt_stride;
+        if (pc.p0 == 0 && pc.p1 < nb) split_seg = pc.b * heads + pc.g;
         const int64_t seg_first = static_cast<int64_t>(lds_uniform(s_pref + pc.b)) * heads +
                                   static_cast<int64_t>(pc.g) * nb;
         const int span = pc.p1 - pc.p0;
@@ -875,12 +920,13 @@ __attribute__((amdgpu_waves_per_eu(HCK_SPLIT_WAVES_PER_EU))) void decode_split_k
         pc.slot = pc.slot * gw + w_in;
         if constexpr (VALU) {
             __shared__ ValuLds<D> s_valu[kSplitBlockWaves];
-            run_piece_valu<D, R, TIERED>(a, pc, nb, seq_len, lane, s_valu[threadIdx.x / kWave]);
+            run_piece_valu<D, R, TIERED>(a, pc, nb, seq_len, row_invalid, lane, s_valu[threadIdx.x / kWave]);
         } else {
-            run_piece<D, BF16, R, TIERED>(a, pc, nb, seq_len, lane, seg_first, total);
+            run_piece<D, BF16, R, TIERED>(a, pc, nb, seq_len, row_invalid, lane, seg_first, total);
         }
         u += span;
     }
+    if (!a.fused && w_in == 0 && lane == 0) a.split_segs[worker] = split_seg;
 }
 
 // Merge the partials of one (b, g) for one query head and write its output row.
@@ -890,7 +936,10 @@ __attribute__((amdgpu_waves_per_eu(HCK_SPLIT_WAVES_PER_EU))) void decode_split_k
 // (many partials per segment, i.e. small batches): the block's four waves share
 // one (b, g, h) and merge their results through LDS.  The partials of a segment
 // are those of workers k_first..k_last when there are fewer workers than units,
-// and one per unit (the worker that owns it) otherwise.
+// and one per unit (the worker that owns it) otherwise.  Only segments split
+// over several workers have partials (the split writes the others' output
+// itself): the grid walks either all segments, skipping the rest, or, when
+// workers are fewer than segments, the workers' split-segment entries.
 #ifndef HCK_WIDE_COMBINE_PIECES
 #define HCK_WIDE_COMBINE_PIECES 12
 #endif
@@ -903,11 +952,25 @@ __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArg
     constexpr int kUnroll = 4;
     constexpr int kStride = WIDE ? kBlockWaves * kGroups : kGroups;
     __shared__ float s_merge[WIDE ? kBlockWaves : 1][kQuads][6];
-    const int seg = blockIdx.x;
     const int wave = threadIdx.x / kWave;
-    const int h = WIDE ? static_cast<int>(blockIdx.y) : static_cast<int>(blockIdx.y) * kBlockWaves + wave;
+    const int Lw = a.group_waves;
+    const int heads = a.num_kv_heads / Lw;
+    int b, g, hy;
+    if (a.combine_by_worker) {
+        // blockIdx.x: a worker; blockIdx.y: (KV head within the head group, head block)
+        const int32_t e = a.split_segs[blockIdx.x];
+        if (e < 0) return;  // whole block
+        const int ny = WIDE ? a.group : (a.group + kBlockWaves - 1) / kBlockWaves;
+        b = e / heads;
+        g = (e % heads) * Lw + static_cast<int>(blockIdx.y) / ny;
+        hy = static_cast<int>(blockIdx.y) % ny;
+    } else {
+        b = static_cast<int>(blockIdx.x) / a.num_kv_heads;
+        g = static_cast<int>(blockIdx.x) % a.num_kv_heads;
+        hy = static_cast<int>(blockIdx.y);
+    }
+    const int h = WIDE ? hy : hy * kBlockWaves + wave;
     if (h >= a.group) return;  // never taken by a wide block: its grid has one block per head
-    const int b = seg / a.num_kv_heads, g = seg % a.num_kv_heads;
     const int lane = threadIdx.x & (kWave - 1);
     const int quad = lane % kQuads, grp = lane / kQuads;
     const int gid = WIDE ? wave * kGroups + grp : grp;
@@ -915,25 +978,27 @@ __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArg
     // pages of the rows before b, and of all rows (the split kernel's prefix)
     const int64_t before = a.row_pref[b], total = a.row_pref[a.batch];
     const int32_t len = a.seq_lens[b];
-    const bool invalid = len < 0 || static_cast<int64_t>(len) > kPageTokens * a.pt_stride;
     const int nb = row_pages(len, a.pt_stride);
+    // The split wrote rows with no pages and segments it did not split
+    // (uniform over the block: a wide block holds one segment).
+    if (nb == 0) return;
+    const bool invalid = static_cast<int64_t>(len) > kPageTokens * a.pt_stride;
     // units of head group g / Lw over the workers' ranges; this head's partials
     // are slot (worker + b * heads + g / Lw) * Lw + g % Lw
-    const int Lw = a.group_waves;
-    const int heads = a.num_kv_heads / Lw;
     const int64_t sseg = static_cast<int64_t>(b) * heads + g / Lw;
     const int w_in = g % Lw;
+    const int64_t T = total * heads;
+    const int64_t u_a = before * heads + static_cast<int64_t>(g / Lw) * nb;
+    const int N = a.waves / Lw;
+    const int k_first = static_cast<int>(((u_a + 1) * N - 1) / T);
+    const int k_last = static_cast<int>(((u_a + nb) * N - 1) / T);
+    const bool per_unit = N > T;  // every non-empty wave holds exactly one unit
+    const int count = per_unit ? nb : k_last - k_first + 1;
+    if (count == 1) return;
     f32x4 res;
     float M = -INFINITY, den = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    if (!invalid && nb > 0) {
-        const int64_t T = total * heads;
-        const int64_t u_a = before * heads + static_cast<int64_t>(g / Lw) * nb;
-        const int N = a.waves / Lw;
-        const int k_first = static_cast<int>(((u_a + 1) * N - 1) / T);
-        const int k_last = static_cast<int>(((u_a + nb) * N - 1) / T);
-        const bool per_unit = N > T;  // every non-empty wave holds exactly one unit
-        const int count = per_unit ? nb : k_last - k_first + 1;
+    if (!invalid) {
         for (int i0 = gid; i0 < count; i0 += kUnroll * kStride) {
             float mk[kUnroll], lk[kUnroll];
             f32x4 ok[kUnroll];
@@ -985,8 +1050,6 @@ __global__ __launch_bounds__(kBlockThreads) void decode_combine_kernel(DecodeArg
     if (invalid) {
         const float nan = __builtin_nanf("");
         res = f32x4{nan, nan, nan, nan};
-    } else if (nb == 0) {
-        res = f32x4{0.f, 0.f, 0.f, 0.f};
     } else {
         res = acc / den;
     }
@@ -1077,10 +1140,17 @@ hipError_t launch_decode_combine(const DecodeArgs& a, int head_dim, int dtype, h
     const bool wide = static_cast<int64_t>(a.waves) >= static_cast<int64_t>(kWideCombinePieces) * segs;
     const void* k = pick_combine(head_dim, dtype, wide);
     if (!k) return hipErrorInvalidValue;
-    void* args[] = {const_cast<DecodeArgs*>(&a)};
-    const unsigned y = wide ? static_cast<unsigned>(a.group)
-                            : static_cast<unsigned>((a.group + kBlockWaves - 1) / kBlockWaves);
-    return launch_kernel(k, dim3(segs, y), dim3(kBlockThreads), args, 0, s, ev);
+    const unsigned ny = wide ? static_cast<unsigned>(a.group)
+                             : static_cast<unsigned>((a.group + kBlockWaves - 1) / kBlockWaves);
+    // Walk the workers' split-segment entries when they are fewer than the
+    // segments (many short rows): each worker starts at most one split segment.
+    DecodeArgs c = a;
+    c.combine_by_worker = a.waves < segs ? 1 : 0;
+    void* args[] = {&c};
+    const dim3 grid = c.combine_by_worker
+                          ? dim3(static_cast<unsigned>(a.waves / a.group_waves), ny * a.group_waves)
+                          : dim3(static_cast<unsigned>(segs), ny);
+    return launch_kernel(k, grid, dim3(kBlockThreads), args, 0, s, ev);
 }
 
 int decode_split_blocks_per_cu(int head_dim, int dtype, int batch) {

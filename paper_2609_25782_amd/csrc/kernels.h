@@ -55,6 +55,10 @@ struct DecodeArgs {
     float* part_o;            // [slots][group][head_dim] unnormalised partial outputs
     float* part_ml;           // [slots][2][group] running max (log2 domain) and weight sum
     int32_t* row_pref;        // [batch + 1] pages before each row (written by the split, read by the combine)
+    int32_t* split_segs;      // [waves / group_waves] per worker, the segment (b * heads + head group)
+                              // whose first piece it holds while later workers hold the rest, or -1
+                              // (written by a separate-merge split, read by the combine)
+    int32_t combine_by_worker;  // set by the combine launch: its grid walks split_segs, not all segments
     void* out;                // [batch][num_q_heads][head_dim]
     int32_t* counters;        // [batch * num_kv_heads] arrival counters, zero between calls
     int32_t fused;            // 1: the last wave of each (b, g) merges its partials
@@ -108,9 +112,11 @@ inline size_t decode_partials_bytes(int64_t slots, int group, int head_dim) {
 }
 
 // Decode workspace: the partials, then the row page prefix (batch + 1 int32),
-// rounded up to 256 bytes.
-inline size_t decode_workspace_bytes(int64_t slots, int group, int head_dim, int batch) {
-    const size_t n = decode_partials_bytes(slots, group, head_dim) + (static_cast<size_t>(batch) + 1) * 4;
+// then one split-segment entry per worker (at most `waves` int32), rounded up
+// to 256 bytes.
+inline size_t decode_workspace_bytes(int64_t slots, int group, int head_dim, int batch, int waves) {
+    const size_t n = decode_partials_bytes(slots, group, head_dim) +
+                     (static_cast<size_t>(batch) + 1 + static_cast<size_t>(waves)) * 4;
     return (n + 255) & ~static_cast<size_t>(255);
 }
 

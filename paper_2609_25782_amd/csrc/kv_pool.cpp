@@ -1491,9 +1491,9 @@ size_t paged_decode_workspace_bytes(const kv_pool* pool, int32_t batch, int32_t 
         return 0;
     const int32_t group = num_q_heads / pool->d.num_kv_heads;
     DeviceGuard g(pool->d.device);
-    const int64_t slots = static_cast<int64_t>(pool->decode_waves()) +
-                          static_cast<int64_t>(batch) * pool->d.num_kv_heads;
-    return hck::decode_workspace_bytes(slots, group, pool->d.head_dim, batch);
+    const int32_t waves = pool->decode_waves();
+    const int64_t slots = static_cast<int64_t>(waves) + static_cast<int64_t>(batch) * pool->d.num_kv_heads;
+    return hck::decode_workspace_bytes(slots, group, pool->d.head_dim, batch, waves);
 }
 
 int paged_decode_attention(kv_pool* pool, int32_t layer, const void* q, const int32_t* page_table,
@@ -1549,7 +1549,7 @@ int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page
     DeviceGuard g(pool->d.device);
     const int32_t waves = pool->decode_waves();
     const int64_t slots = static_cast<int64_t>(waves) + static_cast<int64_t>(batch) * pool->d.num_kv_heads;
-    const size_t need = hck::decode_workspace_bytes(slots, group, pool->d.head_dim, batch);
+    const size_t need = hck::decode_workspace_bytes(slots, group, pool->d.head_dim, batch, waves);
     if (ws_bytes < need) {
         if (no_alloc)
             return fail(KV_ERR_INVALID, "this batch needs %zu bytes of decode scratch; the no-allocation "
@@ -1575,6 +1575,8 @@ int decode_impl(kv_pool* pool, int32_t layer, const void* q, const int32_t* page
     a.part_ml = a.part_o + slots * group * pool->d.head_dim;
     a.row_pref = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) +
                                             hck::decode_partials_bytes(slots, group, pool->d.head_dim));
+    a.split_segs = a.row_pref + batch + 1;
+    a.combine_by_worker = 0;
     a.out = out;
     a.counters = pool->counters;
     a.fused = pool->combine_mode == KV_COMBINE_FUSED ? 1 : 0;

@@ -100,6 +100,36 @@ def test_split_invariance_two_head_groups(dev, waves, fused):
     tolerance_check(got, case.oracle_out())
 
 
+@pytest.mark.parametrize("fused", [True, False])
+@pytest.mark.parametrize("waves", [3, 4, 8, 64, 256])
+def test_every_row_written_many_short_rows(dev, waves, fused):
+    """96 short rows, two of them empty, and fewer waves than (row, KV head)
+    segments: most segments sit whole in one piece, whose wave writes the
+    output itself, a few are cut between workers and merged by the combine,
+    whose grid then walks the workers' split-segment entries.  The output starts
+    as NaN: every row must be written, the empty ones as zeros, the rest within
+    the oracle's tolerance."""
+    rng = np.random.default_rng(23)
+    lens = [int(x) for x in rng.integers(1, 400, size=96)]
+    lens[5] = lens[40] = 0
+    case = Case(1, 16, 4, 128, "bf16", lens, seed=23)
+    pool = build_gpu(case, dev)
+    pool.set_waves(waves)
+    pool.set_combine(fused)
+    _say("short rows: waves=%d fused=%s" % (waves, fused))
+    q = to_device(case.q, "bf16", dev)
+    sl = torch.tensor(lens, dtype=torch.int32, device=dev)
+    out = torch.full((len(lens), 16, 128), float("nan"), dtype=torch.bfloat16, device=dev)
+    pool.decode(0, q, sl, out=out)
+    torch.cuda.synchronize()
+    got = to_host(out)
+    pool.close()
+    assert not np.isnan(got).any()
+    assert np.all(got[[5, 40]] == 0)
+    rows = [b for b in range(len(lens)) if lens[b] > 0]
+    tolerance_check(got[rows], case.oracle_out(rows=rows))
+
+
 @pytest.mark.parametrize("dtype,D,hq,hkv", [("bf16", 128, 32, 4), ("f32", 64, 16, 1), ("bf16", 64, 16, 1)])
 def test_separate_combine(dev, dtype, D, hq, hkv):
     case = Case(1, hq, hkv, D, dtype, [1, 15, 16, 17, 100, 3000, 250], seed=16)
