@@ -1210,7 +1210,7 @@ def main():
                     help="write a scratch buffer of this many MiB before every timed step, so the "
                          "decode starts with the 256 MB Infinity Cache and the L2s holding other data")
     ap.add_argument("--full-json", default="", help="also write the full result (every sweep row) here")
-    ap.add_argument("--only-config", default="", choices=["", "tiny", "step48", "skewed", "prompt_write"],
+    ap.add_argument("--only-config", default="", choices=["", "tiny", "step48", "skewed", "prompt_write", "evict48"],
                     help="profiling aid: time only this workload's decode (no hot-path step) and print "
                          "its figures")
     args = ap.parse_args()
@@ -1234,6 +1234,9 @@ def main():
     dev = torch.device("cuda", 0)
     if args.only_config == "prompt_write":
         print(json.dumps(measure_prompt_write(args.seed, reps=args.steps)), flush=True)
+        return
+    if args.only_config == "evict48":
+        print(json.dumps(measure_evict(args.seed, reps=args.steps)), flush=True)
         return
     if args.only_config:
         print(json.dumps(measure_configs(args.seed, steps=args.steps, warmup=args.warmup,
