@@ -147,11 +147,17 @@ def test_layer_shape_scaled_values(dev):
     _say("layer shape scaled: abs %.3g norm %.3g" % (err, norm))
 
 
+@pytest.mark.parametrize("waves", [0, 1, 4])
 @pytest.mark.parametrize("fused", [True, False])
-def test_zero_and_invalid_lengths(dev, fused):
+def test_zero_and_invalid_lengths(dev, fused, waves):
+    """Zero, negative and over-long lengths.  With one wave every segment is
+    one piece, so the split writes the NaN rows itself; with four, some
+    segments are cut between waves; with the default grid every page is a
+    piece of its own."""
     case = Case(1, 8, 2, 64, "bf16", [40, 0, 70], seed=7)
     pool = build_gpu(case, dev)
     pool.set_combine(fused)
+    pool.set_waves(waves)
     q = to_device(case.q, "bf16", dev)
     sl = torch.tensor([40, 0, 70], dtype=torch.int32, device=dev)
     out = to_host(pool.decode(0, q, sl))
@@ -163,7 +169,12 @@ def test_zero_and_invalid_lengths(dev, fused):
     out2 = to_host(pool.decode(0, q, bad))
     torch.cuda.synchronize()
     assert np.all(np.isnan(out2[1])) and np.all(np.isnan(out2[2]))
-    assert np.array_equal(out2[0], out[0])
+    if waves == 4:
+        # the longer row 2 moves the boundaries between the waves' ranges, so row
+        # 0 is cut differently: equal to the oracle, not bit for bit to the first call
+        tolerance_check(out2[[0]], case.oracle_out(rows=[0]))
+    else:
+        assert np.array_equal(out2[0], out[0])
     # the next call is clean again (the fused merge's counters reset themselves)
     out3 = to_host(pool.decode(0, q, sl))
     torch.cuda.synchronize()
@@ -171,11 +182,13 @@ def test_zero_and_invalid_lengths(dev, fused):
     pool.close()
 
 
+@pytest.mark.parametrize("waves", [0, 1, 4])
 @pytest.mark.parametrize("fused", [True, False])
-def test_out_of_range_page_id_gives_nan(dev, fused):
+def test_out_of_range_page_id_gives_nan(dev, fused, waves):
     case = Case(1, 8, 2, 64, "bf16", [40, 70], seed=8)
     pool = build_gpu(case, dev)
     pool.set_combine(fused)
+    pool.set_waves(waves)
     q = to_device(case.q, "bf16", dev)
     sl = torch.tensor(case.seq_lens, dtype=torch.int32, device=dev)
     pt = pool.page_table[:2].clone()
