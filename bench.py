@@ -1127,6 +1127,10 @@ def measure_spill(seed: int, steps: int = 6, warmup: int = 2):
     kv_bytes = 48 * sum(decode_bytes([L] * n_s, hq, 4, 128, 2))
     rows = []
     copy_stream = torch.cuda.Stream()
+    # the gather on 8 CUs (one per XCD) and the decode on the other 248, so the
+    # gather's waves, which wait on PCIe, never share a CU with the decode
+    from paper_2609_25782_amd.pool import split_streams
+    dec_cu, copy_cu = split_streams(1)
     # The host tier's small fractions look for the prefetch crossover: one
     # layer's gather of f x 269 MB over PCIe (about f x 4.8 ms) fits under one
     # layer's decode (about 55 us) only for f below about 1%.
@@ -1150,21 +1154,25 @@ def measure_spill(seed: int, steps: int = 6, warmup: int = 2):
                 table = torch.empty((n_s, pool.stride), dtype=torch.int32, device="cuda")
                 kv.paged_decode_stage(pool.handle, list(range(n_s)), table.data_ptr())
             torch.cuda.synchronize()
-            for mode in (("direct", "prefetch") if spilled else ("hot", "hot_tiered_kernel")):
+            for mode in (("direct", "prefetch", "prefetch_cu8") if spilled else ("hot", "hot_tiered_kernel")):
                 # all pages hot: the plain kernel, then the tier-aware one (spill on)
                 kv.kv_pool_set_spill(pool.handle, mode != "hot")
+                pre = mode.startswith("prefetch")
+                dec_stream = dec_cu.stream if mode == "prefetch_cu8" else torch.cuda.current_stream()
+                cpy = copy_cu.stream if mode == "prefetch_cu8" else copy_stream
                 times = []
                 for it in range(warmup + steps):
                     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    t0.record()
-                    if mode == "prefetch":
-                        copy_stream.wait_event(t0)
-                        kv.paged_decode_prefetch(pool.handle, 0, copy_stream.cuda_stream)
+                    t0.record(dec_stream)
+                    if pre:
+                        cpy.wait_event(t0)
+                        kv.paged_decode_prefetch(pool.handle, 0, cpy.cuda_stream)
                     for layer in range(48):
-                        if mode == "prefetch" and layer + 1 < 48:
-                            kv.paged_decode_prefetch(pool.handle, layer + 1, copy_stream.cuda_stream)
-                        pool.decode(layer, q, sl, page_table=table if mode == "prefetch" else direct, out=out)
-                    t1.record()
+                        if pre and layer + 1 < 48:
+                            kv.paged_decode_prefetch(pool.handle, layer + 1, cpy.cuda_stream)
+                        pool.decode(layer, q, sl, page_table=table if pre else direct, out=out,
+                                    stream=dec_stream if mode == "prefetch_cu8" else None)
+                    t1.record(dec_stream)
                     torch.cuda.synchronize()
                     if it >= warmup:
                         times.append(t0.elapsed_time(t1))
@@ -1177,6 +1185,8 @@ def measure_spill(seed: int, steps: int = 6, warmup: int = 2):
             pool.close()
             del pool, staging, table, direct
             torch.cuda.empty_cache()
+    dec_cu.close()
+    copy_cu.close()
     return {"config": "32 sessions x 4,096 tokens, 48 layers x 4 KV heads x 128 bf16, 32 query heads "
                       "(12 GiB of KV per step)", "kv_bytes_per_step": kv_bytes, "rows": rows}
 

@@ -567,13 +567,16 @@ int paged_decode_gather_table(kv_pool* pool, const int32_t* sids, int32_t n, int
  * layer l + 1 of the batch's spilled pages are gathered from the cold tier into
  * HBM, and layer l + 1 then reads only HBM.
  *
- * Whether staging pays depends on the cold tier: over device memory it only
- * adds an HBM write and read per spilled byte, and over PCIe reading spilled
- * pages in place (spill on, no staging) measured faster at every spilled share
- * tried (0.25-100% of a 48-layer step's pages), because in-kernel reads overlap
- * PCIe with the other waves' HBM reads while staging adds a launch and a
- * cross-stream wait per layer.  It is for capacity tiers whose access latency
- * a layer's decode can hide and in-kernel reads cannot.
+ * Whether staging pays depends on the cold tier and on the share of spilled
+ * pages.  Over device memory it only adds an HBM write and read per spilled
+ * byte.  Over PCIe it pays when one layer's spilled slices cross PCIe within
+ * one layer's decode (about 0.5-1% of a 48-layer step's pages at 32 x 4K
+ * tokens: 8% faster than reading them in place), provided the gather runs on
+ * a stream confined to a few CUs and the decode on a stream over the others
+ * (kv_stream_create_cu_slots): gather waves that wait on PCIe must not share
+ * CUs with the decode.  Below that window the per-layer cross-stream wait
+ * costs more than the cold reads; above it both paths are PCIe-bound and
+ * reading in place is faster.
  *
  * kv_pool_set_staging gives the pool a device buffer for this (256-byte
  * aligned; NULL or 0 bytes removes it).  It holds two halves (even and odd

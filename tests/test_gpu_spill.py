@@ -244,6 +244,41 @@ def test_decode_through_prefetched_staging(dev, cold, slots, dtype, d):
     pool.close()
 
 
+@pytest.mark.parametrize("cold", ["host", "device"])
+def test_prefetch_on_cu_confined_streams(dev, cold):
+    """The measured arrangement for a PCIe tier: the gather on a stream with one
+    CU per XCD, the decode on a stream over the other CUs; results match the
+    oracle, layer after layer, for two steps."""
+    from paper_2609_25782_amd import hotcold_kv as kv
+    from paper_2609_25782_amd.pool import split_streams
+    _say("prefetch on CU-confined streams, cold tier in %s memory" % cold)
+    pool = _spilled_pool(dev, cold, LENS, hot_pages=30)
+    slice_bytes = 2 * 2 * 16 * 128 * 2
+    staging = torch.empty(2 * 64 * slice_bytes, dtype=torch.uint8, device=dev)
+    kv.kv_pool_set_staging(pool.handle, staging.data_ptr(), staging.numel())
+    table = torch.empty((len(LENS), pool.stride), dtype=torch.int32, device=dev)
+    assert kv.paged_decode_stage(pool.handle, list(range(len(LENS))), table.data_ptr()) > 0
+    sl = torch.tensor(LENS, dtype=torch.int32, device=dev)
+    dec, cpy = split_streams(1)
+    cases = [_oracle(LENS, layer) for layer in (0, 1)]
+    qs = [to_device(c.q, "bf16", dev) for c in cases]
+    torch.cuda.synchronize()
+    for step in range(2):
+        kv.paged_decode_prefetch(pool.handle, 0, cpy.handle)
+        outs = []
+        for layer in (0, 1):
+            if layer + 1 < 2:
+                kv.paged_decode_prefetch(pool.handle, layer + 1, cpy.handle)
+            outs.append(pool.decode(layer, qs[layer], sl, page_table=table, stream=dec.stream))
+        torch.cuda.synchronize()
+        for layer in (0, 1):
+            tolerance_check(to_host(outs[layer]), cases[layer].oracle_out())
+    kv.kv_pool_set_staging(pool.handle, 0, 0)
+    pool.close()
+    dec.close()
+    cpy.close()
+
+
 def test_promote_and_write_into_spilled_pages(dev):
     """Tokens written into spilled pages land in the cold tier; after the other
     session is evicted, promotion copies spilled pages into the freed hot pages
