@@ -74,7 +74,8 @@ def test_layer_config_full_size(dev):
     oracle; then poison of every tail slot past each row's length and of every
     free hot page (bitwise equal to the clean run); then needles at the last token
     of the longest row and at a mid-row page start of another (O(1) outputs that
-    catch any page-table or offset slip), every row against the oracle again."""
+    catch any page-table or offset slip), every row against the oracle again;
+    then the same call with the fused merge and with the vector-ALU split."""
     from paper_2609_25782_amd.pool import HotColdPool
     w = synth.config_layer(0)
     headroom = 8 * synth.pages_for(32768)
@@ -135,6 +136,16 @@ def test_layer_config_full_size(dev):
     _all_rows(w, got, 0, q_np, kv_override=override)
     same = [b for b in range(w.batch) if b not in override]
     assert np.array_equal(got[same], to_host(clean)[same])
+    # the fused merge and the vector-ALU products, at the same full size
+    for name, fused, vector in (("fused merge", True, False), ("vector-ALU split", False, True)):
+        pool.set_combine(fused)
+        pool.set_compute(vector)
+        other = to_host(pool.decode(0, q, sl, page_table=pt))
+        torch.cuda.synchronize()
+        _say("  %s:" % name)
+        _all_rows(w, other, 0, q_np, kv_override=override)
+    pool.set_combine(False)
+    pool.set_compute(False)
     pool.close()
     del pool
     _free()
