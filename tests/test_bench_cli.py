@@ -78,7 +78,7 @@ def _fake_result():
         "spill_decode": {"config": "s" * 100, "rows": [{"cold_tier": "host", "spilled_frac": f, "mode": m,
                                                         "step_ms": 1.0, "GBps": 2.0}
                                                        for f in (0.0025, 0.005, 0.01, 0.02, 0.04, 0.25, 0.5, 1.0)
-                                                       for m in ("direct", "prefetch")] * 2},
+                                                       for m in ("direct", "prefetch", "prefetch_cu8")] * 2},
         "configs": {n: {"us_per_call": {"median": 1.0, "p10": 1.0, "p90": 1.0}, "GBps": 1.0, "pct_of_peak": 1.0,
                         "workload": "w" * 40} for n in ("tiny", "step48", "skewed")}
         | {"graph_step48": [row] * 6,
@@ -100,5 +100,5 @@ def test_stdout_line_stays_short_and_keeps_the_headline_fields():
         assert out[k] == full[k]
     assert out["resume48"]["ms_per_session"] == 2.5
     assert out["configs"]["step48"]["GBps"] == 1.0
-    assert len(out["spill_decode_step_ms"]) == 16
+    assert len(out["spill_decode_step_ms"]) == 24
     assert out["configs"]["append"]["graph_append_ms_per_step"] == 0.05
