@@ -151,6 +151,47 @@ def test_layer_config_full_size(dev):
     _free()
 
 
+@pytest.mark.timeout(600)
+def test_layer_config_round_trip_relocates_bitwise(dev):
+    """The headline layer workload (B=32, L ~ U[8192, 32768], pages scattered at
+    random) in the benchmark's launch configuration: evict 8 sessions to the cold
+    tier and resume them, which puts them on the lowest free hot pages, not their
+    old ones.  Every resumed page holds the bytes its session's page held before
+    the eviction, and the whole batch decodes bit for bit as before."""
+    from paper_2609_25782_amd.pool import HotColdPool
+    w = synth.config_layer(0)
+    headroom = 8 * synth.pages_for(32768)
+    num_hot = w.hot_pages + headroom
+    movers = [int(b) for b in np.argsort(w.seq_lens)[-8:]]  # the 8 longest rows
+    n_cold = sum(synth.pages_for(int(w.seq_lens[b])) for b in movers)
+    pool = HotColdPool(1, 4, 128, "bf16", num_hot, n_cold, w.batch, synth.pages_for(32768))
+    mult = float(synth.value_multiplier(w.value_scale))
+    for b in range(w.batch):
+        assert pool.create_session(int(w.seq_lens[b]), [int(p) for p in w.placement[b]]) == b
+        pool.fill_synthetic(b, b, w.seed, mult)
+    q = _q(synth.queries(w.seed + 1, w.batch, 32, 128, w.value_scale, "bf16"), dev)
+    sl = torch.from_numpy(w.seq_lens.copy()).to(dev)
+    before_rows = pool.page_table[movers].clone()
+    lens = [synth.pages_for(int(w.seq_lens[b])) for b in movers]
+    saved = [pool.hot_page_bytes(before_rows[j, :n].long()).clone() for j, n in enumerate(lens)]
+    before = pool.decode(0, q, sl, page_table=pool.page_table[:w.batch]).clone()
+    pool.evict(movers)
+    pool.resume(movers)
+    torch.cuda.synchronize()
+    after_rows = pool.page_table[movers]
+    moved = int((after_rows != before_rows).sum())
+    assert moved > 0
+    after = pool.decode(0, q, sl, page_table=pool.page_table[:w.batch])
+    torch.cuda.synchronize()
+    assert torch.equal(after, before)
+    for j, n in enumerate(lens):
+        assert torch.equal(pool.hot_page_bytes(after_rows[j, :n].long()), saved[j])
+    _say("round trip of %d sessions: %d page-table entries changed; decode bitwise equal" % (len(movers), moved))
+    pool.close()
+    del pool
+    _free()
+
+
 @pytest.mark.timeout(900)
 def test_step48_config_full_size(dev):
     """48 layers, B=64, lognormal lengths (median 24K, cap 64K), ~170 GB hot pool:
