@@ -24,11 +24,15 @@ def dev():
     return torch.device("cuda", 0)
 
 
-@pytest.mark.parametrize("vector", [False, True])
-def test_decode_step_graph_replays_match_eager(dev, vector):
-    """Both forms of the split kernel: matrix cores and the vector ALU."""
+@pytest.mark.parametrize("vector,many", [(False, False), (True, False), (False, True)])
+def test_decode_step_graph_replays_match_eager(dev, vector, many):
+    """Both forms of the split kernel: matrix cores and the vector ALU.  With
+    many short rows (400 rows: more (row, KV head) segments than waves) the
+    merge walks the waves' split-segment entries, which every replay rewrites."""
     from paper_2609_25782_amd.pool import HotColdPool
     layers, lens = 4, [300, 1000, 57, 2000, 16, 777]
+    if many:
+        lens = [int(x) for x in np.random.default_rng(9).integers(1, 600, size=400)]
     n_pages = sum(synth.pages_for(L) for L in lens)
     pool = HotColdPool(layers, 2, 128, "bf16", n_pages + 10, 0, len(lens), synth.pages_for(2100))
     pool.set_compute(vector)
