@@ -572,10 +572,9 @@ int paged_decode_gather_table(kv_pool* pool, const int32_t* sids, int32_t n, int
  * byte.  Over PCIe it pays when one layer's spilled slices cross PCIe well
  * within one layer's decode (about 0.5% of a 48-layer step's pages at 32 x 4K
  * tokens: 4-9% faster than reading them in place; 1% is the edge), provided
- * the gather runs on
- * a stream confined to a few CUs and the decode on a stream over the others
- * (kv_stream_create_cu_slots): gather waves that wait on PCIe must not share
- * CUs with the decode.  Below that window the per-layer cross-stream wait
+ * the gather runs on a stream confined to a few CUs and the decode on a stream
+ * over the others (kv_stream_create_cu_slots): gather waves that wait on PCIe
+ * must not share CUs with the decode.  Below that window the per-layer cross-stream wait
  * costs more than the cold reads; above it both paths are PCIe-bound and
  * reading in place is faster.
  *
